@@ -1,0 +1,188 @@
+/* semkv.h -- C ABI of the SemKV hot path on MI355X (gfx950).
+ *
+ * SemKV (arxiv 2608.28911) keeps every token of the KV cache and gives each
+ * token one of two adjacent fractional precisions by an importance ranking:
+ * the top r fraction of tokens gets L_hi levels, the rest L_lo levels
+ * (Sec. 3.4, Eq. 4-5); K and V of every layer and KV head of a token share the
+ * token's precision (Sec. 3.5, Eq. 7, Fig. 5).  Generated tokens are
+ * quantized block-exactly in 64-token blocks (Sec. 3.7, Alg. 2).  Decoding
+ * attends over the mixed-precision cache.
+ *
+ * Conventions for every call:
+ *  - Pointers named as device pointers are device memory owned by the caller;
+ *    the library never allocates, frees or synchronizes, and enqueues all of
+ *    its work on the stream it is given (a hipStream_t).
+ *  - Arguments are validated on the host before anything is enqueued; a
+ *    failed validation returns a negative status and enqueues nothing.
+ *  - Data errors found on the device (a NaN score, a non-finite K/V value) are
+ *    OR-ed into the caller's device status word (bit 0: NaN score, bit 1:
+ *    non-finite K/V, bit 2: slot index outside [0, T)); read it after the
+ *    stream is synchronized.
+ *  - A semkv_cache is a plain host struct: configuration, device pointers and
+ *    host-side counts.  Calls on one cache must be serialized on one stream.
+ *    Calls on different caches are independent.
+ *  - fp16 means IEEE binary16 stored as 16-bit words; fp32 is IEEE binary32.
+ */
+#ifndef SEMKV_H
+#define SEMKV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+  SEMKV_OK = 0,
+  SEMKV_EINVAL = -1,       /* bad argument: null pointer, bad shape, bad ratio */
+  SEMKV_EUNSUPPORTED = -2, /* level count, group or head size not supported   */
+  SEMKV_ECAPACITY = -3,    /* pool, prompt or tail capacity would be exceeded */
+  SEMKV_ENAN = -4,         /* reserved for status-word reports                */
+  SEMKV_EHIP = -5,         /* a HIP runtime call failed                       */
+  SEMKV_ESTATE = -6        /* call out of order (e.g. commit before append)   */
+};
+
+enum { SEMKV_BASE_AFFINE = 0, SEMKV_BASE_TQ = 1 };
+enum { SEMKV_STATUS_NAN_SCORE = 1, SEMKV_STATUS_NONFINITE_KV = 2, SEMKV_STATUS_BAD_INDEX = 4 };
+
+/* Configuration of one cache.
+ *  base:   SEMKV_BASE_AFFINE -- per group of `group` channels, an asymmetric
+ *          affine quantizer with two fp16 parameters (scale, zero) (Sec. 4.1);
+ *          L_hi, L_lo in {6, 5} (2.585/2.322 bits) or any two of {3,4,5,6}.
+ *          SEMKV_BASE_TQ -- TurboQuant-MSE: random-sign Hadamard rotation and a
+ *          Lloyd-Max codebook of the unit Gaussian, one fp16 scalar (the row
+ *          norm) per row (Sec. 4.9); L_hi, L_lo in {4, 3} (2.0/1.585 bits).
+ *  group:  affine metadata group in {32, 64, 128}; must be 128 for tq.
+ *  r_num/r_den: high-precision fraction r (Eq. 4), 0 <= r <= 1.
+ *  block:  deferred block size B of Alg. 2; must be 64.
+ *  head_dim must be 128, n_q_heads = 4 * n_kv_heads (GQA group of 4).
+ *  max_prompt, max_new: capacity in tokens per sequence. */
+typedef struct semkv_config {
+  int32_t n_layers, n_kv_heads, n_q_heads, head_dim, batch;
+  int32_t base, L_hi, L_lo, group;
+  int32_t r_num, r_den, block;
+  int64_t max_prompt, max_new;
+} semkv_config;
+
+/* Sizes derived from a configuration (all in bytes unless named otherwise).
+ * Storage layout (the packed format):
+ *  pools:  [batch][n_layers][n_kv_heads] units of unit_stride bytes; a unit is
+ *          cap_hi_tiles high-precision records then cap_lo_tiles
+ *          low-precision records.  A record holds 64 token slots:
+ *            K body (tile_bytes)  V body (tile_bytes)  K meta  V meta
+ *          Bodies hold mixed-radix symbols (Sec. 4.1): a symbol packs n codes
+ *          of base L as sum_i c_i L^i in the least number of bits (n = 5, 4,
+ *          3, 5 for L = 3, 4, 5, 6: 8, 8, 7, 13 bits).  A K line is one token
+ *          row (128 channels), a V line one channel column over the 64 slots;
+ *          segment j of a line is its symbols p = j, j+4, j+8, ...; a body is
+ *          segment 0 of every line, then segments 1, 2, 3, LSB-first, zero
+ *          padded to a multiple of 16 bytes.  Meta: affine, per group g and
+ *          slot s, fp16 {scale, zero} at [g][s]; tq, fp16 rho at [s].
+ *          Slots of a pool are in increasing token position, prompt tokens
+ *          first, then each closed generation block.
+ *  tail:   fp16 [batch][n_layers][n_kv_heads][2 (K,V)][64][128], the
+ *          generated tokens not yet quantized (Alg. 2).
+ *  tail_scores: fp32 [batch][64].
+ *  flags:  uint32 [batch][flag_words]: bit i%32 of word i/32 is 1 iff token i
+ *          has the high precision (the 1-bit per-token flag of Sec. 4.1).
+ *  workspace: scratch of semkv_decode_attn. */
+typedef struct semkv_sizes {
+  size_t pool_bytes, tail_bytes, tail_score_bytes, flag_bytes, workspace_bytes;
+  int64_t flag_words, cap_hi_tiles, cap_lo_tiles, unit_stride;
+  int64_t tile_bytes_hi, tile_bytes_lo, meta_bytes, record_bytes_hi, record_bytes_lo;
+} semkv_sizes;
+
+/* One cache.  Filled by semkv_cache_init; the counts are updated by the calls
+ * below and may be read (not written) by the caller. */
+typedef struct semkv_cache {
+  semkv_config cfg;
+  semkv_sizes sz;
+  uint8_t* pools;             /* device */
+  uint16_t* tail;             /* device, fp16 */
+  float* tail_scores;         /* device */
+  uint32_t* flags;            /* device */
+  const uint32_t* tq_signs;   /* device [n_layers][n_kv_heads][4] (tq) or NULL */
+  int32_t* status;            /* device status word */
+  float mu_hi[16], tau_hi[16], mu_lo[16], tau_lo[16];  /* tq codebooks */
+  int64_t n_prompt;           /* prompt tokens quantized (same for every sequence) */
+  int64_t n_hi, n_lo;         /* rows in the high / low pool of every unit */
+  int32_t n_scored;           /* tail rows whose score was committed */
+  uint32_t appended[4];       /* layers that appended the current tail row */
+} semkv_cache;
+
+/* Message for a status code; never NULL. */
+const char* semkv_strerror(int status);
+
+/* Sizes of every buffer for `cfg`; validates the configuration. */
+int semkv_cache_sizes(const semkv_config* cfg, semkv_sizes* out);
+
+/* Lloyd-Max codebook of the unit Gaussian with L levels (2 <= L <= 16),
+ * computed on the host by bisection on the optimality conditions and rounded
+ * to fp32: mu[L] reconstruction points, tau[L-1] thresholds (Sec. 4.9). */
+int semkv_tq_codebook(int L, float* mu, float* tau);
+
+/* Initialize `c` over caller buffers sized by semkv_cache_sizes.  The buffers
+ * need no clearing except `flags` and `status`, which must be zero.
+ * tq_signs: device uint32 [n_layers][n_kv_heads][4]; bit i set = channel i of
+ * that head is negated before the Hadamard transform (tq only, else NULL). */
+int semkv_cache_init(semkv_cache* c, const semkv_config* cfg, void* pools, void* tail,
+                     float* tail_scores, uint32_t* flags, const uint32_t* tq_signs,
+                     int32_t* status);
+
+/* Eq. (4)-(5) for every sequence: K = floor(r T); the K tokens with the
+ * highest scores get the high precision, equal scores ordered by lower token
+ * index, -0 equal to +0.  scores: device fp32 [batch][T].  Writes the flag
+ * bits of tokens [0, T) and the slot lists hi_idx: device int32
+ * [batch][K] (ascending), lo_idx: device int32 [batch][T-K] (ascending); a
+ * list with no entries may be NULL.
+ * A NaN score sets SEMKV_STATUS_NAN_SCORE. */
+int semkv_rank(semkv_cache* c, const float* scores, int64_t T, int32_t* hi_idx,
+               int32_t* lo_idx, hipStream_t stream);
+
+/* Eq. (7) for the prompt (Alg. 1): quantize K and V of token hi_idx[b][i]
+ * (lo_idx[b][i]) with L_hi (L_lo) levels into slot i of the high (low) pool of
+ * every (b, layer, kv head) unit and pack them.  K, V: device fp16; element
+ * (b, h, t, d) at b*sB + h*sH + t*sT + d (+ l*sL when layer == -1, which
+ * quantizes every layer).  T must be the value given to semkv_rank.
+ * Non-finite K/V sets SEMKV_STATUS_NONFINITE_KV. */
+int semkv_quantize_pack(semkv_cache* c, int32_t layer, const uint16_t* K, const uint16_t* V,
+                        int64_t sL, int64_t sB, int64_t sH, int64_t sT, int64_t T,
+                        const int32_t* hi_idx, const int32_t* lo_idx, hipStream_t stream);
+
+/* Alg. 2 (append): store the current generated token's K and V of `layer` at
+ * fp16 in the tail.  k_new, v_new: device fp16 [batch][n_kv_heads][128]
+ * (with layer == -1: [n_layers][batch][n_kv_heads][128]). */
+int semkv_append_kv(semkv_cache* c, int32_t layer, const uint16_t* k_new, const uint16_t* v_new,
+                    hipStream_t stream);
+
+/* Alg. 2 (score): record the current token's score (device fp32 [batch]).
+ * Every layer must have appended the token.  When 64 scores are held the
+ * block closes: in each sequence exactly round(r*64) tokens of the block (the
+ * highest scores, ties to the lower index) are quantized with L_hi, the rest
+ * with L_lo, and appended to the pools. */
+int semkv_append_commit(semkv_cache* c, const float* score_new, hipStream_t stream);
+
+/* Alg. 2 (end of turn): close a partial block of n < 64 scored tokens with
+ * round(r*n) high-precision tokens (nearest integer, ties to even). */
+int semkv_flush(semkv_cache* c, hipStream_t stream);
+
+/* Bytes of workspace semkv_decode_attn needs for this cache's current counts. */
+int semkv_workspace_bytes(const semkv_cache* c, size_t* bytes);
+
+/* Decode attention of one layer: for each sequence b and query head h (KV head
+ * h/4), out[b][h] = softmax(q[b][h] . k_t / sqrt(128)) . v_t over every token
+ * t of the sequence: both pools (dequantized on the fly) and the fp16 tail
+ * rows appended so far, including this layer's current token if appended.
+ * q: device fp16 [batch][n_q_heads][128]; out: device fp32, same shape.
+ * workspace: device, ws_bytes >= semkv_workspace_bytes(). */
+int semkv_decode_attn(const semkv_cache* c, int32_t layer, const uint16_t* q, float* out,
+                      void* workspace, size_t ws_bytes, hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SEMKV_H */

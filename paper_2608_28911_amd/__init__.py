@@ -1,0 +1,148 @@
+"""SemKV hot path on MI355X: Python binding of libsemkv.so.
+
+The binding only marshals arguments: torch supplies device memory and the
+current HIP stream, every step of the path (ranking, quantize + pack, deferred
+append and close, decode attention) runs in the library's gfx950 kernels.
+"""
+import ctypes
+
+import numpy as np
+
+from . import _abi
+from ._abi import BASE_AFFINE, BASE_TQ, SemKVError, check, lib
+
+__all__ = ["SemKVCache", "SemKVError", "BASE_AFFINE", "BASE_TQ", "tq_codebook", "cache_sizes"]
+
+
+def _stream():
+    import torch
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _ptr(t):
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def make_config(n_layers, n_kv_heads, batch, base, L_hi, L_lo, group, r_num, r_den,
+                max_prompt, max_new, head_dim=128, n_q_heads=None, block=64) -> _abi.Config:
+    return _abi.Config(n_layers=n_layers, n_kv_heads=n_kv_heads,
+                       n_q_heads=4 * n_kv_heads if n_q_heads is None else n_q_heads,
+                       head_dim=head_dim, batch=batch, base=base, L_hi=L_hi, L_lo=L_lo, group=group,
+                       r_num=r_num, r_den=r_den, block=block, max_prompt=max_prompt, max_new=max_new)
+
+
+def cache_sizes(cfg: _abi.Config) -> _abi.Sizes:
+    s = _abi.Sizes()
+    check(lib().semkv_cache_sizes(ctypes.byref(cfg), ctypes.byref(s)), "semkv_cache_sizes")
+    return s
+
+
+def tq_codebook(L):
+    mu = np.zeros(16, np.float32)
+    tau = np.zeros(16, np.float32)
+    check(lib().semkv_tq_codebook(L, mu.ctypes.data, tau.ctypes.data), "semkv_tq_codebook")
+    return mu[:L].copy(), tau[:L - 1].copy()
+
+
+class SemKVCache:
+    """One mixed-precision KV cache on the current GPU (buffers are torch tensors)."""
+
+    def __init__(self, cfg: _abi.Config, sign_words=None, device="cuda"):
+        import torch
+        self.cfg = cfg
+        self.sz = cache_sizes(cfg)
+        dev = torch.device(device)
+        self.pools = torch.empty(self.sz.pool_bytes, dtype=torch.uint8, device=dev)
+        self.tail = torch.empty(self.sz.tail_bytes // 2, dtype=torch.float16, device=dev)
+        self.tail_scores = torch.zeros(self.sz.tail_score_bytes // 4, dtype=torch.float32, device=dev)
+        self.flags = torch.zeros(self.sz.flag_bytes // 4, dtype=torch.int32, device=dev)
+        self.status_word = torch.zeros(4, dtype=torch.int32, device=dev)
+        self.signs = None
+        if cfg.base == BASE_TQ:
+            sw = np.ascontiguousarray(sign_words, dtype=np.uint32).reshape(cfg.n_layers, cfg.n_kv_heads, 4)
+            self.signs = torch.from_numpy(sw.view(np.int32)).to(dev)
+        self.c = _abi.Cache()
+        check(lib().semkv_cache_init(ctypes.byref(self.c), ctypes.byref(cfg), _ptr(self.pools),
+                                     _ptr(self.tail), _ptr(self.tail_scores), _ptr(self.flags),
+                                     _ptr(self.signs) if self.signs is not None else None,
+                                     _ptr(self.status_word)), "semkv_cache_init")
+        self._ws = None
+
+    # -- the hot path ------------------------------------------------------
+    def rank(self, scores):
+        """scores: fp32 [B, T] on the device -> (hi_idx [B, K], lo_idx [B, T-K]) int32."""
+        import torch
+        scores = scores.contiguous()
+        B, T = scores.shape
+        K = self.cfg.r_num * T // self.cfg.r_den
+        hi = torch.empty((B, K), dtype=torch.int32, device=scores.device)
+        lo = torch.empty((B, T - K), dtype=torch.int32, device=scores.device)
+        check(lib().semkv_rank(ctypes.byref(self.c), _ptr(scores), T, _ptr(hi), _ptr(lo), _stream()),
+              "semkv_rank")
+        return hi, lo
+
+    def quantize_pack(self, layer, K, V, hi_idx, lo_idx):
+        """K, V: fp16 [B, H_kv, T, 128] (layer >= 0) or [n_layers, B, H_kv, T, 128] (layer = -1)."""
+        assert K.dtype == V.dtype and K.dtype.itemsize == 2 and K.stride() == V.stride()
+        st = K.stride()
+        if layer < 0:
+            sL, sB, sH, sT = st[0], st[1], st[2], st[3]
+        else:
+            sL, (sB, sH, sT) = 0, st[:3]
+        T = K.shape[-2]
+        check(lib().semkv_quantize_pack(ctypes.byref(self.c), layer, _ptr(K), _ptr(V), sL, sB, sH, sT, T,
+                                        _ptr(hi_idx), _ptr(lo_idx), _stream()), "semkv_quantize_pack")
+
+    def append_kv(self, layer, k, v):
+        check(lib().semkv_append_kv(ctypes.byref(self.c), layer, _ptr(k.contiguous()), _ptr(v.contiguous()),
+                                    _stream()), "semkv_append_kv")
+
+    def append_commit(self, score):
+        check(lib().semkv_append_commit(ctypes.byref(self.c), _ptr(score.contiguous()), _stream()),
+              "semkv_append_commit")
+
+    def flush(self):
+        check(lib().semkv_flush(ctypes.byref(self.c), _stream()), "semkv_flush")
+
+    def workspace_bytes(self):
+        n = ctypes.c_size_t()
+        check(lib().semkv_workspace_bytes(ctypes.byref(self.c), ctypes.byref(n)), "semkv_workspace_bytes")
+        return n.value
+
+    def workspace(self):
+        import torch
+        need = max(self.workspace_bytes(), 16)
+        if self._ws is None or self._ws.numel() * 4 < need:
+            self._ws = torch.empty((need + 3) // 4, dtype=torch.float32, device=self.pools.device)
+        return self._ws
+
+    def decode_attn(self, layer, q, out=None, workspace=None):
+        """q: fp16 [B, H_q, 128] -> fp32 [B, H_q, 128]."""
+        import torch
+        q = q.contiguous()
+        if out is None:
+            out = torch.empty(q.shape, dtype=torch.float32, device=q.device)
+        ws = self.workspace() if workspace is None else workspace
+        check(lib().semkv_decode_attn(ctypes.byref(self.c), layer, _ptr(q), _ptr(out), _ptr(ws),
+                                      ws.numel() * ws.element_size(), _stream()), "semkv_decode_attn")
+        return out
+
+    # -- state -------------------------------------------------------------
+    @property
+    def counts(self):
+        return dict(n_prompt=self.c.n_prompt, n_hi=self.c.n_hi, n_lo=self.c.n_lo, n_scored=self.c.n_scored)
+
+    def status(self) -> int:
+        return int(self.status_word[0].item())
+
+    def unit_offset(self, b, layer, kvh) -> int:
+        return ((b * self.cfg.n_layers + layer) * self.cfg.n_kv_heads + kvh) * self.sz.unit_stride
+
+    def pool_bytes(self, b, layer, kvh, pool, n_tiles=None):
+        """Device bytes of the records of one pool of one unit (a torch view)."""
+        off = self.unit_offset(b, layer, kvh)
+        rb = self.sz.record_bytes_hi if pool == 0 else self.sz.record_bytes_lo
+        if pool == 1:
+            off += self.sz.cap_hi_tiles * self.sz.record_bytes_hi
+        n = (self.sz.cap_hi_tiles if pool == 0 else self.sz.cap_lo_tiles) if n_tiles is None else n_tiles
+        return self.pools[off:off + n * rb]

@@ -1,0 +1,450 @@
+// quant.hip -- quantize + pack of prompt tokens (Alg. 1, Eq. 7), the fp16 tail
+// append and the block close of generated tokens (Alg. 2), for gfx950.
+//
+// One workgroup (256 threads) builds one 64-slot record of one pool of one
+// (sequence, layer, kv head) unit.  Four consecutive lanes own one token row:
+// lane q holds channels [32q, 32q+32).  Codes go to LDS, then each thread packs
+// whole segments (Sec. 4.1 mixed-radix symbols) into the LDS body with atomic
+// ORs, and the record is written with 16-byte stores.
+#include <hip/hip_fp16.h>
+
+#include "semkv_internal.h"
+
+namespace semkv {
+namespace {
+
+constexpr int kPitch = 132;             // LDS row pitch of the code arrays (bytes)
+constexpr int kMaxBodyWords = 2672 / 4; // largest body: L = 6
+
+__device__ inline float h2f(uint16_t b) { return __half2float(__ushort_as_half(b)); }
+__device__ inline uint16_t f2h(float f) { return __half_as_ushort(__float2half_rn(f)); }
+
+__device__ inline void load_quarter(const uint16_t* src, float x[32]) {
+  const uint4* p = reinterpret_cast<const uint4*>(src);
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    uint4 w = p[k];
+    uint32_t d[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      x[8 * k + 2 * e] = h2f(uint16_t(d[e] & 0xFFFFu));
+      x[8 * k + 2 * e + 1] = h2f(uint16_t(d[e] >> 16));
+    }
+  }
+}
+
+// Asymmetric affine quantizer (Sec. 4.1) of one row quarter; the min/max of a
+// group of G channels is combined over the G/32 lanes holding it.  Returns
+// {scale, zero} as fp16 bits (low half = scale).
+template <int L>
+__device__ uint32_t affine_quarter(const float x[32], int G, uint8_t* code, bool& bad) {
+  float mn = x[0], mx = x[0];
+  bool nf = false;
+#pragma unroll
+  for (int i = 0; i < 32; ++i) {
+    mn = fminf(mn, x[i]);
+    mx = fmaxf(mx, x[i]);
+    nf |= !isfinite(x[i]);
+  }
+  if (G >= 64) {
+    mn = fminf(mn, __shfl_xor(mn, 1));
+    mx = fmaxf(mx, __shfl_xor(mx, 1));
+  }
+  if (G >= 128) {
+    mn = fminf(mn, __shfl_xor(mn, 2));
+    mx = fmaxf(mx, __shfl_xor(mx, 2));
+  }
+  float zero = mn + 0.0f;                               // -0 -> +0
+  uint16_t s16 = f2h(__fdiv_rn(mx - mn, float(L - 1)));
+  float sf = h2f(s16);
+  float inv = sf == 0.0f ? 0.0f : __fdiv_rn(1.0f, sf);
+#pragma unroll
+  for (int i = 0; i < 32; ++i) {
+    float c = rintf((x[i] - zero) * inv);
+    c = fminf(fmaxf(c, 0.0f), float(L - 1));
+    code[i] = uint8_t(c);
+  }
+  bad |= nf;
+  return uint32_t(s16) | (uint32_t(f2h(zero)) << 16);
+}
+
+// TurboQuant-MSE base (Sec. 4.9) of one row quarter: sign flip, unnormalized
+// Walsh-Hadamard transform (stages 1..64), the row norm by a fixed pairwise
+// tree, one fp16 scalar, and Lloyd-Max threshold codes.  Returns rho bits.
+template <int L>
+__device__ uint16_t tq_quarter(const float x[32], int q, const uint32_t* sw, const float* tau,
+                               uint8_t* code, bool& bad) {
+  float u[32], a[32];
+  bool nf = false;
+  uint32_t sbits = sw[q];
+#pragma unroll
+  for (int i = 0; i < 32; ++i) {
+    u[i] = ((sbits >> i) & 1u) ? -x[i] : x[i];
+    a[i] = x[i] * x[i];
+    nf |= !isfinite(x[i]);
+  }
+#pragma unroll
+  for (int h = 1; h < 32; h <<= 1)
+#pragma unroll
+    for (int i = 0; i < 32; ++i)
+      if (!(i & h)) {
+        float p = u[i], r = u[i + h];
+        u[i] = p + r;
+        u[i + h] = p - r;
+      }
+#pragma unroll
+  for (int i = 0; i < 32; ++i) {                         // h = 32: partner lane q ^ 1
+    float o = __shfl_xor(u[i], 1);
+    u[i] = (q & 1) ? o - u[i] : u[i] + o;
+  }
+#pragma unroll
+  for (int i = 0; i < 32; ++i) {                         // h = 64: partner lane q ^ 2
+    float o = __shfl_xor(u[i], 2);
+    u[i] = (q & 2) ? o - u[i] : u[i] + o;
+  }
+#pragma unroll
+  for (int i = 0; i < 32; ++i) a[i] = a[i] + __shfl_xor(a[i], 2);   // h = 64 (lanes 0,1 keep)
+#pragma unroll
+  for (int i = 0; i < 32; ++i) a[i] = a[i] + __shfl_xor(a[i], 1);   // h = 32 (lane 0 keeps)
+#pragma unroll
+  for (int h = 16; h >= 1; h >>= 1)
+#pragma unroll
+    for (int i = 0; i < h; ++i) a[i] = a[i] + a[i + h];
+  uint16_t r16 = f2h(__fsqrt_rn(a[0]));
+  if ((r16 & 0x7FFFu) == 0x7C00u) r16 = 0x7BFFu;       // saturate to 65504
+  int lane = __lane_id();
+  r16 = uint16_t(__shfl(int(r16), lane & ~3));
+  float rf = h2f(r16);
+  float thr[L - 1];
+#pragma unroll
+  for (int k = 0; k < L - 1; ++k) thr[k] = rf * tau[k];
+#pragma unroll
+  for (int i = 0; i < 32; ++i) {
+    int c = 0;
+#pragma unroll
+    for (int k = 0; k < L - 1; ++k) c += u[i] > thr[k] ? 1 : 0;
+    code[i] = uint8_t(c);
+  }
+  bad |= nf;
+  return r16;
+}
+
+// Quantize the quarter row held by this lane and write its metadata.
+template <int BASE, int L>
+__device__ void quantize_quarter(const PoolGeom& g, const float x[32], int q, int layer, int kvh,
+                                 const float* tau, uint8_t* code, uint8_t* meta_dst, int slot,
+                                 bool valid, bool& bad) {
+  if (BASE == 0) {
+    uint32_t m = affine_quarter<L>(x, g.G, code, bad);
+    int per = g.G / 32;
+    if (q % per == 0)
+      reinterpret_cast<uint32_t*>(meta_dst)[(q / per) * kSlots + slot] = valid ? m : 0u;
+  } else {
+    const uint32_t* sw = g.signs + (int64_t(layer) * g.n_kv_heads + kvh) * 4;
+    uint16_t r = tq_quarter<L>(x, q, sw, tau, code, bad);
+    if (q == 0) reinterpret_cast<uint16_t*>(meta_dst)[slot] = valid ? r : uint16_t(0);
+  }
+}
+
+// OR the bits of one segment into an LDS body.  The segment holds symbols
+// p = j, j+4, ... of a line of NV codes: code p*n+i of the line is at
+// codes[(p*n+i)*stride].
+template <int L, int NV, int NL>
+__device__ void pack_segment(const uint8_t* codes, int stride, int line, int j, uint32_t* body) {
+  constexpr int n = sym_digits(L);
+  constexpr int S = num_syms(L, NV);
+  uint64_t lo = 0, hi = 0;
+  int nb = 0;
+#pragma unroll
+  for (int p0 = 0; p0 < S; p0 += 4) {
+    int p = p0 + j;
+    if (p < S) {
+      int nd = NV - n * p < n ? NV - n * p : n;
+      uint32_t v = 0;
+      for (int i = nd - 1; i >= 0; --i) v = v * L + codes[(n * p + i) * stride];
+      int w = width_of(L, nd);
+      if (nb < 64) {
+        lo |= uint64_t(v) << nb;
+        if (nb + w > 64) hi |= uint64_t(v) >> (64 - nb);
+      } else {
+        hi |= uint64_t(v) << (nb - 64);
+      }
+      nb += w;
+    }
+  }
+  int off = seg_start(L, NV, NL, 0);
+  for (int i = 0; i < j; ++i) off += NL * seg_bits(L, NV, i);
+  off += line * seg_bits(L, NV, j);
+  int w0 = off >> 5, sh = off & 31;
+  uint32_t s[4] = {uint32_t(lo), uint32_t(lo >> 32), uint32_t(hi), uint32_t(hi >> 32)};
+  uint32_t o[5];
+  o[0] = s[0] << sh;
+#pragma unroll
+  for (int k = 1; k < 4; ++k) o[k] = (s[k] << sh) | (sh ? s[k - 1] >> (32 - sh) : 0u);
+  o[4] = sh ? s[3] >> (32 - sh) : 0u;
+#pragma unroll
+  for (int k = 0; k < 5; ++k)
+    if (32 * k < sh + nb && o[k]) atomicOr(&body[w0 + k], o[k]);
+}
+
+// Decode one segment of an LDS body back into codes (used to extend a
+// partially filled record when a generation block closes).
+template <int L, int NV, int NL>
+__device__ void unpack_segment(const uint32_t* body, int line, int j, uint8_t* codes, int stride) {
+  constexpr int n = sym_digits(L);
+  constexpr int S = num_syms(L, NV);
+  int off = 0;
+  for (int i = 0; i < j; ++i) off += NL * seg_bits(L, NV, i);
+  off += line * seg_bits(L, NV, j);
+#pragma unroll
+  for (int p0 = 0; p0 < S; p0 += 4) {
+    int p = p0 + j;
+    if (p < S) {
+      int nd = NV - n * p < n ? NV - n * p : n;
+      int w = width_of(L, nd);
+      int wd = off >> 5, sh = off & 31;
+      uint64_t pair = uint64_t(body[wd]) | (uint64_t(body[wd + 1]) << 32);
+      uint32_t v = uint32_t(pair >> sh) & ((1u << w) - 1u);
+      for (int i = 0; i < nd; ++i) {
+        codes[(n * p + i) * stride] = uint8_t(v % L);
+        v /= L;
+      }
+      off += w;
+    }
+  }
+}
+
+template <int L>
+__device__ void pack_record(const uint8_t* ck, const uint8_t* cv, uint32_t* bk, uint32_t* bv) {
+  int tid = threadIdx.x;
+  pack_segment<L, kD, kSlots>(ck + (tid & 63) * kPitch, 1, tid & 63, tid >> 6, bk);
+#pragma unroll
+  for (int e = 0; e < 2; ++e) {
+    int s = tid + 256 * e;
+    pack_segment<L, kSlots, kD>(cv + (s & 127), kPitch, s & 127, s >> 7, bv);
+  }
+}
+
+__device__ void store_bodies(uint8_t* rec, const uint32_t* bk, const uint32_t* bv, int tb) {
+  const uint4* sk = reinterpret_cast<const uint4*>(bk);
+  const uint4* sv = reinterpret_cast<const uint4*>(bv);
+  uint4* dk = reinterpret_cast<uint4*>(rec);
+  uint4* dv = reinterpret_cast<uint4*>(rec + tb);
+  for (int i = threadIdx.x; i < tb / 16; i += 256) {
+    dk[i] = sk[i];
+    dv[i] = sv[i];
+  }
+}
+
+struct Lds {
+  alignas(16) uint8_t ck[kSlots * kPitch];
+  alignas(16) uint8_t cv[kSlots * kPitch];
+  alignas(16) uint32_t bk[kMaxBodyWords + 8];
+  alignas(16) uint32_t bv[kMaxBodyWords + 8];
+};
+
+template <int BASE, int L>
+__device__ void prefill_record(const QuantArgs& a, Lds& s, int pool, int tile, int b, int l, int h) {
+  const PoolGeom& g = a.g;
+  int tid = threadIdx.x, r = tid >> 2, q = tid & 3;
+  int64_t slot = int64_t(tile) * kSlots + r;
+  bool valid = slot < a.n_pool[pool];
+  int tok = valid ? a.idx[pool][int64_t(b) * a.n_pool[pool] + slot] : 0;
+  if (tok < 0 || tok >= a.T) {             // a slot list not produced by semkv_rank
+    if (valid) atomicOr(g.status, 4);
+    tok = 0;
+  }
+  constexpr int tb = tile_bytes(L);
+  uint8_t* rec = g.pools + unit_offset(g, b, l, h) + (pool ? g.lo_offset : 0) + int64_t(tile) * g.rec_bytes[pool];
+  for (int i = tid; i < kMaxBodyWords + 8; i += 256) s.bk[i] = s.bv[i] = 0u;
+  bool bad = false;
+  const int64_t base_off = int64_t(l) * a.sL + int64_t(b) * a.sB + int64_t(h) * a.sH + int64_t(tok) * a.sT + 32 * q;
+  float x[32];
+  uint8_t code[32];
+#pragma unroll
+  for (int kv = 0; kv < 2; ++kv) {
+    if (valid) {
+      load_quarter((kv ? a.V : a.K) + base_off, x);
+    } else {
+#pragma unroll
+      for (int i = 0; i < 32; ++i) x[i] = 0.0f;
+    }
+    quantize_quarter<BASE, L>(g, x, q, l, h, g.tau[pool], code, rec + 2 * tb + kv * g.meta_bytes, r, valid, bad);
+    uint8_t* dst = (kv ? s.cv : s.ck) + r * kPitch + 32 * q;
+#pragma unroll
+    for (int i = 0; i < 32; ++i) dst[i] = valid ? code[i] : uint8_t(0);
+  }
+  if (bad && valid) atomicOr(g.status, 2);
+  __syncthreads();
+  pack_record<L>(s.ck, s.cv, s.bk, s.bv);
+  __syncthreads();
+  store_bodies(rec, s.bk, s.bv, tb);
+}
+
+template <int BASE, int LH, int LL>
+__global__ __launch_bounds__(256) void quantize_pack_kernel(QuantArgs a) {
+  __shared__ Lds s;
+  int tile = blockIdx.x, pool = blockIdx.y & 1, h = blockIdx.y >> 1;
+  int b = blockIdx.z / a.n_layers_launched, l = a.layer0 + blockIdx.z % a.n_layers_launched;
+  if (int64_t(tile) * kSlots >= a.n_pool[pool]) return;
+  if (pool == 0) prefill_record<BASE, LH>(a, s, 0, tile, b, l, h);
+  else prefill_record<BASE, LL>(a, s, 1, tile, b, l, h);
+}
+
+// ---------------------------------------------------------------- close --
+
+template <int BASE, int L>
+__device__ void close_record(const CloseArgs& a, Lds& s, const int* row_of, int m, int pool,
+                             int tile, int b, int l, int h) {
+  const PoolGeom& g = a.g;
+  int tid = threadIdx.x, r = tid >> 2, q = tid & 3;
+  constexpr int tb = tile_bytes(L);
+  uint8_t* rec = g.pools + unit_offset(g, b, l, h) + (pool ? g.lo_offset : 0) + int64_t(tile) * g.rec_bytes[pool];
+  int64_t first = int64_t(tile) * kSlots;
+  int64_t n0 = a.n0[pool];
+  // existing rows of this record are unpacked; the rest start at code 0
+  for (int i = tid; i < kMaxBodyWords + 8; i += 256) s.bk[i] = s.bv[i] = 0u;
+  __syncthreads();
+  if (first < n0) {
+    const uint32_t* gk = reinterpret_cast<const uint32_t*>(rec);
+    const uint32_t* gv = reinterpret_cast<const uint32_t*>(rec + tb);
+    for (int i = tid; i < tb / 4; i += 256) {
+      s.bk[i] = gk[i];
+      s.bv[i] = gv[i];
+    }
+  }
+  __syncthreads();
+  unpack_segment<L, kD, kSlots>(s.bk, tid & 63, tid >> 6, s.ck + (tid & 63) * kPitch, 1);
+#pragma unroll
+  for (int e = 0; e < 2; ++e) {
+    int sg = tid + 256 * e;
+    unpack_segment<L, kSlots, kD>(s.bv, sg & 127, sg >> 7, s.cv + (sg & 127), kPitch);
+  }
+  __syncthreads();
+  int64_t slot = first + r;
+  bool fresh = slot >= n0;                 // slots written by this close
+  bool valid = fresh && slot < n0 + m;
+  int row = valid ? row_of[slot - n0] : 0;
+  bool bad = false;
+  if (fresh) {
+    const uint16_t* src = a.tail + ((((int64_t(b) * g.n_layers + l) * g.n_kv_heads + h) * 2) * kSlots + row) * kD + 32 * q;
+    float x[32];
+    uint8_t code[32];
+#pragma unroll
+    for (int kv = 0; kv < 2; ++kv) {
+      if (valid) {
+        load_quarter(src + kv * kSlots * kD, x);
+      } else {
+#pragma unroll
+        for (int i = 0; i < 32; ++i) x[i] = 0.0f;
+      }
+      quantize_quarter<BASE, L>(g, x, q, l, h, g.tau[pool], code, rec + 2 * tb + kv * g.meta_bytes, r, valid, bad);
+      uint8_t* dst = (kv ? s.cv : s.ck) + r * kPitch + 32 * q;
+#pragma unroll
+      for (int i = 0; i < 32; ++i) dst[i] = valid ? code[i] : uint8_t(0);
+    }
+  }
+  if (bad && valid) atomicOr(g.status, 2);
+  __syncthreads();
+  for (int i = tid; i < kMaxBodyWords + 8; i += 256) s.bk[i] = s.bv[i] = 0u;
+  __syncthreads();
+  pack_record<L>(s.ck, s.cv, s.bk, s.bv);
+  __syncthreads();
+  store_bodies(rec, s.bk, s.bv, tb);
+}
+
+template <int BASE, int LH, int LL>
+__global__ __launch_bounds__(256) void close_kernel(CloseArgs a) {
+  __shared__ Lds s;
+  __shared__ float sc[kSlots];
+  __shared__ int cls[kSlots], row_of[2][kSlots];
+  int tid = threadIdx.x;
+  int pool = blockIdx.y & 1, h = blockIdx.y >> 1;
+  int b = blockIdx.z / a.g.n_layers, l = blockIdx.z % a.g.n_layers;
+  if (tid < a.n) {
+    float v = a.tail_scores[int64_t(b) * kSlots + tid];
+    sc[tid] = v == 0.0f ? 0.0f : v;
+    if (isnan(v)) atomicOr(a.g.status, 1);
+  }
+  __syncthreads();
+  if (tid < a.n) {                         // rank inside the block (Alg. 2)
+    float v = sc[tid];
+    int rank = 0;
+    for (int j = 0; j < a.n; ++j) rank += (sc[j] > v || (sc[j] == v && j < tid)) ? 1 : 0;
+    cls[tid] = rank < a.k_hi ? 0 : 1;
+  }
+  __syncthreads();
+  if (tid < a.n) {
+    int c = cls[tid], pos = 0;
+    for (int j = 0; j < tid; ++j) pos += cls[j] == c ? 1 : 0;
+    row_of[c][pos] = tid;
+    if (c == 0 && pool == 0 && h == 0 && l == 0 && blockIdx.x == 0) {
+      int64_t t = a.pos0 + tid;
+      atomicOr(&a.flags[int64_t(b) * a.flag_words + (t >> 5)], 1u << (t & 31));
+    }
+  }
+  __syncthreads();
+  int m = pool == 0 ? a.k_hi : a.n - a.k_hi;
+  int64_t n0 = a.n0[pool];
+  int64_t tile = n0 / kSlots + blockIdx.x;
+  if (m == 0 || tile > (n0 + m - 1) / kSlots) return;
+  if (pool == 0) close_record<BASE, LH>(a, s, row_of[0], m, 0, int(tile), b, l, h);
+  else close_record<BASE, LL>(a, s, row_of[1], m, 1, int(tile), b, l, h);
+}
+
+__global__ void append_kernel(AppendArgs a) {
+  // one block per (layer, b, kv head); 64 threads copy K and V rows
+  int z = blockIdx.x;
+  int h = z % a.n_kv_heads;
+  int b = (z / a.n_kv_heads) % a.batch;
+  int li = z / (a.n_kv_heads * a.batch);
+  int l = a.layer0 + li;
+  const uint32_t* k = reinterpret_cast<const uint32_t*>(a.k + ((int64_t(li) * a.batch + b) * a.n_kv_heads + h) * kD);
+  const uint32_t* v = reinterpret_cast<const uint32_t*>(a.v + ((int64_t(li) * a.batch + b) * a.n_kv_heads + h) * kD);
+  uint32_t* dst = reinterpret_cast<uint32_t*>(a.tail + ((((int64_t(b) * a.n_layers + l) * a.n_kv_heads + h) * 2) * kSlots + a.slot) * kD);
+  int t = threadIdx.x;
+  dst[t] = k[t];
+  dst[kSlots * kD / 2 + t] = v[t];
+}
+
+template <int BASE, int LH, int LL>
+int launch_qp(const QuantArgs& a, hipStream_t st) {
+  dim3 grid(a.max_tiles, 2 * a.g.n_kv_heads, a.g.batch * a.n_layers_launched);
+  hipLaunchKernelGGL((quantize_pack_kernel<BASE, LH, LL>), grid, dim3(256), 0, st, a);
+  return hipGetLastError() == hipSuccess ? 0 : -5;
+}
+
+template <int BASE, int LH, int LL>
+int launch_cl(const CloseArgs& a, hipStream_t st) {
+  dim3 grid(2, 2 * a.g.n_kv_heads, a.g.batch * a.g.n_layers);
+  hipLaunchKernelGGL((close_kernel<BASE, LH, LL>), grid, dim3(256), 0, st, a);
+  return hipGetLastError() == hipSuccess ? 0 : -5;
+}
+
+}  // namespace
+
+#define SEMKV_DISPATCH_LEVELS(BASE, LH, LL, FN, ...)                                  \
+  if (BASE == 0 && LH == 6 && LL == 5) return FN<0, 6, 5>(__VA_ARGS__);              \
+  if (BASE == 0 && LH == 5 && LL == 4) return FN<0, 5, 4>(__VA_ARGS__);              \
+  if (BASE == 0 && LH == 6 && LL == 4) return FN<0, 6, 4>(__VA_ARGS__);              \
+  if (BASE == 0 && LH == 4 && LL == 3) return FN<0, 4, 3>(__VA_ARGS__);              \
+  if (BASE == 0 && LH == 5 && LL == 3) return FN<0, 5, 3>(__VA_ARGS__);              \
+  if (BASE == 0 && LH == 6 && LL == 3) return FN<0, 6, 3>(__VA_ARGS__);              \
+  if (BASE == 1 && LH == 4 && LL == 3) return FN<1, 4, 3>(__VA_ARGS__);              \
+  return -2;
+
+int launch_quantize(const QuantArgs& a, hipStream_t s) {
+  SEMKV_DISPATCH_LEVELS(a.g.base, a.g.L[0], a.g.L[1], launch_qp, a, s)
+}
+
+int launch_close(const CloseArgs& a, hipStream_t s) {
+  SEMKV_DISPATCH_LEVELS(a.g.base, a.g.L[0], a.g.L[1], launch_cl, a, s)
+}
+
+int launch_append(const AppendArgs& a, hipStream_t s) {
+  dim3 grid(a.n_layers_launched * a.batch * a.n_kv_heads);
+  hipLaunchKernelGGL(append_kernel, grid, dim3(64), 0, s, a);
+  return hipGetLastError() == hipSuccess ? 0 : -5;
+}
+
+}  // namespace semkv

@@ -1,0 +1,391 @@
+// semkv_api.hip -- host side of the C ABI declared in include/semkv.h:
+// validation, buffer geometry, host-side counts of the deferred state machine
+// (Alg. 2) and kernel launches.  Nothing here allocates or synchronizes.
+#include <math.h>
+#include <string.h>
+
+#include "semkv.h"
+#include "semkv_internal.h"
+
+using namespace semkv;
+
+namespace {
+
+bool levels_ok(int base, int lh, int ll) {
+  if (base == SEMKV_BASE_TQ) return lh == 4 && ll == 3;
+  static const int pairs[][2] = {{6, 5}, {5, 4}, {6, 4}, {4, 3}, {5, 3}, {6, 3}};
+  for (auto& p : pairs)
+    if (p[0] == lh && p[1] == ll) return true;
+  return false;
+}
+
+int64_t top_count(int64_t T, int64_t rn, int64_t rd) { return rn * T / rd; }   // floor(r T)
+
+int64_t round_half_even(int64_t n, int64_t rn, int64_t rd) {                    // round(r n)
+  int64_t a = rn * n, q = a / rd, rem = a - q * rd;
+  if (2 * rem > rd || (2 * rem == rd && (q & 1))) ++q;
+  return q;
+}
+
+PoolGeom geom(const semkv_cache* c) {
+  PoolGeom g;
+  memset(&g, 0, sizeof(g));
+  const semkv_config& k = c->cfg;
+  g.pools = c->pools;
+  g.unit_stride = c->sz.unit_stride;
+  g.lo_offset = c->sz.cap_hi_tiles * c->sz.record_bytes_hi;
+  g.rec_bytes[0] = int32_t(c->sz.record_bytes_hi);
+  g.rec_bytes[1] = int32_t(c->sz.record_bytes_lo);
+  g.tile_bytes[0] = int32_t(c->sz.tile_bytes_hi);
+  g.tile_bytes[1] = int32_t(c->sz.tile_bytes_lo);
+  g.meta_bytes = int32_t(c->sz.meta_bytes);
+  g.L[0] = k.L_hi;
+  g.L[1] = k.L_lo;
+  g.base = k.base;
+  g.G = k.group;
+  g.n_layers = k.n_layers;
+  g.n_kv_heads = k.n_kv_heads;
+  g.batch = k.batch;
+  memcpy(g.tau[0], c->tau_hi, sizeof(g.tau[0]));
+  memcpy(g.tau[1], c->tau_lo, sizeof(g.tau[1]));
+  g.signs = c->tq_signs;
+  g.status = c->status;
+  return g;
+}
+
+bool all_appended(const semkv_cache* c) {
+  for (int l = 0; l < c->cfg.n_layers; ++l)
+    if (!((c->appended[l >> 5] >> (l & 31)) & 1u)) return false;
+  return true;
+}
+
+bool none_appended(const semkv_cache* c) {
+  return !(c->appended[0] | c->appended[1] | c->appended[2] | c->appended[3]);
+}
+
+// standard normal density and tail
+double npdf(double x) { return exp(-0.5 * x * x) / sqrt(2.0 * M_PI); }
+double ncdf(double x) { return 0.5 * erfc(-x / sqrt(2.0)); }
+
+template <class F>
+double bisect(F f, double lo, double hi) {
+  double flo = f(lo);
+  for (int it = 0; it < 200; ++it) {
+    double mid = 0.5 * (lo + hi);
+    if (mid == lo || mid == hi) break;
+    double fm = f(mid);
+    if ((fm < 0) == (flo < 0)) {
+      lo = mid;
+      flo = fm;
+    } else {
+      hi = mid;
+    }
+  }
+  return 0.5 * (lo + hi);
+}
+
+// Decode split plan: tiles per split (a multiple of 4, one per wave) chosen
+// so the grid has about 1024 workgroups.
+void plan(const semkv_cache* c, int n_tail, int* chunk, int ns[2], int* nsplit) {
+  int64_t nt0 = (c->n_hi + kSlots - 1) / kSlots, nt1 = (c->n_lo + kSlots - 1) / kSlots;
+  int64_t total = int64_t(c->cfg.batch) * c->cfg.n_kv_heads * (nt0 + nt1);
+  int64_t ch = (total + 1023) / 1024;
+  ch = (ch + 3) / 4 * 4;
+  if (ch < 4) ch = 4;
+  *chunk = int(ch);
+  ns[0] = int((nt0 + ch - 1) / ch);
+  ns[1] = int((nt1 + ch - 1) / ch);
+  *nsplit = ns[0] + ns[1] + (n_tail > 0 ? 1 : 0);
+}
+
+int close_block(semkv_cache* c, int n, hipStream_t stream) {
+  const semkv_config& k = c->cfg;
+  int64_t kh = round_half_even(n, k.r_num, k.r_den);
+  if (c->n_hi + kh > c->sz.cap_hi_tiles * kSlots || c->n_lo + (n - kh) > c->sz.cap_lo_tiles * kSlots)
+    return SEMKV_ECAPACITY;
+  int64_t pos0 = c->n_hi + c->n_lo;
+  if (pos0 + n > c->sz.flag_words * 32) return SEMKV_ECAPACITY;
+  CloseArgs a;
+  memset(&a, 0, sizeof(a));
+  a.g = geom(c);
+  a.tail = c->tail;
+  a.tail_scores = c->tail_scores;
+  a.n = n;
+  a.k_hi = int32_t(kh);
+  a.n0[0] = c->n_hi;
+  a.n0[1] = c->n_lo;
+  a.flags = c->flags;
+  a.flag_words = c->sz.flag_words;
+  a.pos0 = pos0;
+  int st = launch_close(a, stream);
+  if (st) return st;
+  c->n_hi += kh;
+  c->n_lo += n - kh;
+  c->n_scored = 0;
+  return SEMKV_OK;
+}
+
+__global__ void store_score_kernel(float* dst, const float* src, int slot, int batch) {
+  int b = threadIdx.x;
+  if (b < batch) dst[b * kSlots + slot] = src[b];
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* semkv_strerror(int status) {
+  switch (status) {
+    case SEMKV_OK: return "ok";
+    case SEMKV_EINVAL: return "invalid argument";
+    case SEMKV_EUNSUPPORTED: return "unsupported configuration";
+    case SEMKV_ECAPACITY: return "capacity exceeded";
+    case SEMKV_ENAN: return "non-finite data";
+    case SEMKV_EHIP: return "HIP runtime error";
+    case SEMKV_ESTATE: return "call out of order";
+    default: return "unknown status";
+  }
+}
+
+int semkv_cache_sizes(const semkv_config* cfg, semkv_sizes* out) {
+  if (!cfg || !out) return SEMKV_EINVAL;
+  const semkv_config& k = *cfg;
+  if (k.n_layers < 1 || k.n_kv_heads < 1 || k.batch < 1 || k.n_layers > 128) return SEMKV_EINVAL;
+  if (k.r_den <= 0 || k.r_num < 0 || k.r_num > k.r_den || k.max_prompt < 0 || k.max_new < 0)
+    return SEMKV_EINVAL;
+  if (k.max_prompt > (int64_t(1) << 30) || k.max_new > (int64_t(1) << 30)) return SEMKV_EINVAL;
+  if (k.head_dim != 128 || k.n_q_heads != 4 * k.n_kv_heads || k.block != 64) return SEMKV_EUNSUPPORTED;
+  if (k.base != SEMKV_BASE_AFFINE && k.base != SEMKV_BASE_TQ) return SEMKV_EUNSUPPORTED;
+  if (!levels_ok(k.base, k.L_hi, k.L_lo)) return SEMKV_EUNSUPPORTED;
+  if (k.base == SEMKV_BASE_AFFINE && k.group != 32 && k.group != 64 && k.group != 128) return SEMKV_EUNSUPPORTED;
+  if (k.base == SEMKV_BASE_TQ && k.group != 128) return SEMKV_EUNSUPPORTED;
+  memset(out, 0, sizeof(*out));
+  int64_t khi = top_count(k.max_prompt, k.r_num, k.r_den);
+  int64_t hi_rows = khi + k.max_new, lo_rows = k.max_prompt - khi + k.max_new;
+  out->cap_hi_tiles = (hi_rows + kSlots - 1) / kSlots;
+  out->cap_lo_tiles = (lo_rows + kSlots - 1) / kSlots;
+  if (out->cap_hi_tiles < 1) out->cap_hi_tiles = 1;
+  if (out->cap_lo_tiles < 1) out->cap_lo_tiles = 1;
+  out->tile_bytes_hi = tile_bytes(k.L_hi);
+  out->tile_bytes_lo = tile_bytes(k.L_lo);
+  out->meta_bytes = meta_bytes(k.base, k.group);
+  out->record_bytes_hi = record_bytes(k.base, k.L_hi, k.group);
+  out->record_bytes_lo = record_bytes(k.base, k.L_lo, k.group);
+  out->unit_stride = out->cap_hi_tiles * out->record_bytes_hi + out->cap_lo_tiles * out->record_bytes_lo;
+  int64_t units = int64_t(k.batch) * k.n_layers * k.n_kv_heads;
+  out->pool_bytes = size_t(units * out->unit_stride);
+  out->tail_bytes = size_t(units * 2 * kSlots * kD * 2);
+  out->tail_score_bytes = size_t(k.batch) * kSlots * 4;
+  out->flag_words = (k.max_prompt + k.max_new + 31) / 32 + 1;
+  out->flag_bytes = size_t(k.batch * out->flag_words * 4);
+  int64_t max_split = out->cap_hi_tiles + out->cap_lo_tiles + 1;
+  out->workspace_bytes = size_t(int64_t(k.batch) * k.n_kv_heads * max_split * 4 * kPartial * 4);
+  return SEMKV_OK;
+}
+
+int semkv_tq_codebook(int L, float* mu, float* tau) {
+  if (!mu || !tau) return SEMKV_EINVAL;
+  if (L == 2) {                      // cells (-inf, 0], (0, inf): centroid 2 phi(0)
+    double m = 2.0 * npdf(0.0);
+    mu[0] = float(-m);
+    mu[1] = float(m);
+    tau[0] = 0.0f;
+    return SEMKV_OK;
+  }
+  if (L == 3) {                      // levels -m, 0, m; thresholds -m/2, m/2
+    auto f = [](double m) { double t = 0.5 * m; return npdf(t) / (1.0 - ncdf(t)) - m; };
+    double m = bisect(f, 0.5, 3.0);
+    mu[0] = float(-m);
+    mu[1] = 0.0f;
+    mu[2] = float(m);
+    tau[0] = float(-0.5 * m);
+    tau[1] = float(0.5 * m);
+    return SEMKV_OK;
+  }
+  if (L == 4) {                      // levels -b, -a, a, b; thresholds -t, 0, t with t = (a+b)/2
+    auto inner = [](double t) { return (npdf(0.0) - npdf(t)) / (ncdf(t) - 0.5); };
+    auto outer = [](double t) { return npdf(t) / (1.0 - ncdf(t)); };
+    auto f = [&](double t) { return 0.5 * (inner(t) + outer(t)) - t; };
+    double t = bisect(f, 0.1, 3.0);
+    double a = inner(t), b = outer(t);
+    mu[0] = float(-b);
+    mu[1] = float(-a);
+    mu[2] = float(a);
+    mu[3] = float(b);
+    tau[0] = float(-t);
+    tau[1] = 0.0f;
+    tau[2] = float(t);
+    return SEMKV_OK;
+  }
+  return SEMKV_EUNSUPPORTED;
+}
+
+int semkv_cache_init(semkv_cache* c, const semkv_config* cfg, void* pools, void* tail,
+                     float* tail_scores, uint32_t* flags, const uint32_t* tq_signs, int32_t* status) {
+  if (!c || !cfg) return SEMKV_EINVAL;
+  semkv_sizes sz;
+  int st = semkv_cache_sizes(cfg, &sz);
+  if (st) return st;
+  if (!pools || !tail || !tail_scores || !flags || !status) return SEMKV_EINVAL;
+  if (cfg->base == SEMKV_BASE_TQ && !tq_signs) return SEMKV_EINVAL;
+  if ((uintptr_t(pools) | uintptr_t(tail)) & 15) return SEMKV_EINVAL;
+  memset(c, 0, sizeof(*c));
+  c->cfg = *cfg;
+  c->sz = sz;
+  c->pools = static_cast<uint8_t*>(pools);
+  c->tail = static_cast<uint16_t*>(tail);
+  c->tail_scores = tail_scores;
+  c->flags = flags;
+  c->tq_signs = tq_signs;
+  c->status = status;
+  if (cfg->base == SEMKV_BASE_TQ) {
+    semkv_tq_codebook(cfg->L_hi, c->mu_hi, c->tau_hi);
+    semkv_tq_codebook(cfg->L_lo, c->mu_lo, c->tau_lo);
+  }
+  return SEMKV_OK;
+}
+
+int semkv_rank(semkv_cache* c, const float* scores, int64_t T, int32_t* hi_idx, int32_t* lo_idx,
+               hipStream_t stream) {
+  if (!c || !scores || T < 1) return SEMKV_EINVAL;
+  if (T > c->cfg.max_prompt) return SEMKV_ECAPACITY;
+  const int64_t kh = top_count(T, c->cfg.r_num, c->cfg.r_den);
+  if ((kh > 0 && !hi_idx) || (kh < T && !lo_idx)) return SEMKV_EINVAL;   // an empty list may be NULL
+  RankArgs a;
+  a.scores = scores;
+  a.T = T;
+  a.K = top_count(T, c->cfg.r_num, c->cfg.r_den);
+  a.ld_s = T;
+  a.flags = c->flags;
+  a.flag_words = c->sz.flag_words;
+  a.hi_idx = hi_idx;
+  a.lo_idx = lo_idx;
+  a.status = c->status;
+  return launch_rank(a, c->cfg.batch, stream);
+}
+
+int semkv_quantize_pack(semkv_cache* c, int32_t layer, const uint16_t* K, const uint16_t* V,
+                        int64_t sL, int64_t sB, int64_t sH, int64_t sT, int64_t T,
+                        const int32_t* hi_idx, const int32_t* lo_idx, hipStream_t stream) {
+  if (!c || !K || !V || T < 1) return SEMKV_EINVAL;
+  const semkv_config& k = c->cfg;
+  if (layer < -1 || layer >= k.n_layers) return SEMKV_EINVAL;
+  if (T > k.max_prompt) return SEMKV_ECAPACITY;
+  if (((uintptr_t(K) | uintptr_t(V)) & 15) || ((sB | sH | sT | (layer < 0 ? sL : 0)) & 7) || sT < 128)
+    return SEMKV_EINVAL;
+  int64_t kh = top_count(T, k.r_num, k.r_den);
+  if ((kh > 0 && !hi_idx) || (kh < T && !lo_idx)) return SEMKV_EINVAL;
+  bool fresh = c->n_hi == 0 && c->n_lo == 0 && c->n_prompt == 0;
+  bool same = c->n_prompt == T && c->n_hi == kh && c->n_lo == T - kh;
+  if (!fresh && !same) return SEMKV_ESTATE;   // generated blocks already closed
+  QuantArgs a;
+  memset(&a, 0, sizeof(a));
+  a.g = geom(c);
+  a.K = K;
+  a.V = V;
+  a.sL = sL;
+  a.sB = sB;
+  a.sH = sH;
+  a.sT = sT;
+  a.layer0 = layer < 0 ? 0 : layer;
+  a.n_layers_launched = layer < 0 ? k.n_layers : 1;
+  a.idx[0] = hi_idx;
+  a.idx[1] = lo_idx;
+  a.n_pool[0] = kh;
+  a.n_pool[1] = T - kh;
+  a.T = T;
+  int64_t mt = ((kh > T - kh ? kh : T - kh) + kSlots - 1) / kSlots;
+  a.max_tiles = int32_t(mt);
+  int st = launch_quantize(a, stream);
+  if (st) return st;
+  c->n_prompt = T;
+  c->n_hi = kh;
+  c->n_lo = T - kh;
+  return SEMKV_OK;
+}
+
+int semkv_append_kv(semkv_cache* c, int32_t layer, const uint16_t* k_new, const uint16_t* v_new,
+                    hipStream_t stream) {
+  if (!c || !k_new || !v_new) return SEMKV_EINVAL;
+  const semkv_config& k = c->cfg;
+  if (layer < -1 || layer >= k.n_layers) return SEMKV_EINVAL;
+  if (c->n_hi + c->n_lo + c->n_scored + 1 > k.max_prompt + k.max_new) return SEMKV_ECAPACITY;
+  if (c->n_scored >= kSlots) return SEMKV_ESTATE;
+  if ((uintptr_t(k_new) | uintptr_t(v_new)) & 3) return SEMKV_EINVAL;
+  AppendArgs a;
+  a.tail = c->tail;
+  a.k = k_new;
+  a.v = v_new;
+  a.layer0 = layer < 0 ? 0 : layer;
+  a.n_layers_launched = layer < 0 ? k.n_layers : 1;
+  a.n_layers = k.n_layers;
+  a.n_kv_heads = k.n_kv_heads;
+  a.batch = k.batch;
+  a.slot = c->n_scored;
+  int st = launch_append(a, stream);
+  if (st) return st;
+  for (int l = a.layer0; l < a.layer0 + a.n_layers_launched; ++l) c->appended[l >> 5] |= 1u << (l & 31);
+  return SEMKV_OK;
+}
+
+int semkv_append_commit(semkv_cache* c, const float* score_new, hipStream_t stream) {
+  if (!c || !score_new) return SEMKV_EINVAL;
+  if (!all_appended(c)) return SEMKV_ESTATE;
+  if (c->cfg.batch > 1024) return SEMKV_EUNSUPPORTED;
+  hipLaunchKernelGGL(store_score_kernel, dim3(1), dim3(1024), 0, stream, c->tail_scores, score_new,
+                     c->n_scored, c->cfg.batch);
+  if (hipGetLastError() != hipSuccess) return SEMKV_EHIP;
+  c->n_scored += 1;
+  memset(c->appended, 0, sizeof(c->appended));
+  if (c->n_scored == kSlots) return close_block(c, kSlots, stream);
+  return SEMKV_OK;
+}
+
+int semkv_flush(semkv_cache* c, hipStream_t stream) {
+  if (!c) return SEMKV_EINVAL;
+  if (!none_appended(c)) return SEMKV_ESTATE;
+  if (c->n_scored == 0) return SEMKV_OK;
+  return close_block(c, c->n_scored, stream);
+}
+
+int semkv_workspace_bytes(const semkv_cache* c, size_t* bytes) {
+  if (!c || !bytes) return SEMKV_EINVAL;
+  int chunk, ns[2], nsplit;
+  plan(c, 1, &chunk, ns, &nsplit);
+  *bytes = size_t(int64_t(c->cfg.batch) * c->cfg.n_kv_heads * nsplit * 4 * kPartial * 4);
+  return SEMKV_OK;
+}
+
+int semkv_decode_attn(const semkv_cache* c, int32_t layer, const uint16_t* q, float* out,
+                      void* workspace, size_t ws_bytes, hipStream_t stream) {
+  if (!c || !q || !out || !workspace) return SEMKV_EINVAL;
+  const semkv_config& k = c->cfg;
+  if (layer < 0 || layer >= k.n_layers) return SEMKV_EINVAL;
+  if ((uintptr_t(q) & 3) || (uintptr_t(workspace) & 15)) return SEMKV_EINVAL;
+  int n_tail = c->n_scored + (((c->appended[layer >> 5] >> (layer & 31)) & 1u) ? 1 : 0);
+  DecodeArgs a;
+  memset(&a, 0, sizeof(a));
+  int chunk, ns[2], nsplit;
+  plan(c, n_tail, &chunk, ns, &nsplit);
+  if (nsplit == 0) return SEMKV_ESTATE;      // nothing cached yet
+  size_t need = size_t(int64_t(k.batch) * k.n_kv_heads * nsplit * 4 * kPartial * 4);
+  if (ws_bytes < need) return SEMKV_EINVAL;
+  a.g = geom(c);
+  a.tail = c->tail;
+  a.q = q;
+  a.ws = static_cast<float*>(workspace);
+  a.out = out;
+  a.layer = layer;
+  a.n_rows[0] = c->n_hi;
+  a.n_rows[1] = c->n_lo;
+  a.n_tail = n_tail;
+  a.chunk = chunk;
+  a.ns[0] = ns[0];
+  a.ns[1] = ns[1];
+  a.nsplit = nsplit;
+  memcpy(a.mu[0], c->mu_hi, sizeof(a.mu[0]));
+  memcpy(a.mu[1], c->mu_lo, sizeof(a.mu[1]));
+  return launch_decode(a, stream);
+}
+
+}  // extern "C"

@@ -1,0 +1,86 @@
+// semkv_internal.h -- argument blocks and launchers shared by the host API
+// (semkv_api.hip) and the kernels (rank.hip, quant.hip, decode.hip).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "semkv_fmt.h"
+
+namespace semkv {
+
+// Per-pool view of the storage of one cache, as kernels need it.
+struct PoolGeom {
+  uint8_t* pools;          // device base of all units
+  int64_t unit_stride;     // bytes per (b, layer, kv head) unit
+  int64_t lo_offset;       // byte offset of the low pool inside a unit
+  int32_t rec_bytes[2];    // record bytes of the high / low pool
+  int32_t tile_bytes[2];   // body bytes of the high / low pool
+  int32_t meta_bytes;      // bytes of one K or V metadata block
+  int32_t L[2];            // levels of the high / low pool
+  int32_t base, G, n_layers, n_kv_heads, batch;
+  float tau[2][16];        // tq thresholds of the high / low pool
+  const uint32_t* signs;   // tq sign masks [n_layers][n_kv_heads][4]
+  int32_t* status;         // device status word
+};
+
+__host__ __device__ inline int64_t unit_offset(const PoolGeom& g, int b, int l, int h) {
+  return ((int64_t(b) * g.n_layers + l) * g.n_kv_heads + h) * g.unit_stride;
+}
+
+struct RankArgs {
+  const float* scores; int64_t T, K, ld_s;
+  uint32_t* flags; int64_t flag_words;
+  int32_t* hi_idx; int32_t* lo_idx;
+  int32_t* status;
+};
+
+struct QuantArgs {
+  PoolGeom g;
+  const uint16_t* K; const uint16_t* V;
+  int64_t sL, sB, sH, sT;
+  int32_t layer0, n_layers_launched;
+  const int32_t* idx[2];   // [batch][n_pool[p]]
+  int64_t n_pool[2];
+  int64_t T;               // tokens per sequence (slot lists index [0, T))
+  int32_t max_tiles;
+};
+
+struct CloseArgs {
+  PoolGeom g;
+  const uint16_t* tail;    // [b][l][h][2][64][128]
+  const float* tail_scores;// [b][64]
+  int32_t n;               // scored rows in the block (1..64)
+  int32_t k_hi;            // rows of the block that take the high precision
+  int64_t n0[2];           // rows already in the high / low pool
+  uint32_t* flags; int64_t flag_words; int64_t pos0;  // token position of tail row 0
+};
+
+struct AppendArgs {
+  uint16_t* tail; const uint16_t* k; const uint16_t* v;
+  int32_t layer0, n_layers_launched, n_layers, n_kv_heads, batch, slot;
+};
+
+struct DecodeArgs {
+  PoolGeom g;
+  const uint16_t* tail;    // fp16 tail base
+  const uint16_t* q;       // [b][Hq][128]
+  float* ws;               // partials [b][kvh][nsplit][4][132]
+  float* out;              // [b][Hq][128]
+  int32_t layer;
+  int64_t n_rows[2];       // rows in the high / low pool
+  int32_t n_tail;          // fp16 tail rows visible to this layer
+  int32_t chunk;           // tiles per split
+  int32_t ns[2];           // splits over the high / low pool
+  int32_t nsplit;          // splits per unit (ns[0] + ns[1] + tail)
+  float mu[2][16];         // tq codebooks
+};
+
+constexpr int kPartial = 132;  // m, l, 2 pad, o[128]
+
+int launch_rank(const RankArgs& a, int batch, hipStream_t s);
+int launch_quantize(const QuantArgs& a, hipStream_t s);
+int launch_append(const AppendArgs& a, hipStream_t s);
+int launch_close(const CloseArgs& a, hipStream_t s);
+int launch_decode(const DecodeArgs& a, hipStream_t s);
+
+}  // namespace semkv

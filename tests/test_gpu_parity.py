@@ -1,0 +1,137 @@
+"""GPU parity of the HIP path (through the C ABI) against the oracle at sizes
+the oracle finishes in seconds: bit-exact flags, slot lists, packed bytes and
+metadata; decode attention within 2e-3 max-abs."""
+import numpy as np
+import pytest
+
+from oracle import oracle as O
+from tests import gpu_util as U
+from workloads import get_config, synth
+
+pytestmark = pytest.mark.gpu
+
+
+def _check_prefill(cfgw, T, n_layers=1, units=None, scores=None):
+    import torch
+    cache = U.make_cache(cfgw, T, n_layers=n_layers, max_new=0)
+    scores, hi, lo = U.prefill(cache, cfgw, T, scores=scores)
+    assert cache.status() == 0
+    hi, lo = hi.cpu().numpy(), lo.cpu().numpy()
+    K = O.top_count(T, cfgw.r_num, cfgw.r_den)
+    flags = []
+    for b in range(cfgw.batch):
+        f, ohi, olo = O.rank(scores[b], cfgw.r_num, cfgw.r_den)
+        assert np.array_equal(hi[b], ohi) and np.array_equal(lo[b], olo), "slot lists, seq %d" % b
+        assert np.array_equal(U.flags_bits(cache, b, T), f), "flags, seq %d" % b
+        flags.append(f)
+    if units is None:
+        units = [(b, l, h) for b in range(cfgw.batch) for l in range(n_layers) for h in range(cfgw.n_kv_heads)]
+    for (b, l, h) in units:
+        u = U.oracle_unit(cfgw, l, b, h, flags[b], T)
+        for p, n in ((0, K), (1, T - K)):
+            if n == 0:
+                continue
+            got = U.gpu_records(cache, b, l, h, p, n)
+            want = u.records(p)
+            assert got.shape == want.shape
+            if not np.array_equal(got, want):
+                bad = np.flatnonzero(got != want)
+                raise AssertionError("unit %s pool %d: %d bytes differ, first at %d" % ((b, l, h), p, bad.size, bad[0]))
+    return cache, flags
+
+
+def _check_decode(cache, cfgw, T, flags, layers, units=None, step=0):
+    import torch
+    for l in layers:
+        q = synth.query(cfgw, l, step)
+        out = cache.decode_attn(l, torch.from_numpy(q).cuda()).cpu().numpy()
+        out2 = cache.decode_attn(l, torch.from_numpy(q).cuda()).cpu().numpy()
+        assert np.array_equal(out, out2), "decode is not deterministic"
+        for b in range(cfgw.batch):
+            for h in range(cfgw.n_kv_heads):
+                if units is not None and (b, l, h) not in units:
+                    continue
+                u = U.oracle_unit(cfgw, l, b, h, flags[b], T)
+                want = u.attend(q[b, 4 * h:4 * h + 4].astype(np.float64))
+                U.assert_attention_close(out[b, 4 * h:4 * h + 4], want, "unit %s" % ((b, l, h),))
+
+
+def test_single_layer_t2048_g32_full_parity():
+    cfgw = get_config(0)
+    cache, flags = _check_prefill(cfgw, 2048)
+    _check_decode(cache, cfgw, 2048, flags, [0])
+
+
+@pytest.mark.parametrize("T", [1, 37, 64, 65, 1000])
+@pytest.mark.parametrize("G", [32, 64, 128])
+def test_ragged_lengths_and_groups(T, G):
+    cfgw = get_config(0, group=G, batch=2, n_kv_heads=2, n_q_heads=8)
+    cache, flags = _check_prefill(cfgw, T)
+    _check_decode(cache, cfgw, T, flags, [0])
+
+
+@pytest.mark.parametrize("r", [(0, 1), (1, 1), (1, 2)])
+def test_all_low_all_high_half(r):
+    cfgw = get_config(0, r_num=r[0], r_den=r[1], n_kv_heads=2, n_q_heads=8)
+    cache, flags = _check_prefill(cfgw, 300)
+    _check_decode(cache, cfgw, 300, flags, [0])
+
+
+def test_tied_scores_and_signed_zero():
+    cfgw = get_config(0, batch=3, n_kv_heads=1, n_q_heads=4)
+    T = 777
+    s = np.zeros((3, T), np.float32)
+    s[0] = 1.0                                            # all equal: lowest indices win
+    s[1] = np.where(np.arange(T) % 2, 0.0, -0.0)          # +0 and -0 tie
+    s[2] = np.random.default_rng(3).integers(0, 3, T).astype(np.float32)
+    s[2, 5] = np.inf
+    s[2, 6] = -np.inf
+    cache, flags = _check_prefill(cfgw, T, scores=s)
+    _check_decode(cache, cfgw, T, flags, [0])
+
+
+@pytest.mark.parametrize("levels", [(6, 4), (4, 3), (5, 3)])
+def test_other_affine_level_pairs(levels):
+    cfgw = get_config(0, L_hi=levels[0], L_lo=levels[1], n_kv_heads=2, n_q_heads=8, group=64)
+    cache, flags = _check_prefill(cfgw, 500)
+    _check_decode(cache, cfgw, 500, flags, [0])
+
+
+def test_turboquant_base_small():
+    cfgw = get_config(4, n_layers=2, n_kv_heads=2, n_q_heads=8)
+    cache, flags = _check_prefill(cfgw, 1500, n_layers=2)
+    _check_decode(cache, cfgw, 1500, flags, [0, 1])
+
+
+def test_constant_rows_quantize_exactly():
+    import torch
+    cfgw = get_config(0, n_kv_heads=1, n_q_heads=4, group=32)
+    T = 200
+    rng = np.random.default_rng(9)
+    K = np.repeat(rng.standard_normal((1, 1, T, 4)), 32, -1).astype(np.float16)
+    V = np.repeat(rng.standard_normal((1, 1, T, 4)), 32, -1).astype(np.float16)
+    cache = U.make_cache(cfgw, T, max_new=0)
+    s = synth.all_scores(cfgw, T)
+    U.prefill(cache, cfgw, T, scores=s, kv=lambda l: (K, V))
+    q = synth.query(cfgw, 0, 0)
+    out = cache.decode_attn(0, torch.from_numpy(q).cuda()).cpu().numpy()
+    want = O.attention(q[0, :4].astype(np.float64), K[0, 0].astype(np.float64), V[0, 0].astype(np.float64))
+    U.assert_attention_close(out[0, :4], want, "constant rows")
+
+
+def test_status_word_reports_nan_and_inf():
+    import torch
+    cfgw = get_config(0, n_kv_heads=1, n_q_heads=4)
+    T = 100
+    s = synth.all_scores(cfgw, T)
+    s[0, 7] = np.nan
+    cache = U.make_cache(cfgw, T, max_new=0)
+    cache.rank(torch.from_numpy(s).cuda())
+    torch.cuda.synchronize()
+    assert cache.status() & 1
+    K, V = synth.layer_kv(cfgw, 0, T)
+    K[0, 0, 3, 9] = np.inf
+    cache2 = U.make_cache(cfgw, T, max_new=0)
+    s2 = synth.all_scores(cfgw, T)
+    U.prefill(cache2, cfgw, T, scores=s2, kv=lambda l: (K, V))
+    assert cache2.status() & 2
