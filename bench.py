@@ -1,0 +1,242 @@
+#!/usr/bin/env python
+"""Benchmark of the SemKV hot path on one MI355X.
+
+Workload (default): Llama-3.1-8B KV geometry, 32 layers x 8 KV heads x 128,
+32 query heads, batch 1, 32768-token prompt; importance scores Zipf(1.1); the
+top 26 % of tokens at 6 levels (2.585 b), the rest at 5 levels (2.322 b);
+affine base with fp16 scale/zero per 128-channel row.  Inputs are seeded
+synthetic tensors generated on the device.
+
+Timed step: one decoded token of every sequence through all 32 layers, i.e.
+32 launches of the split-K decode attention kernel over the mixed-precision
+cache (pools resident in HBM).  The K timed steps are one HIP graph replay
+bracketed by events and device synchronization.  The prefill path (rank,
+quantize + pack) is timed separately and reported beside it.
+
+Prints one JSON line.  --gpus N with N > 1 is refused: this build runs on
+one GPU.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, AMD published peak
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=128)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="llama8b_kv_b1_t32768_affine")
+    ap.add_argument("--group", type=int, default=None, help="override the affine metadata group")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0, help="budget of the oracle sample")
+    return ap.parse_args()
+
+
+def algorithmic_decode_bytes(cfgw, n_hi, n_lo):
+    """Bytes one decode launch (one layer) must move: the packed K and V codes
+    of every cached token (row-exact mixed-radix bits), their metadata, the
+    query and the output."""
+    from paper_2608_28911_amd.fmt import line_bits
+    meta = (128 // cfgw.group) * 4 if cfgw.base == "affine" else 2
+    per_hi = 2 * line_bits(cfgw.L_hi, 128) / 8 + 2 * meta
+    per_lo = 2 * line_bits(cfgw.L_lo, 128) / 8 + 2 * meta
+    units = cfgw.batch * cfgw.n_kv_heads
+    qo = cfgw.batch * cfgw.n_q_heads * 128 * (2 + 4)
+    return units * (n_hi * per_hi + n_lo * per_lo) + qo
+
+
+def cpu_baseline(cfgw, seconds):
+    """The oracle, as it stands, on a bounded sample: decode attention of whole
+    (layer, kv head) units at the workload's context length."""
+    from oracle import oracle as O
+    from workloads import synth
+    T = cfgw.prompt_len
+    base = 0 if cfgw.base == "affine" else 1
+    units, t_attn, t_quant, q_bytes = 0, 0.0, 0.0, 0
+    s = synth.scores(cfgw, 0, T)
+    flag, _, _ = O.rank(s, cfgw.r_num, cfgw.r_den)
+    l = 0
+    while t_attn + t_quant < seconds and units < cfgw.n_layers * cfgw.n_kv_heads:
+        h = units % cfgw.n_kv_heads
+        l = units // cfgw.n_kv_heads
+        K, V = synth.unit_kv(cfgw, l, 0, h, T)
+        u = O.UnitCache(base, cfgw.L_hi, cfgw.L_lo, cfgw.group, cfgw.r_num, cfgw.r_den,
+                        sign_words=synth.sign_words(cfgw, l, h) if base else None)
+        t0 = time.perf_counter()
+        u.prefill(K, V, flag)
+        u.records(0)
+        u.records(1)
+        t_quant += time.perf_counter() - t0
+        q_bytes += K.nbytes + V.nbytes
+        q = synth.query(cfgw, l, 0)[0, 4 * h:4 * h + 4].astype(np.float64)
+        t0 = time.perf_counter()
+        u.attend(q)
+        t_attn += time.perf_counter() - t0
+        units += 1
+    per_unit = t_attn / units
+    units_per_step = cfgw.n_layers * cfgw.batch * cfgw.n_kv_heads
+    threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    return {
+        "value": 1.0 / (per_unit * units_per_step) * cfgw.batch,
+        "unit": "tokens/s",
+        "cores": min(threads, 4),
+        "kind": "oracle",
+        "sample": "%d (layer, kv head) units of batch 0 at T=%d: fp64 dequantize + softmax "
+                  "attention of 4 query heads, %.2f s/unit, scaled to %d units per token"
+                  % (units, T, per_unit, units_per_step),
+        "quantize_pack_gbps": q_bytes / t_quant / 1e9,
+        "quantize_pack_cores": threads,
+    }
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print("bench.py: this build runs on one GPU; --gpus %d is not supported "
+              "(the multi-GPU sharding plan is described in DESIGN.md)" % args.gpus, file=sys.stderr)
+        sys.exit(2)
+    import torch
+    import paper_2608_28911_amd as P
+    from workloads import get_config, synth
+
+    cfgw = get_config(args.workload)
+    if args.group:
+        from dataclasses import replace
+        cfgw = replace(cfgw, group=args.group)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    B, H, Hq, T, nL = cfgw.batch, cfgw.n_kv_heads, cfgw.n_q_heads, cfgw.prompt_len, cfgw.n_layers
+    base = P.BASE_AFFINE if cfgw.base == "affine" else P.BASE_TQ
+    cfg = P.make_config(n_layers=nL, n_kv_heads=H, batch=B, base=base, L_hi=cfgw.L_hi, L_lo=cfgw.L_lo,
+                        group=cfgw.group, r_num=cfgw.r_num, r_den=cfgw.r_den, max_prompt=T, max_new=0)
+    signs = synth.all_sign_words(cfgw) if base == P.BASE_TQ else None
+    cache = P.SemKVCache(cfg, sign_words=signs)
+
+    # ---- synthetic inputs, resident in HBM
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(cfgw.seed)
+    K = torch.empty((nL, B, H, T, 128), dtype=torch.float16, device=dev)
+    V = torch.empty_like(K)
+    for l in range(nL):
+        k = torch.randn((B, H, T, 128), generator=gen, device=dev, dtype=torch.float32)
+        ch = torch.randperm(128, generator=gen, device=dev)[:cfgw.outliers * H].view(H, cfgw.outliers)
+        for h in range(H):
+            k[:, h, :, ch[h]] *= cfgw.outlier_scale
+        K[l] = k.half()
+        V[l] = torch.randn((B, H, T, 128), generator=gen, device=dev, dtype=torch.float32).half()
+        del k
+    scores = torch.from_numpy(synth.all_scores(cfgw, T)).to(dev)
+    n_steps = args.warmup + args.steps
+    q = (torch.randn((n_steps, nL, B, Hq, 128), generator=gen, device=dev, dtype=torch.float32)).half()
+    out = torch.empty((nL, B, Hq, 128), dtype=torch.float32, device=dev)
+    torch.cuda.synchronize()
+
+    # ---- prefill: rank + quantize/pack, timed with events
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+    hi, lo = cache.rank(scores)
+    ev[0].record()
+    for _ in range(3):
+        hi, lo = cache.rank(scores)
+    ev[1].record()
+    cache.quantize_pack(-1, K, V, hi, lo)
+    torch.cuda.synchronize()
+    ev[2].record()
+    reps = 3
+    for _ in range(reps):
+        cache.quantize_pack(-1, K, V, hi, lo)
+    ev[3].record()
+    torch.cuda.synchronize()
+    assert cache.status() == 0, "device status word %d" % cache.status()
+    rank_us = ev[0].elapsed_time(ev[1]) / 3 * 1e3
+    quant_ms = ev[2].elapsed_time(ev[3]) / reps
+    n_hi, n_lo = cache.c.n_hi, cache.c.n_lo
+    t_hi, t_lo = -(-n_hi // 64), -(-n_lo // 64)
+    quant_bytes = 2 * K.numel() * 2 + nL * B * H * (t_hi * cache.sz.record_bytes_hi + t_lo * cache.sz.record_bytes_lo)
+    del K, V
+    torch.cuda.empty_cache()
+
+    # ---- decode: all timed steps captured in one graph
+    ws = cache.workspace()
+
+    def step(i):
+        for l in range(nL):
+            cache.decode_attn(l, q[i, l], out=out[l], workspace=ws)
+
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        for i in range(args.warmup):
+            step(i)
+        eager_last = None
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    # eager reference of the last timed step, to check the graph replays
+    step(n_steps - 1)
+    torch.cuda.synchronize()
+    eager_last = out.clone()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        for i in range(args.warmup, n_steps):
+            step(i)
+    torch.cuda.synchronize()
+    graph.replay()                           # warm replay (also a correctness check below)
+    torch.cuda.synchronize()
+    assert torch.equal(out, eager_last), "graph replay differs from eager decode"
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    graph.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    assert torch.equal(out, eager_last), "graph replay differs from eager decode"
+    ms = e0.elapsed_time(e1)
+    ms_per_step = ms / args.steps
+    launches = args.steps * nL
+    avg_launch_us = ms * 1e3 / launches
+    alg = algorithmic_decode_bytes(cfgw, n_hi, n_lo)
+    achieved = alg / (avg_launch_us * 1e-6) / 1e9
+    tokens_per_s = B * args.steps / (ms * 1e-3)
+
+    line = {
+        "metric": "mixed-prec decode attn tokens/s + effective HBM GB/s (% peak); quantize+pack GB/s",
+        "value": round(tokens_per_s, 2),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f16",
+        "data": "synthetic",
+        "config": {"workload": cfgw.name, "layers": nL, "batch": B, "context": T, "kv_heads": H,
+                   "q_heads": Hq, "head_dim": 128, "base": cfgw.base, "levels": [cfgw.L_hi, cfgw.L_lo],
+                   "r": cfgw.r_num / cfgw.r_den, "group": cfgw.group, "rows_hi": n_hi, "rows_lo": n_lo},
+        "effective_hbm_gbps": round(achieved, 1),
+        "effective_hbm_frac": round(achieved / HBM_PEAK_GBS, 4),
+        "decode_us_per_layer": round(avg_launch_us, 3),
+        "quantize_pack_gbps": round(quant_bytes / (quant_ms * 1e-3) / 1e9, 1),
+        "quantize_pack_ms": round(quant_ms, 3),
+        "rank_us": round(rank_us, 1),
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                     "kernel": "decode_kernel", "bytes_per_launch": int(alg)},
+    }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(cfgw, args.cpu_seconds)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -169,7 +169,8 @@ int semkv_append_commit(semkv_cache* c, const float* score_new, hipStream_t stre
  * round(r*n) high-precision tokens (nearest integer, ties to even). */
 int semkv_flush(semkv_cache* c, hipStream_t stream);
 
-/* Bytes of workspace semkv_decode_attn needs for this cache's current counts. */
+/* Bytes of workspace semkv_decode_attn needs for this cache's current counts
+ * (semkv_sizes.workspace_bytes bounds it for every count). */
 int semkv_workspace_bytes(const semkv_cache* c, size_t* bytes);
 
 /* Decode attention of one layer: for each sequence b and query head h (KV head
@@ -177,7 +178,10 @@ int semkv_workspace_bytes(const semkv_cache* c, size_t* bytes);
  * t of the sequence: both pools (dequantized on the fly) and the fp16 tail
  * rows appended so far, including this layer's current token if appended.
  * q: device fp16 [batch][n_q_heads][128]; out: device fp32, same shape.
- * workspace: device, ws_bytes >= semkv_workspace_bytes(). */
+ * workspace: device, ws_bytes >= semkv_workspace_bytes(); it starts with
+ * per-(sequence, kv head) counters that must be zero before the first call
+ * (allocate it zeroed); every call leaves them zero again.  One workspace may
+ * serve successive calls on one stream, not concurrent calls. */
 int semkv_decode_attn(const semkv_cache* c, int32_t layer, const uint16_t* q, float* out,
                       void* workspace, size_t ws_bytes, hipStream_t stream);
 

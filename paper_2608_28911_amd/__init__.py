@@ -113,7 +113,8 @@ class SemKVCache:
         import torch
         need = max(self.workspace_bytes(), 16)
         if self._ws is None or self._ws.numel() * 4 < need:
-            self._ws = torch.empty((need + 3) // 4, dtype=torch.float32, device=self.pools.device)
+            self._ws = torch.zeros((max(need, self.sz.workspace_bytes) + 3) // 4, dtype=torch.float32,
+                                   device=self.pools.device)
         return self._ws
 
     def decode_attn(self, layer, q, out=None, workspace=None):

@@ -18,8 +18,9 @@
 //   softmax online, base 2; unnormalized p, per-record rescale.
 //   values  C[16 channels x 16 cols] += A[16 x 32 tokens] B[32 tokens x 16]
 //           with A the V digits (V symbols run along tokens) and B = p * s.
-// Waves merge in LDS; a second kernel merges the splits (log-sum-exp) and, for
-// the TurboQuant-MSE base, applies the inverse random-sign Hadamard rotation.
+// Waves merge in LDS; the last workgroup of each (sequence, kv head) merges the
+// splits (log-sum-exp) and, for the TurboQuant-MSE base, applies the inverse
+// random-sign Hadamard rotation.
 #include <hip/hip_fp16.h>
 
 #include "semkv_internal.h"
@@ -425,6 +426,16 @@ __device__ void pool_split(const DecodeArgs& a, Shared& sm, int pool, int t_begi
   __syncthreads();
 }
 
+// Partials cross workgroups (and XCDs, whose L2 caches are not coherent with
+// each other): they are written and read with agent-scope atomic accesses,
+// which go to the coherent level without any cache write-back or invalidate.
+__device__ inline void st_agent(float* p, float v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ inline float ld_agent(const float* p) {
+  return __hip_atomic_load(const_cast<float*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 __device__ void write_partial(const DecodeArgs& a, Shared& sm, int b, int kvh, int split) {
   const int tid = threadIdx.x, h = tid >> 6, c = (tid & 63) * 2;
   float M = -INFINITY;
@@ -440,11 +451,11 @@ __device__ void write_partial(const DecodeArgs& a, Shared& sm, int b, int kvh, i
   }
   float* dst = a.ws + ((int64_t(b) * a.g.n_kv_heads + kvh) * a.nsplit + split) * 4 * kPartial + h * kPartial;
   if ((tid & 63) == 0) {
-    dst[0] = M;
-    dst[1] = Lsum;
+    st_agent(dst, M);
+    st_agent(dst + 1, Lsum);
   }
-  dst[4 + c] = o0;
-  dst[4 + c + 1] = o1;
+  st_agent(dst + 4 + c, o0);
+  st_agent(dst + 5 + c, o1);
 }
 
 // fp16 tail of generated tokens, plain vector arithmetic (at most 64 rows)
@@ -581,38 +592,88 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a) {
     tail_split<BASE>(a, sm, qorig, b, kvh);
   }
   write_partial(a, sm, b, kvh, split);
+  // the last workgroup of this (sequence, kv head) merges the splits: every
+  // thread waits for its partial stores (workgroup release), then one counter
+  // increment per workgroup at agent scope
+  __shared__ int last;
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+  __syncthreads();
+  if (tid == 0) {
+    uint32_t* ctr = a.counters + b * g.n_kv_heads + kvh;
+    uint32_t old = __hip_atomic_fetch_add(ctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    last = old == uint32_t(a.nsplit - 1);
+    if (last) __hip_atomic_store(ctr, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+  __syncthreads();
+  if (!last) return;
+  merge_splits<BASE>(a, sm, b, kvh);
 }
 
+// Merge of the splits of one (sequence, kv head), run by the last workgroup
+// to finish: log-sum-exp over the partials, then for the tq base the inverse
+// rotation o = sign . H o_rot.
 template <int BASE>
-__global__ __launch_bounds__(128) void merge_kernel(DecodeArgs a) {
-  __shared__ float o[kD];
-  const int h = blockIdx.x, b = blockIdx.y, c = threadIdx.x;
-  const int kvh = h >> 2, hh = h & 3;
-  const float* base = a.ws + (int64_t(b) * a.g.n_kv_heads + kvh) * a.nsplit * 4 * kPartial + hh * kPartial;
-  float M = -INFINITY;
-  for (int s = 0; s < a.nsplit; ++s) M = fmaxf(M, base[s * 4 * kPartial]);
-  float Lsum = 0.0f, O = 0.0f;
-  for (int s = 0; s < a.nsplit; ++s) {
-    const float* p = base + s * 4 * kPartial;
-    float sc = p[0] == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(p[0] - M);
-    Lsum += p[1] * sc;
-    O += p[4 + c] * sc;
+__device__ void merge_splits(const DecodeArgs& a, Shared& sm, int b, int kvh) {
+  const int tid = threadIdx.x, h = tid >> 6, c = (tid & 63) * 2;
+  const int ns = a.nsplit;
+  const float* unit = a.ws + (int64_t(b) * a.g.n_kv_heads + kvh) * ns * 4 * kPartial;
+  float* mm = &sm.u.pp[0][0][0];           // [ns][4] maxima, then [ns][4] sums
+  float* ll = mm + kMaxSplits * 4;
+  for (int i = tid; i < ns * 4; i += 256) {
+    mm[i] = ld_agent(unit + i * kPartial);
+    ll[i] = ld_agent(unit + i * kPartial + 1);
   }
-  float x = O / Lsum;
-  if (BASE == 1) {                         // o = sign . H o_rot
-    o[c] = x;
+  __syncthreads();
+  float M = -INFINITY;
+  for (int s = 0; s < ns; ++s) M = fmaxf(M, mm[s * 4 + h]);
+  float Lsum = 0.0f, o0 = 0.0f, o1 = 0.0f;
+  const float* op = unit + h * kPartial + 4 + c;
+  int s = 0;
+  for (; s + 4 <= ns; s += 4) {              // four splits' loads in flight
+    float x[4][2];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      x[k][0] = ld_agent(op + (s + k) * 4 * kPartial);
+      x[k][1] = ld_agent(op + (s + k) * 4 * kPartial + 1);
+    }
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      float m = mm[(s + k) * 4 + h];
+      float sc = m == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(m - M);
+      Lsum += ll[(s + k) * 4 + h] * sc;
+      o0 += x[k][0] * sc;
+      o1 += x[k][1] * sc;
+    }
+  }
+  for (; s < ns; ++s) {
+    float m = mm[s * 4 + h];
+    float sc = m == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(m - M);
+    Lsum += ll[s * 4 + h] * sc;
+    o0 += ld_agent(op + s * 4 * kPartial) * sc;
+    o1 += ld_agent(op + s * 4 * kPartial + 1) * sc;
+  }
+  o0 /= Lsum;
+  o1 /= Lsum;
+  if (BASE == 1) {
+    __syncthreads();
+    sm.q[h][c] = o0;
+    sm.q[h][c + 1] = o1;
     __syncthreads();
     for (int hs = 1; hs < kD; hs <<= 1) {
-      float y = o[c ^ hs];
-      float v = (c & hs) ? y - o[c] : o[c] + y;
+      int i = tid & 63;
+      int lo = (i / hs) * 2 * hs + (i % hs), hi = lo + hs;
+      float xa = sm.q[h][lo], ya = sm.q[h][hi];
       __syncthreads();
-      o[c] = v;
+      sm.q[h][lo] = xa + ya;
+      sm.q[h][hi] = xa - ya;
       __syncthreads();
     }
     const uint32_t* sw = a.g.signs + (int64_t(a.layer) * a.g.n_kv_heads + kvh) * 4;
-    x = ((sw[c >> 5] >> (c & 31)) & 1u) ? -o[c] : o[c];
+    o0 = ((sw[c >> 5] >> (c & 31)) & 1u) ? -sm.q[h][c] : sm.q[h][c];
+    o1 = ((sw[(c + 1) >> 5] >> ((c + 1) & 31)) & 1u) ? -sm.q[h][c + 1] : sm.q[h][c + 1];
   }
-  a.out[(int64_t(b) * a.g.n_kv_heads * 4 + h) * kD + c] = x;
+  float2* dst = reinterpret_cast<float2*>(a.out + ((int64_t(b) * a.g.n_kv_heads + kvh) * 4 + h) * kD + c);
+  *dst = make_float2(o0, o1);
 }
 
 template <int BASE, int LH, int LL>
@@ -621,7 +682,6 @@ int launch_dec(const DecodeArgs& a, hipStream_t st) {
   if (BASE == 1 || a.g.G == 128) hipLaunchKernelGGL((decode_kernel<BASE, LH, LL, 128>), grid, dim3(256), 0, st, a);
   else if (a.g.G == 64) hipLaunchKernelGGL((decode_kernel<BASE, LH, LL, 64>), grid, dim3(256), 0, st, a);
   else hipLaunchKernelGGL((decode_kernel<BASE, LH, LL, 32>), grid, dim3(256), 0, st, a);
-  hipLaunchKernelGGL((merge_kernel<BASE>), dim3(a.g.n_kv_heads * 4, a.g.batch), dim3(128), 0, st, a);
   return hipGetLastError() == hipSuccess ? 0 : -5;
 }
 

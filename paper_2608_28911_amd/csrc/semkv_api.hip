@@ -90,12 +90,21 @@ void plan(const semkv_cache* c, int n_tail, int* chunk, int ns[2], int* nsplit) 
   int64_t nt0 = (c->n_hi + kSlots - 1) / kSlots, nt1 = (c->n_lo + kSlots - 1) / kSlots;
   int64_t total = int64_t(c->cfg.batch) * c->cfg.n_kv_heads * (nt0 + nt1);
   int64_t ch = (total + 1023) / 1024;
+  const int64_t cap = kMaxSplits - 3;        // two partial chunks and the tail
+  if (ch < (nt0 + nt1 + cap - 1) / cap) ch = (nt0 + nt1 + cap - 1) / cap;
   ch = (ch + 3) / 4 * 4;
   if (ch < 4) ch = 4;
   *chunk = int(ch);
   ns[0] = int((nt0 + ch - 1) / ch);
   ns[1] = int((nt1 + ch - 1) / ch);
   *nsplit = ns[0] + ns[1] + (n_tail > 0 ? 1 : 0);
+}
+
+// workspace: [b][kvh] uint32 counters (padded to 256 bytes), then the partials
+size_t counter_bytes(const semkv_config& k) { return size_t((int64_t(k.batch) * k.n_kv_heads * 4 + 255) / 256 * 256); }
+
+size_t workspace_need(const semkv_config& k, int nsplit) {
+  return counter_bytes(k) + size_t(int64_t(k.batch) * k.n_kv_heads * nsplit * 4 * kPartial * 4);
 }
 
 int close_block(semkv_cache* c, int n, hipStream_t stream) {
@@ -179,7 +188,7 @@ int semkv_cache_sizes(const semkv_config* cfg, semkv_sizes* out) {
   out->flag_words = (k.max_prompt + k.max_new + 31) / 32 + 1;
   out->flag_bytes = size_t(k.batch * out->flag_words * 4);
   int64_t max_split = out->cap_hi_tiles + out->cap_lo_tiles + 1;
-  out->workspace_bytes = size_t(int64_t(k.batch) * k.n_kv_heads * max_split * 4 * kPartial * 4);
+  out->workspace_bytes = workspace_need(k, int(max_split));
   return SEMKV_OK;
 }
 
@@ -352,7 +361,7 @@ int semkv_workspace_bytes(const semkv_cache* c, size_t* bytes) {
   if (!c || !bytes) return SEMKV_EINVAL;
   int chunk, ns[2], nsplit;
   plan(c, 1, &chunk, ns, &nsplit);
-  *bytes = size_t(int64_t(c->cfg.batch) * c->cfg.n_kv_heads * nsplit * 4 * kPartial * 4);
+  *bytes = workspace_need(c->cfg, nsplit);
   return SEMKV_OK;
 }
 
@@ -368,12 +377,12 @@ int semkv_decode_attn(const semkv_cache* c, int32_t layer, const uint16_t* q, fl
   int chunk, ns[2], nsplit;
   plan(c, n_tail, &chunk, ns, &nsplit);
   if (nsplit == 0) return SEMKV_ESTATE;      // nothing cached yet
-  size_t need = size_t(int64_t(k.batch) * k.n_kv_heads * nsplit * 4 * kPartial * 4);
-  if (ws_bytes < need) return SEMKV_EINVAL;
+  if (ws_bytes < workspace_need(k, nsplit)) return SEMKV_EINVAL;
   a.g = geom(c);
   a.tail = c->tail;
   a.q = q;
-  a.ws = static_cast<float*>(workspace);
+  a.counters = static_cast<uint32_t*>(workspace);
+  a.ws = reinterpret_cast<float*>(static_cast<uint8_t*>(workspace) + counter_bytes(k));
   a.out = out;
   a.layer = layer;
   a.n_rows[0] = c->n_hi;

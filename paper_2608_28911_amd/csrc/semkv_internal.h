@@ -65,6 +65,7 @@ struct DecodeArgs {
   const uint16_t* tail;    // fp16 tail base
   const uint16_t* q;       // [b][Hq][128]
   float* ws;               // partials [b][kvh][nsplit][4][132]
+  uint32_t* counters;      // [b][kvh] finished-split counters, zero between calls
   float* out;              // [b][Hq][128]
   int32_t layer;
   int64_t n_rows[2];       // rows in the high / low pool
@@ -76,6 +77,7 @@ struct DecodeArgs {
 };
 
 constexpr int kPartial = 132;  // m, l, 2 pad, o[128]
+constexpr int kMaxSplits = 256;   // splits per (sequence, kv head)
 
 int launch_rank(const RankArgs& a, int batch, hipStream_t s);
 int launch_quantize(const QuantArgs& a, hipStream_t s);

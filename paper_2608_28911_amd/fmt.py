@@ -1,0 +1,23 @@
+"""Size arithmetic of the packed format (the same rules as csrc/semkv_fmt.h),
+for byte accounting in the benchmark: a symbol packs n codes of base L in the
+least number of bits, n = 5, 4, 3, 5 for L = 3, 4, 5, 6 (mixed-radix packing,
+SemKV Sec. 4.1)."""
+
+DIGITS = {3: 5, 4: 4, 5: 3, 6: 5}
+
+
+def width(L, nd):
+    w = 0
+    while (1 << w) < L ** nd:
+        w += 1
+    return w
+
+
+def line_bits(L, nvalues):
+    """Bits of one line of nvalues codes (a 128-channel token row or a
+    64-slot channel column)."""
+    n = DIGITS[L]
+    bits = (nvalues // n) * width(L, n)
+    if nvalues % n:
+        bits += width(L, nvalues % n)
+    return bits
