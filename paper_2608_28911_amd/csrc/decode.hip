@@ -37,12 +37,22 @@ constexpr float kDigitScale = 262144.0f;   // 2^18: digit d is fed as d * 2^-18
 
 // ------------------------------------------------------------ traits ----
 
+__host__ __device__ constexpr int ipow(int b, int e) {
+  int r = 1;
+  for (int i = 0; i < e; ++i) r *= b;
+  return r;
+}
+
+// Chunk layout: 8 MFMA slots per lane group per chunk, filled by SPC symbols
+// of STRIDE slots each; slot_digit / slot_plane give the code a slot holds
+// (-1: a zero pad slot).  4-level codes of the tq base take two slots, their
+// low and high bit (the Lloyd-Max levels are affine in those bits).
 template <int BASE, int L>
 struct Traits {
   static constexpr int n = sym_digits(L);
   static constexpr int P = (BASE == 1 && L == 4) ? 2 : 1;   // MFMA slots per code
-  static constexpr int SPS = n * P;                          // slots per symbol
-  static constexpr int SPC = 8 / SPS;                        // symbols per chunk
+  static constexpr int SPC = (L == 5 || (L == 4 && BASE == 0)) ? 2 : 1;
+  static constexpr int STRIDE = 8 / SPC;
   static constexpr int SK = num_syms(L, kD), SV = num_syms(L, kSlots);
   static constexpr int NSK = (SK + 3) / 4, NSV = (SV + 3) / 4;
   static constexpr int NCK = (NSK + SPC - 1) / SPC, NCV = (NSV + SPC - 1) / SPC;
@@ -50,7 +60,24 @@ struct Traits {
   static constexpr int TB = tile_bytes(L);
   static constexpr int KSEGW = (NSK * W + 31) / 32;          // normalized dwords of a K segment
   static constexpr int VSEGW = (NSV * W + 31) / 32;
+  // decode table: symbol -> MFMA operand dwords (codes pre-shifted to d << 6).
+  // L = 6 splits a symbol into s mod 216 (3 codes) and s div 216 (2 codes).
+  static constexpr int EDW = STRIDE / 2;                     // dwords per table entry
+  static constexpr int NENT = L == 6 ? 216 : ipow(L, n);
+  static constexpr int LUTDW = L == 6 ? 216 * 2 + 36 : NENT * EDW;
+  static constexpr int LUTSTRIDE = (LUTDW + 63) / 64 * 64 + 16;   // replicas start 16 banks apart
 };
+
+template <int BASE, int L>
+__host__ __device__ constexpr int slot_digit(int w) {
+  return (BASE == 1 && L == 4) ? w / 2
+       : L == 6 ? (w < 3 ? w : (w == 4 || w == 5) ? w - 1 : -1)
+       : L == 5 ? (w < 3 ? w : -1)
+       : L == 3 ? (w < 5 ? w : -1)
+       : w;                                                  // affine L = 4
+}
+template <int BASE, int L>
+__host__ __device__ constexpr int slot_plane(int w) { return (BASE == 1 && L == 4) ? w % 2 : 0; }
 
 // floor(s / L^i) for every symbol s < L^n as (s*2^8 * M) >> 32 with
 // M = ceil(2^24 / L^i): one 24-bit high multiply.
@@ -117,64 +144,94 @@ __device__ inline void load_segment(const uint8_t* body, int bitoff, uint32_t (&
   for (int k = 0; k < NW; ++k) seg[k] = __builtin_amdgcn_alignbit(r[k + 1], r[k], sh);
 }
 
-// MFMA slots of symbol K of a segment: its codes (or, with two planes, the
-// low and high bit of each 4-level code); packed below as fp16 bit patterns.
-template <int BASE, int L, int K, int NW, int NS>
-__device__ inline void symbol_slots(const uint32_t (&seg)[NW], const uint32_t (&mask)[NS], uint32_t* slot) {
+// Decode tables in LDS (one replica per lane group), built once per workgroup.
+template <int BASE, int L>
+__device__ void build_lut(uint32_t* lut) {
   using Tr = Traits<BASE, L>;
-  if constexpr (K < NS) {
-    uint32_t v = field<K * Tr::W, Tr::W, NW>(seg) & mask[K];
-    uint32_t d[Tr::n];
-    digits_of<L, Tr::n>(v, d);
-#pragma unroll
-    for (int w = 0; w < Tr::SPS; ++w)
-      slot[w] = Tr::P == 1 ? d[w] : (d[w / 2] >> (w % 2)) & 1u;
-  } else {
-#pragma unroll
-    for (int w = 0; w < Tr::SPS; ++w) slot[w] = 0;
+  for (int i = threadIdx.x; i < 4 * Tr::LUTDW; i += blockDim.x) {
+    const int rep = i / Tr::LUTDW, e = i % Tr::LUTDW;
+    uint32_t w = 0;
+    if (L == 6) {
+      if (e < 432) {                    // table A: s mod 216 -> codes 0, 1, 2
+        const int v = e / 2;
+        w = e & 1 ? (uint32_t(v / 36) << 6) : (uint32_t(v % 6) << 6) | (uint32_t(v / 6 % 6) << 22);
+      } else {                          // table B: s div 216 -> codes 3, 4
+        const int v = e - 432;
+        w = (uint32_t(v % 6) << 6) | (uint32_t(v / 6) << 22);
+      }
+    } else {
+      const int v = e / Tr::EDW, k = e % Tr::EDW;   // dword k: slots 2k, 2k+1
+      uint32_t half[2];
+      for (int h = 0; h < 2; ++h) {
+        const int wsl = 2 * k + h, dg = slot_digit<BASE, L>(wsl);
+        uint32_t d = 0;
+        if (dg >= 0) {
+          uint32_t c = uint32_t(v);
+          for (int t = 0; t < dg; ++t) c /= uint32_t(L);
+          c %= uint32_t(L);
+          d = slot_plane<BASE, L>(wsl) ? (c >> 1) : (Tr::P == 2 ? (c & 1u) : c);
+        }
+        half[h] = d << 6;
+      }
+      w = half[0] | (half[1] << 16);
+    }
+    lut[rep * Tr::LUTSTRIDE + e] = w;
   }
 }
 
-// MFMA A operand of chunk C of a segment: symbols SPC*C .. SPC*C+SPC-1.
-template <int BASE, int L, int C, int NW, int NS>
-__device__ inline half8 chunk_operand(const uint32_t (&seg)[NW], const uint32_t (&mask)[NS]) {
+template <int BASE, int L, int K, int NW, int NS>
+__device__ inline uint32_t seg_symbol(const uint32_t (&seg)[NW], const uint32_t (&mask)[NS]) {
   using Tr = Traits<BASE, L>;
-  uint32_t slot[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-  symbol_slots<BASE, L, Tr::SPC * C, NW, NS>(seg, mask, slot);
-  if constexpr (Tr::SPC == 2) symbol_slots<BASE, L, Tr::SPC * C + 1, NW, NS>(seg, mask, slot + Tr::SPS);
-  uint4v r;                                   // two codes per dword, each as d << 6
-  r.x = (slot[0] | (slot[1] << 16)) << 6;
-  r.y = (slot[2] | (slot[3] << 16)) << 6;
-  r.z = (slot[4] | (slot[5] << 16)) << 6;
-  r.w = (slot[6] | (slot[7] << 16)) << 6;
+  if constexpr (K < NS) return field<K * Tr::W, Tr::W, NW>(seg) & mask[K];
+  else return 0u;
+}
+
+// MFMA operand of chunk C of a segment (symbols SPC*C ..), read from the tables
+template <int BASE, int L, int C, int NW, int NS>
+__device__ inline half8 chunk_operand(const uint32_t (&seg)[NW], const uint32_t (&mask)[NS], const uint32_t* lut) {
+  using Tr = Traits<BASE, L>;
+  uint4v r;
+  if constexpr (L == 6) {
+    const uint32_t v = seg_symbol<BASE, L, C, NW, NS>(seg, mask);
+    const uint32_t hi = mulhi24(v << 8, magic(6, 3));      // v div 216
+    const uint32_t lo = v - 216u * hi;
+    const uint2 a = *reinterpret_cast<const uint2*>(lut + 2 * lo);
+    r = uint4v{a.x, a.y, lut[432 + hi], 0u};
+  } else if constexpr (Tr::SPC == 2) {
+    const uint2 a = *reinterpret_cast<const uint2*>(lut + 2 * seg_symbol<BASE, L, 2 * C, NW, NS>(seg, mask));
+    const uint2 b = *reinterpret_cast<const uint2*>(lut + 2 * seg_symbol<BASE, L, 2 * C + 1, NW, NS>(seg, mask));
+    r = uint4v{a.x, a.y, b.x, b.y};
+  } else {
+    const uint4 a = *reinterpret_cast<const uint4*>(lut + 4 * seg_symbol<BASE, L, C, NW, NS>(seg, mask));
+    r = uint4v{a.x, a.y, a.z, a.w};
+  }
   return __builtin_bit_cast(half8, r);
 }
 
 template <int BASE, int L, int NW, int NS, int NC>
 __device__ inline float4v contract(const uint32_t (&seg)[NW], const uint32_t (&mask)[NS],
-                                   const half8 (&B)[NC], float4v acc) {
+                                   const half8 (&B)[NC], float4v acc, const uint32_t* lut) {
   static_assert(NC <= 11, "chunks");
-#define SEMKV_C(C) if constexpr (C < NC) acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(chunk_operand<BASE, L, C, NW, NS>(seg, mask), B[C], acc, 0, 0, 0);
+#define SEMKV_C(C) if constexpr (C < NC) acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(chunk_operand<BASE, L, C, NW, NS>(seg, mask, lut), B[C], acc, 0, 0, 0);
   SEMKV_C(0) SEMKV_C(1) SEMKV_C(2) SEMKV_C(3) SEMKV_C(4) SEMKV_C(5)
   SEMKV_C(6) SEMKV_C(7) SEMKV_C(8) SEMKV_C(9) SEMKV_C(10)
 #undef SEMKV_C
   return acc;
 }
 
-// slot e of chunk c of lane group j -> (line position, plane) or -1
+// slot e of chunk c of lane group j -> position in the line (channel or
+// token) and plane, or -1 for a pad slot or a position past the line
 template <int BASE, int L>
 __device__ inline int slot_pos(int nvals, int j, int c, int e, int& plane) {
   using Tr = Traits<BASE, L>;
-  plane = 0;
-  if (e >= Tr::SPC * Tr::SPS) return -1;
-  int k = Tr::SPC * c + e / Tr::SPS;
-  int w = e % Tr::SPS;
-  int dig = w / Tr::P;
-  plane = w % Tr::P;
-  int p = j + 4 * k;
-  int S = (nvals + Tr::n - 1) / Tr::n;
+  const int k = Tr::SPC * c + e / Tr::STRIDE, w = e % Tr::STRIDE;
+  const int dig = slot_digit<BASE, L>(w);
+  plane = slot_plane<BASE, L>(w);
+  if (dig < 0) return -1;
+  const int p = j + 4 * k;
+  const int S = (nvals + Tr::n - 1) / Tr::n;
   if (p >= S) return -1;
-  int nd = nvals - Tr::n * p < Tr::n ? nvals - Tr::n * p : Tr::n;
+  const int nd = nvals - Tr::n * p < Tr::n ? nvals - Tr::n * p : Tr::n;
   if (dig >= nd) return -1;
   return Tr::n * p + dig;
 }
@@ -197,231 +254,320 @@ __device__ inline int seg_off(int L, int nvals, int nlines, int j, int line) {
   return off + line * seg_bits(L, nvals, j);
 }
 
-struct Shared {
-  float q[4][kD];          // query of the 4 heads (rotated for tq)
-  float zw[16];            // per column: sum of q over its group (zero-point weight)
+__device__ inline float hf(uint16_t b) { return __half2float(__ushort_as_half(b)); }
+
+// fp16 weight arrays of one wave: [plane][hi|lo][head][group][80 token slots]
+// (slots 64..79 stay zero: chunk slots past the last token read them), then a
+// zero block that unused columns read at every plane offset.
+constexpr int kPvTok = 80;
+
+template <int BASE, int L, int G>
+struct Geo {
+  using Tr = Traits<BASE, L>;
+  static constexpr int MB = meta_bytes(BASE, G);
+  static constexpr int RB = 2 * Tr::TB + 2 * MB;
+  static constexpr int NLD = (RB + 1023) / 1024;            // 1 KB staging loads per record
+  static constexpr int NG = BASE == 0 ? kD / G : 2;          // score rows per head
+  static constexpr int NGV = BASE == 0 ? kD / G : 1;         // value groups
+  static constexpr int NPL = Tr::P;                          // value planes (tq, 4 levels: 2)
+  static constexpr bool LOPASS = NGV > 2;                    // low part in a second pass
+  static constexpr int PLSTRIDE = 2 * 4 * NGV * kPvTok;    // halves per plane
+  static constexpr int PV = (2 * NPL - 1) * PLSTRIDE + kPvTok;  // planes + zero block
+};
+
+template <int NLD, int PV, int LUT>
+struct SharedT {
+  alignas(16) uint8_t stage[4][2][NLD * 1024];   // two staged records per wave
+  alignas(16) uint32_t lut[4 * LUT];             // decode table, one replica per lane group
+  alignas(16) _Float16 pv[4][PV];               // per wave p*s weights, fp16 hi/lo
+  float q[4][kD];                                // query of the 4 heads (rotated for tq)
+  float zw[16];                                  // per (head, row group): sum of q
+  float zc[4][4][4];                             // per wave, head, group: sum p * zero
   union {
-    float pp[4][kSlots][16];           // per wave: p * s_V per (token, column)
-    struct {
-      float m[4][4], l[4][4];
-      float o[4][4][kD];
-    } mg;
-    struct {
-      float lg[4][kSlots];
-      float mx[4], sum[4];
-      float o[4][kD];
-    } tl;
+    struct { float m[4][4], l[4][4]; float o[4][4][kD]; } mg;
+    struct { float lg[4][kSlots]; float mx[4], sum[4]; float o[4][kD]; } tl;
+    struct { float mm[kMaxSplits * 4]; float ll[kMaxSplits * 4]; } mr;
   } u;
 };
 
-__device__ inline float hf(uint16_t b) { return __half2float(__ushort_as_half(b)); }
+template <int CTRL>
+__device__ inline float dpp(float x) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), CTRL, 0xF, 0xF, false));
+}
+// reductions over the 16 lanes of a row (row_ror 8, 4, 2, 1)
+__device__ inline float row_max16(float x) {
+  x = fmaxf(x, dpp<0x128>(x));
+  x = fmaxf(x, dpp<0x124>(x));
+  x = fmaxf(x, dpp<0x122>(x));
+  return fmaxf(x, dpp<0x121>(x));
+}
+__device__ inline float row_sum16(float x) {
+  x += dpp<0x128>(x);
+  x += dpp<0x124>(x);
+  x += dpp<0x122>(x);
+  return x + dpp<0x121>(x);
+}
 
-template <int BASE, int L, int G>
-__device__ void pool_split(const DecodeArgs& a, Shared& sm, int pool, int t_begin, int t_end,
+// LDS-staged segment: NW dwords starting at bit `bitoff` of an LDS body
+template <int NW>
+__device__ inline void lds_segment(const uint8_t* body, int bitoff, uint32_t (&seg)[NW]) {
+  const uint32_t* p = reinterpret_cast<const uint32_t*>(body) + (bitoff >> 5);
+  uint32_t r[NW + 1];
+#pragma unroll
+  for (int k = 0; k <= NW; ++k) r[k] = p[k];
+  const int sh = bitoff & 31;
+#pragma unroll
+  for (int k = 0; k < NW; ++k) seg[k] = __builtin_amdgcn_alignbit(r[k + 1], r[k], sh);
+}
+
+// Copy one record into a wave's LDS buffer with direct global->LDS loads
+// (16 bytes per lane per load; the last load may read past the record into
+// memory the pool allocation keeps as slack).
+template <int NLD>
+__device__ inline void stage_record(const uint8_t* rec, uint8_t* lds, int lane) {
+#pragma unroll
+  for (int j = 0; j < NLD; ++j)
+    __builtin_amdgcn_global_load_lds(rec + j * 1024 + lane * 16,
+                                     (__attribute__((address_space(3))) void*)(lds + j * 1024), 16, 0, 0);
+}
+
+template <int NLD>
+__device__ inline void wait_staged(bool one_more_in_flight) {
+  // vmcnt(NLD) while the next record's NLD loads are in flight, else vmcnt(0)
+  if (one_more_in_flight) __builtin_amdgcn_s_waitcnt(0x0F70 | (NLD & 15) | ((NLD >> 4) << 14));
+  else __builtin_amdgcn_s_waitcnt(0x0F70);
+  __asm__ volatile("" ::: "memory");   // no LDS read of the record moves above the wait
+}
+
+template <int BASE, int L, int G, class SH>
+__device__ void pool_split(const DecodeArgs& a, SH& sm, int pool, int t_begin, int t_end,
                            int b, int kvh) {
   using Tr = Traits<BASE, L>;
+  using Ge = Geo<BASE, L, G>;
   const PoolGeom& g = a.g;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  const int n = lane & 15, r = lane >> 4, kg = r;          // MFMA column / row group
-  const int hh = n >> 2, gg = n & 3;                       // head and group of column n
-  // score columns: affine, q of head h on group g; tq, high and low fp16 part of q_rot
-  constexpr int NG = BASE == 0 ? kD / G : 2;
-  // value columns: V group vg of column n; the weight p*s is split into fp16 high
-  // and low parts, the low part in the spare columns 4h + NGV + vg when NGV <= 2,
-  // else (G = 32) in a second MFMA pass
-  constexpr int NGV = BASE == 0 ? kD / G : 1;
-  constexpr bool LOPASS = NGV > 2;
-  const int vg = gg < NGV ? gg : (!LOPASS && gg < 2 * NGV ? gg - NGV : -1);
-  const bool vlo = gg >= NGV;
+  const int n = lane & 15, r = lane >> 4, kg = r;
   // tq: mu = -m, 0, m (L = 3) or -b, -a, a, b (L = 4)
   const float* mu = a.mu[pool];
   const float cS = BASE == 0 ? 1.0f : (L == 3 ? mu[2] / 128.0f : 1.0f / 128.0f);
   const float cZ = BASE == 0 ? 0.0f : (L == 3 ? -mu[2] / 128.0f : -mu[3] / 128.0f);
-  const float wP0 = BASE == 0 ? 1.0f : (L == 3 ? 1.0f : mu[3] - mu[2]);
-  const float wP1 = BASE == 0 ? 1.0f : (L == 3 ? 1.0f : mu[2] + mu[3]);
+  const float wP[2] = {BASE == 0 ? 1.0f : (L == 3 ? 1.0f : mu[3] - mu[2]),
+                       BASE == 0 ? 1.0f : (L == 3 ? 1.0f : mu[2] + mu[3])};
 
-  // score B operand: column n = 4h + g, slot -> channel
-  half8 Bq[Tr::NCK];
+  // ---- score A operand: row 4h + kq of lane row n; slot -> channel of lane group kg
+  half8 Aq[Tr::NCK];
+  {
+    const int h = n >> 2, kq = n & 3;
 #pragma unroll
-  for (int c = 0; c < Tr::NCK; ++c) {
-    _Float16 v[8];
+    for (int c = 0; c < Tr::NCK; ++c) {
+      _Float16 v[8];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      int pl;
-      int ch = slot_pos<BASE, L>(kD, kg, c, e, pl);
-      float x = 0.0f;
-      if (ch >= 0 && gg < NG) {
-        if (BASE == 0) {
-          x = (ch / G == gg) ? sm.q[hh][ch] : 0.0f;
-          v[e] = _Float16(x);
-        } else {
-          float w = (pl ? wP1 : wP0) * sm.q[hh][ch];
-          _Float16 h0 = _Float16(w);
-          v[e] = gg == 0 ? h0 : _Float16(w - float(h0));
-        }
-      } else {
+      for (int e = 0; e < 8; ++e) {
+        int pl;
+        const int ch = slot_pos<BASE, L>(kD, kg, c, e, pl);
         v[e] = _Float16(0.0f);
+        if (ch >= 0 && kq < Ge::NG) {
+          if (BASE == 0) {
+            if (ch / G == kq) v[e] = _Float16(sm.q[h][ch]);
+          } else {
+            const float w = wP[pl] * sm.q[h][ch];
+            const _Float16 hi = _Float16(w);
+            v[e] = kq == 0 ? hi : _Float16(w - float(hi));
+          }
+        }
       }
+      Aq[c] = half8{v[0], v[1], v[2], v[3], v[4], v[5], v[6], v[7]};
     }
-    Bq[c] = half8{v[0], v[1], v[2], v[3], v[4], v[5], v[6], v[7]};
   }
+  build_lut<BASE, L>(sm.lut);
+  const uint32_t* lut = sm.lut + kg * Tr::LUTSTRIDE;
   uint32_t kmask[Tr::NSK], vmask[Tr::NSV];
   segment_masks<BASE, L, kD>(kg, kmask, Tr::NSK);
   segment_masks<BASE, L, kSlots>(kg, vmask, Tr::NSV);
-  const int koff0 = seg_off(L, kD, kSlots, kg, 0), kstep = seg_bits(L, kD, kg);
-  const int voff0 = seg_off(L, kSlots, kD, kg, 0), vstep = seg_bits(L, kSlots, kg);
-  const float zwn = sm.zw[n];
+  const int koff0 = seg_off(L, kD, kSlots, kg, n), kstep = 16 * seg_bits(L, kD, kg);
+  const int voff0 = seg_off(L, kSlots, kD, kg, n), vstep = 16 * seg_bits(L, kSlots, kg);
+  // softmax lanes: token n of each 16-token block, head r
+  const int hs = r;
+  float zws[Ge::NG];
+#pragma unroll
+  for (int i = 0; i < Ge::NG; ++i) zws[i] = sm.zw[hs * 4 + i];
+  // value B operand lanes: column n = 4h + gg
+  const int hv = n >> 2, gg = n & 3;
+  const int vg = gg < Ge::NGV ? gg : (!Ge::LOPASS && gg < 2 * Ge::NGV ? gg - Ge::NGV : -1);
+  const bool vlo = gg >= Ge::NGV;
+  _Float16* pvw = sm.pv[wave];
+  constexpr int PLSTRIDE = Ge::PLSTRIDE;
+  const int pvzero = Ge::NPL * PLSTRIDE;
+  // base index (plane 0) of this lane's column, token 0 of its lane group's first symbol
+  const int pvcol = (vg >= 0 ? (((vlo ? 1 : 0) * 4 + hv) * Ge::NGV + vg) * kPvTok : pvzero) + Tr::n * kg;
+  const int pvlo_col = (vg >= 0 ? ((4 + hv) * Ge::NGV + vg) * kPvTok : pvzero) + Tr::n * kg;   // LOPASS
+  for (int i = lane; i < Ge::PV; i += 64) pvw[i] = _Float16(0.0f);
 
-  float m_run = -INFINITY, l_run = 0.0f, z_run = 0.0f;
+  float m_run = -INFINITY, l_run = 0.0f;
+  float z_run[Ge::NGV];
+#pragma unroll
+  for (int i = 0; i < Ge::NGV; ++i) z_run[i] = 0.0f;
   float4v acc_o[8];
 #pragma unroll
   for (int cb = 0; cb < 8; ++cb) acc_o[cb] = float4v{0, 0, 0, 0};
 
   const uint8_t* unit = g.pools + unit_offset(g, b, a.layer, kvh) + (pool ? g.lo_offset : 0);
   const int64_t nrows = a.n_rows[pool];
-  float (*pp)[16] = sm.u.pp[wave];
+  uint8_t* buf0 = sm.stage[wave][0];
+  uint8_t* buf1 = sm.stage[wave][1];
+  const int first = t_begin + wave;
+  const int count = first < t_end ? (t_end - first + 3) / 4 : 0;
+  if (count > 0) stage_record<Ge::NLD>(unit + int64_t(first) * Ge::RB, buf0, lane);
 
-  for (int tile = t_begin + wave; tile < t_end; tile += 4) {
-    const uint8_t* rec = unit + int64_t(tile) * g.rec_bytes[pool];
+  for (int it = 0; it < count; ++it) {
+    const int tile = first + 4 * it;
+    uint8_t* rec = (it & 1) ? buf1 : buf0;
+    if (it + 1 < count) {
+      __asm__ volatile("" ::: "memory");
+      __builtin_amdgcn_s_waitcnt(0xC07F);                  // lgkmcnt(0): last reads of that buffer done
+      stage_record<Ge::NLD>(unit + int64_t(tile + 4) * Ge::RB, (it & 1) ? buf0 : buf1, lane);
+      wait_staged<Ge::NLD>(true);
+    } else {
+      wait_staged<Ge::NLD>(false);
+    }
     const uint8_t* kmeta = rec + 2 * Tr::TB;
-    const uint8_t* vmeta = kmeta + g.meta_bytes;
+    const uint8_t* vmeta = kmeta + Ge::MB;
     const int nvalid = nrows - int64_t(tile) * kSlots < kSlots ? int(nrows - int64_t(tile) * kSlots) : kSlots;
 
-    // ---- scores
-    float lg[4][4];
+    // ---- scores: C[(h, kq)][token] = q_h,kq . codes; lane holds token n, head r
+    float lg[4];
 #pragma unroll
     for (int blk = 0; blk < 4; ++blk) {
       uint32_t seg[Tr::KSEGW];
-      load_segment<Tr::KSEGW>(rec, koff0 + (16 * blk + n) * kstep, seg);
-      float4v acc = contract<BASE, L, Tr::KSEGW, Tr::NSK, Tr::NCK>(seg, kmask, Bq, float4v{0, 0, 0, 0});
-      const int t0 = 16 * blk + 4 * r;
-      float sk[4], zk[4];
+      lds_segment<Tr::KSEGW>(rec, koff0 + blk * kstep, seg);
+      float4v acc = float4v{0, 0, 0, 0};
+#define SEMKV_S(C) if constexpr (C < Tr::NCK) acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(Aq[C], chunk_operand<BASE, L, C, Tr::KSEGW, Tr::NSK>(seg, kmask, lut), acc, 0, 0, 0);
+      SEMKV_S(0) SEMKV_S(1) SEMKV_S(2) SEMKV_S(3) SEMKV_S(4) SEMKV_S(5) SEMKV_S(6) SEMKV_S(7) SEMKV_S(8) SEMKV_S(9) SEMKV_S(10)
+#undef SEMKV_S
+      const int t = 16 * blk + n;
+      float x = 0.0f;
       if (BASE == 0) {
-        uint4 mt = gg < NG ? *reinterpret_cast<const uint4*>(kmeta + (gg * kSlots + t0) * 4) : uint4{0, 0, 0, 0};
-        uint32_t mm[4] = {mt.x, mt.y, mt.z, mt.w};
 #pragma unroll
-        for (int i = 0; i < 4; ++i) { sk[i] = hf(mm[i] & 0xFFFFu); zk[i] = hf(mm[i] >> 16); }
-      } else {
-        uint2 mt = *reinterpret_cast<const uint2*>(kmeta + t0 * 2);
-        uint32_t mm[2] = {mt.x, mt.y};
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          float rho = hf((mm[i >> 1] >> (16 * (i & 1))) & 0xFFFFu);
-          sk[i] = rho * cS;
-          zk[i] = rho * cZ;
+        for (int i = 0; i < Ge::NG; ++i) {
+          const uint32_t m = *reinterpret_cast<const uint32_t*>(kmeta + (i * kSlots + t) * 4);
+          x += acc[i] * hf(m & 0xFFFFu) + hf(m >> 16) * zws[i] * (1.0f / kDigitScale);
         }
+      } else {
+        const float rho = hf(*reinterpret_cast<const uint16_t*>(kmeta + t * 2));
+        x = (acc[0] + acc[1]) * (rho * cS) + rho * cZ * zws[0] * (1.0f / kDigitScale);
       }
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        float x = acc[i] * kDigitScale * sk[i] + zk[i] * zwn;
-        x += __shfl_xor(x, 1);
-        x += __shfl_xor(x, 2);
-        lg[blk][i] = (t0 + i < nvalid) ? x * (kLog2e * 0.08838834764831845f) : -INFINITY;
-      }
+      lg[blk] = t < nvalid ? x * (kDigitScale * kLog2e * 0.08838834764831845f) : -INFINITY;
     }
-    // ---- online softmax (base 2)
-    float mt = lg[0][0];
-#pragma unroll
-    for (int blk = 0; blk < 4; ++blk)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) mt = fmaxf(mt, lg[blk][i]);
-    mt = fmaxf(mt, __shfl_xor(mt, 16));
-    mt = fmaxf(mt, __shfl_xor(mt, 32));
+    // ---- online softmax (base 2) for head r over this record's 64 tokens
+    float mt = fmaxf(fmaxf(lg[0], lg[1]), fmaxf(lg[2], lg[3]));
+    mt = row_max16(mt);
     const float m_new = fmaxf(m_run, mt);
     const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
     m_run = m_new;
-    float lsum = 0.0f, zsum = 0.0f;
+    float lsum = 0.0f;
+#pragma unroll
+    for (int i = 0; i < Ge::NGV; ++i) z_run[i] *= alpha;
 #pragma unroll
     for (int blk = 0; blk < 4; ++blk) {
-      const int t0 = 16 * blk + 4 * r;
-      float sv[4], zv[4];
+      const int t = 16 * blk + n;
+      const float p = __builtin_amdgcn_exp2f(lg[blk] - m_new);   // 0 for masked tokens
+      lsum += p;
       if (BASE == 0) {
-        uint4 mt4 = vg >= 0 ? *reinterpret_cast<const uint4*>(vmeta + (vg * kSlots + t0) * 4) : uint4{0, 0, 0, 0};
-        uint32_t mm[4] = {mt4.x, mt4.y, mt4.z, mt4.w};
 #pragma unroll
-        for (int i = 0; i < 4; ++i) { sv[i] = hf(mm[i] & 0xFFFFu); zv[i] = vlo ? 0.0f : hf(mm[i] >> 16); }
-      } else {
-        uint2 mt2 = *reinterpret_cast<const uint2*>(vmeta + t0 * 2);
-        uint32_t mm[2] = {mt2.x, mt2.y};
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          float rho = hf((mm[i >> 1] >> (16 * (i & 1))) & 0xFFFFu);
-          sv[i] = vg >= 0 ? rho * cS : 0.0f;
-          zv[i] = gg == 0 ? rho * cZ : 0.0f;
+        for (int i = 0; i < Ge::NGV; ++i) {
+          const uint32_t m = *reinterpret_cast<const uint32_t*>(vmeta + (i * kSlots + t) * 4);
+          const float x = p * hf(m & 0xFFFFu);
+          const _Float16 hi = _Float16(x);
+          pvw[((0 * 4 + hs) * Ge::NGV + i) * kPvTok + t] = hi;
+          pvw[((1 * 4 + hs) * Ge::NGV + i) * kPvTok + t] = _Float16(x - float(hi));
+          z_run[i] += p * hf(m >> 16);
         }
-      }
+      } else {
+        const float rho = hf(*reinterpret_cast<const uint16_t*>(vmeta + t * 2));
+        const float ps = p * rho * cS;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        float p = __builtin_amdgcn_exp2f(lg[blk][i] - m_new);
-        bool ok = t0 + i < nvalid;
-        p = ok ? p : 0.0f;
-        lsum += p;
-        zsum += p * (ok ? zv[i] : 0.0f);
-        pp[t0 + i][n] = p * (ok ? sv[i] : 0.0f);
+        for (int pl = 0; pl < Ge::NPL; ++pl) {
+          const float x = ps * wP[pl];
+          const _Float16 hi = _Float16(x);
+          pvw[pl * PLSTRIDE + (0 * 4 + hs) * kPvTok + t] = hi;
+          pvw[pl * PLSTRIDE + (1 * 4 + hs) * kPvTok + t] = _Float16(x - float(hi));
+        }
+        z_run[0] += p * rho * cZ;
       }
     }
     l_run = l_run * alpha + lsum;
-    z_run = z_run * alpha + zsum;
+    // acc_o columns belong to head n >> 2: fetch that head's alpha
+    {
+      const float al[4] = {__builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, alpha), 0)),
+                           __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, alpha), 16)),
+                           __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, alpha), 32)),
+                           __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, alpha), 48))};
+      if (al[0] != 1.0f || al[1] != 1.0f || al[2] != 1.0f || al[3] != 1.0f) {
+        const float av = al[hv];
 #pragma unroll
-    for (int cb = 0; cb < 8; ++cb) acc_o[cb] *= alpha;
-    // p * s_V written by other lanes of this wave is read below
+        for (int cb = 0; cb < 8; ++cb) acc_o[cb] *= av;
+      }
+    }
+    // weights written above by other lanes of this wave are read below
     __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
     __builtin_amdgcn_wave_barrier();
 
-    // ---- values: B = p * s_V over the token slots of each chunk
-    half8 Bp[Tr::NCV], Bl[LOPASS ? Tr::NCV : 1];
+    // ---- values: C[channel][column] += V codes (tokens) x weights
+    half8 Bp[Tr::NCV], Bl[Ge::LOPASS ? Tr::NCV : 1];
 #pragma unroll
     for (int c = 0; c < Tr::NCV; ++c) {
       _Float16 v[8], w[8];
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        int pl;
-        int t = slot_pos<BASE, L>(kSlots, kg, c, e, pl);
-        float x = 0.0f;
-        if (t >= 0 && vg >= 0) x = pp[t][n] * (pl ? wP1 : wP0);
-        _Float16 h = _Float16(x);
-        _Float16 l = _Float16(x - float(h));
-        v[e] = vlo ? l : h;
-        w[e] = l;
+        // slot e -> token n*(kg + 4k) + digit; slots past the last token land
+        // in the zero slots 64..79 (pad slots of the chunk are plain zeros)
+        const int k = Tr::SPC * c + e / Tr::STRIDE;
+        const int dig = slot_digit<BASE, L>(e % Tr::STRIDE), pl = slot_plane<BASE, L>(e % Tr::STRIDE);
+        const bool pad = dig < 0;
+        const int toff = Tr::n * 4 * k + (pad ? 0 : dig);
+        v[e] = pad ? _Float16(0.0f) : pvw[pl * PLSTRIDE + pvcol + toff];
+        if constexpr (Ge::LOPASS) w[e] = pad ? _Float16(0.0f) : pvw[pl * PLSTRIDE + pvlo_col + toff];
       }
       Bp[c] = half8{v[0], v[1], v[2], v[3], v[4], v[5], v[6], v[7]};
-      if constexpr (LOPASS) Bl[c] = half8{w[0], w[1], w[2], w[3], w[4], w[5], w[6], w[7]};
+      if constexpr (Ge::LOPASS) Bl[c] = half8{w[0], w[1], w[2], w[3], w[4], w[5], w[6], w[7]};
     }
     const uint8_t* vbody = rec + Tr::TB;
 #pragma unroll
     for (int cb = 0; cb < 8; ++cb) {
       uint32_t seg[Tr::VSEGW];
-      load_segment<Tr::VSEGW>(vbody, voff0 + (16 * cb + n) * vstep, seg);
-      acc_o[cb] = contract<BASE, L, Tr::VSEGW, Tr::NSV, Tr::NCV>(seg, vmask, Bp, acc_o[cb]);
-      if constexpr (LOPASS) acc_o[cb] = contract<BASE, L, Tr::VSEGW, Tr::NSV, Tr::NCV>(seg, vmask, Bl, acc_o[cb]);
+      lds_segment<Tr::VSEGW>(vbody, voff0 + cb * vstep, seg);
+      acc_o[cb] = contract<BASE, L, Tr::VSEGW, Tr::NSV, Tr::NCV>(seg, vmask, Bp, acc_o[cb], lut);
+      if constexpr (Ge::LOPASS) acc_o[cb] = contract<BASE, L, Tr::VSEGW, Tr::NSV, Tr::NCV>(seg, vmask, Bl, acc_o[cb], lut);
     }
-    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
-    __builtin_amdgcn_wave_barrier();
   }
 
-  // ---- wave totals over the 4 row groups, then the workgroup merge
-  if constexpr (!LOPASS) {
+  // ---- wave totals: sums over the tokens of a row; fold low columns into high ones
+  l_run = row_sum16(l_run);
+#pragma unroll
+  for (int i = 0; i < Ge::NGV; ++i) z_run[i] = row_sum16(z_run[i]);
+  if constexpr (!Ge::LOPASS) {
 #pragma unroll
     for (int cb = 0; cb < 8; ++cb)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) acc_o[cb][i] += __shfl_xor(acc_o[cb][i], NGV);
+      for (int i = 0; i < 4; ++i)
+        acc_o[cb][i] += Ge::NGV == 1 ? dpp<0xB1>(acc_o[cb][i]) : dpp<0x4E>(acc_o[cb][i]);   // quad xor 1 / xor 2
   }
-  l_run += __shfl_xor(l_run, 16);
-  l_run += __shfl_xor(l_run, 32);
-  z_run += __shfl_xor(z_run, 16);
-  z_run += __shfl_xor(z_run, 32);
+  if (n == 0) {
+#pragma unroll
+    for (int i = 0; i < Ge::NGV; ++i) sm.zc[wave][hs][i] = z_run[i];
+  }
   __syncthreads();
-  if (r == 0 && gg == 0) {
-    sm.u.mg.m[wave][hh] = m_run;
-    sm.u.mg.l[wave][hh] = l_run;
+  if (n == 0) {
+    sm.u.mg.m[wave][hs] = m_run;
+    sm.u.mg.l[wave][hs] = l_run;
   }
 #pragma unroll
   for (int cb = 0; cb < 8; ++cb)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      int ch = 16 * cb + 4 * r + i;
-      bool mine = BASE == 0 ? (ch / G == gg) : (gg == 0);
-      if (mine) sm.u.mg.o[wave][hh][ch] = acc_o[cb][i] * kDigitScale + z_run;
+      const int ch = 16 * cb + 4 * r + i;
+      const bool mine = BASE == 0 ? (ch / G == gg) : (gg == 0);
+      if (mine) sm.u.mg.o[wave][hv][ch] = acc_o[cb][i] * kDigitScale + sm.zc[wave][hv][BASE == 0 ? gg : 0];
     }
   __syncthreads();
 }
@@ -436,7 +582,8 @@ __device__ inline float ld_agent(const float* p) {
   return __hip_atomic_load(const_cast<float*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-__device__ void write_partial(const DecodeArgs& a, Shared& sm, int b, int kvh, int split) {
+template <class SH>
+__device__ void write_partial(const DecodeArgs& a, SH& sm, int b, int kvh, int split) {
   const int tid = threadIdx.x, h = tid >> 6, c = (tid & 63) * 2;
   float M = -INFINITY;
 #pragma unroll
@@ -459,8 +606,8 @@ __device__ void write_partial(const DecodeArgs& a, Shared& sm, int b, int kvh, i
 }
 
 // fp16 tail of generated tokens, plain vector arithmetic (at most 64 rows)
-template <int BASE>
-__device__ void tail_split(const DecodeArgs& a, Shared& sm, float (*qorig)[kD], int b, int kvh) {
+template <int BASE, class SH>
+__device__ void tail_split(const DecodeArgs& a, SH& sm, float (*qorig)[kD], int b, int kvh) {
   const PoolGeom& g = a.g;
   const int tid = threadIdx.x;
   const int nt = a.n_tail;
@@ -536,7 +683,13 @@ __device__ void tail_split(const DecodeArgs& a, Shared& sm, float (*qorig)[kD], 
 
 template <int BASE, int LH, int LL, int G>
 __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a) {
-  __shared__ Shared sm;
+  using GH = Geo<BASE, LH, G>;
+  using GL = Geo<BASE, LL, G>;
+  constexpr int NLD = GH::NLD > GL::NLD ? GH::NLD : GL::NLD;
+  constexpr int PV = GH::PV > GL::PV ? GH::PV : GL::PV;
+  constexpr int LUT = Traits<BASE, LH>::LUTSTRIDE > Traits<BASE, LL>::LUTSTRIDE ? Traits<BASE, LH>::LUTSTRIDE
+                                                                                 : Traits<BASE, LL>::LUTSTRIDE;
+  __shared__ SharedT<NLD, PV, LUT> sm;
   __shared__ float qorig[4][kD];
   const int split = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
   const int tid = threadIdx.x;
@@ -612,13 +765,13 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a) {
 // Merge of the splits of one (sequence, kv head), run by the last workgroup
 // to finish: log-sum-exp over the partials, then for the tq base the inverse
 // rotation o = sign . H o_rot.
-template <int BASE>
-__device__ void merge_splits(const DecodeArgs& a, Shared& sm, int b, int kvh) {
+template <int BASE, class SH>
+__device__ void merge_splits(const DecodeArgs& a, SH& sm, int b, int kvh) {
   const int tid = threadIdx.x, h = tid >> 6, c = (tid & 63) * 2;
   const int ns = a.nsplit;
   const float* unit = a.ws + (int64_t(b) * a.g.n_kv_heads + kvh) * ns * 4 * kPartial;
-  float* mm = &sm.u.pp[0][0][0];           // [ns][4] maxima, then [ns][4] sums
-  float* ll = mm + kMaxSplits * 4;
+  float* mm = sm.u.mr.mm;                 // [ns][4] maxima
+  float* ll = sm.u.mr.ll;                 // [ns][4] sums
   for (int i = tid; i < ns * 4; i += 256) {
     mm[i] = ld_agent(unit + i * kPartial);
     ll[i] = ld_agent(unit + i * kPartial + 1);

@@ -182,7 +182,7 @@ int semkv_cache_sizes(const semkv_config* cfg, semkv_sizes* out) {
   out->record_bytes_lo = record_bytes(k.base, k.L_lo, k.group);
   out->unit_stride = out->cap_hi_tiles * out->record_bytes_hi + out->cap_lo_tiles * out->record_bytes_lo;
   int64_t units = int64_t(k.batch) * k.n_layers * k.n_kv_heads;
-  out->pool_bytes = size_t(units * out->unit_stride);
+  out->pool_bytes = size_t(units * out->unit_stride) + kStageSlack;   // staging loads read past the last record
   out->tail_bytes = size_t(units * 2 * kSlots * kD * 2);
   out->tail_score_bytes = size_t(k.batch) * kSlots * 4;
   out->flag_words = (k.max_prompt + k.max_new + 31) / 32 + 1;

@@ -78,6 +78,7 @@ struct DecodeArgs {
 
 constexpr int kPartial = 132;  // m, l, 2 pad, o[128]
 constexpr int kMaxSplits = 256;   // splits per (sequence, kv head)
+constexpr int kStageSlack = 1024; // bytes after the last record that staging loads may read
 
 int launch_rank(const RankArgs& a, int batch, hipStream_t s);
 int launch_quantize(const QuantArgs& a, hipStream_t s);
