@@ -236,22 +236,27 @@ __device__ inline int slot_pos(int nvals, int j, int c, int e, int& plane) {
   return Tr::n * p + dig;
 }
 
-template <int BASE, int L, int NVALS>
-__device__ inline void segment_masks(int j, uint32_t* mask, int ns) {
-  constexpr int n = sym_digits(L);
-  constexpr int S = num_syms(L, NVALS);
-  for (int k = 0; k < ns; ++k) {
-    int p = j + 4 * k;
-    if (p >= S) { mask[k] = 0; continue; }
-    int nd = NVALS - n * p < n ? NVALS - n * p : n;
-    mask[k] = (1u << width_of(L, nd)) - 1u;
-  }
+// masks of the symbols of segment j (zero past the line's last symbol)
+template <int L, int NVALS, int NLINES, int NS>
+__device__ inline void segment_masks(int j, uint32_t (&mask)[NS]) {
+  constexpr SegTable<L, NVALS, NLINES> t{};
+#pragma unroll
+  for (int k = 0; k < NS; ++k)
+    mask[k] = pick4(j, (1u << t.width[0][k]) - 1u, (1u << t.width[1][k]) - 1u,
+                    (1u << t.width[2][k]) - 1u, (1u << t.width[3][k]) - 1u);
 }
 
-__device__ inline int seg_off(int L, int nvals, int nlines, int j, int line) {
-  int off = 0;
-  for (int i = 0; i < j; ++i) off += nlines * seg_bits(L, nvals, i);
-  return off + line * seg_bits(L, nvals, j);
+// first bit of line `line` in segment j, and the bits one line of it takes
+template <int L, int NVALS, int NLINES>
+__device__ inline int seg_off(int j, int line) {
+  constexpr SegTable<L, NVALS, NLINES> t{};
+  return pick4(j, t.start[0], t.start[1], t.start[2], t.start[3]) +
+         line * pick4(j, t.bits[0], t.bits[1], t.bits[2], t.bits[3]);
+}
+template <int L, int NVALS, int NLINES>
+__device__ inline int seg_line_bits(int j) {
+  constexpr SegTable<L, NVALS, NLINES> t{};
+  return pick4(j, t.bits[0], t.bits[1], t.bits[2], t.bits[3]);
 }
 
 __device__ inline float hf(uint16_t b) { return __half2float(__ushort_as_half(b)); }
@@ -380,12 +385,13 @@ __device__ void pool_split(const DecodeArgs& a, SH& sm, int pool, int t_begin, i
     }
   }
   build_lut<BASE, L>(sm.lut);
+  __syncthreads();                      // every wave reads all of the tables
   const uint32_t* lut = sm.lut + kg * Tr::LUTSTRIDE;
   uint32_t kmask[Tr::NSK], vmask[Tr::NSV];
-  segment_masks<BASE, L, kD>(kg, kmask, Tr::NSK);
-  segment_masks<BASE, L, kSlots>(kg, vmask, Tr::NSV);
-  const int koff0 = seg_off(L, kD, kSlots, kg, n), kstep = 16 * seg_bits(L, kD, kg);
-  const int voff0 = seg_off(L, kSlots, kD, kg, n), vstep = 16 * seg_bits(L, kSlots, kg);
+  segment_masks<L, kD, kSlots>(kg, kmask);
+  segment_masks<L, kSlots, kD>(kg, vmask);
+  const int koff0 = seg_off<L, kD, kSlots>(kg, n), kstep = 16 * seg_line_bits<L, kD, kSlots>(kg);
+  const int voff0 = seg_off<L, kSlots, kD>(kg, n), vstep = 16 * seg_line_bits<L, kSlots, kD>(kg);
   // softmax lanes: token n of each 16-token block, head r
   const int hs = r;
   float zws[Ge::NG];

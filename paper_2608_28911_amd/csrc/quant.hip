@@ -153,16 +153,19 @@ template <int L, int NV, int NL>
 __device__ void pack_segment(const uint8_t* codes, int stride, int line, int j, uint32_t* body) {
   constexpr int n = sym_digits(L);
   constexpr int S = num_syms(L, NV);
+  constexpr SegTable<L, NV, NL> t{};
   uint64_t lo = 0, hi = 0;
   int nb = 0;
 #pragma unroll
-  for (int p0 = 0; p0 < S; p0 += 4) {
-    int p = p0 + j;
-    if (p < S) {
-      int nd = NV - n * p < n ? NV - n * p : n;
+  for (int k = 0; 4 * k < S; ++k) {
+    const int p = j + 4 * k;
+    const int w = pick4(j, t.width[0][k], t.width[1][k], t.width[2][k], t.width[3][k]);
+    const int nd = pick4(j, t.ndig[0][k], t.ndig[1][k], t.ndig[2][k], t.ndig[3][k]);
+    if (w > 0) {
       uint32_t v = 0;
-      for (int i = nd - 1; i >= 0; --i) v = v * L + codes[(n * p + i) * stride];
-      int w = width_of(L, nd);
+#pragma unroll
+      for (int i = n - 1; i >= 0; --i)
+        if (i < nd) v = v * L + codes[(n * p + i) * stride];
       if (nb < 64) {
         lo |= uint64_t(v) << nb;
         if (nb + w > 64) hi |= uint64_t(v) >> (64 - nb);
@@ -172,9 +175,8 @@ __device__ void pack_segment(const uint8_t* codes, int stride, int line, int j, 
       nb += w;
     }
   }
-  int off = seg_start(L, NV, NL, 0);
-  for (int i = 0; i < j; ++i) off += NL * seg_bits(L, NV, i);
-  off += line * seg_bits(L, NV, j);
+  const int off = pick4(j, t.start[0], t.start[1], t.start[2], t.start[3]) +
+                  line * pick4(j, t.bits[0], t.bits[1], t.bits[2], t.bits[3]);
   int w0 = off >> 5, sh = off & 31;
   uint32_t s[4] = {uint32_t(lo), uint32_t(lo >> 32), uint32_t(hi), uint32_t(hi >> 32)};
   uint32_t o[5];
@@ -193,22 +195,24 @@ template <int L, int NV, int NL>
 __device__ void unpack_segment(const uint32_t* body, int line, int j, uint8_t* codes, int stride) {
   constexpr int n = sym_digits(L);
   constexpr int S = num_syms(L, NV);
-  int off = 0;
-  for (int i = 0; i < j; ++i) off += NL * seg_bits(L, NV, i);
-  off += line * seg_bits(L, NV, j);
+  constexpr SegTable<L, NV, NL> t{};
+  int off = pick4(j, t.start[0], t.start[1], t.start[2], t.start[3]) +
+            line * pick4(j, t.bits[0], t.bits[1], t.bits[2], t.bits[3]);
 #pragma unroll
-  for (int p0 = 0; p0 < S; p0 += 4) {
-    int p = p0 + j;
-    if (p < S) {
-      int nd = NV - n * p < n ? NV - n * p : n;
-      int w = width_of(L, nd);
+  for (int k = 0; 4 * k < S; ++k) {
+    const int p = j + 4 * k;
+    const int w = pick4(j, t.width[0][k], t.width[1][k], t.width[2][k], t.width[3][k]);
+    const int nd = pick4(j, t.ndig[0][k], t.ndig[1][k], t.ndig[2][k], t.ndig[3][k]);
+    if (w > 0) {
       int wd = off >> 5, sh = off & 31;
       uint64_t pair = uint64_t(body[wd]) | (uint64_t(body[wd + 1]) << 32);
       uint32_t v = uint32_t(pair >> sh) & ((1u << w) - 1u);
-      for (int i = 0; i < nd; ++i) {
-        codes[(n * p + i) * stride] = uint8_t(v % L);
-        v /= L;
-      }
+#pragma unroll
+      for (int i = 0; i < n; ++i)
+        if (i < nd) {
+          codes[(n * p + i) * stride] = uint8_t(v % L);
+          v /= L;
+        }
       off += w;
     }
   }

@@ -83,4 +83,33 @@ __host__ __device__ constexpr int record_bytes(int base, int L, int G) {
   return 2 * tile_bytes(L) + 2 * meta_bytes(base, G);
 }
 
+// Per-segment geometry of a body of NL lines of NV codes as compile-time
+// tables: kernels that pick a segment by lane read constants rather than
+// re-running the loops above.
+template <int L, int NV, int NL>
+struct SegTable {
+  static_assert(num_syms(L, NV) <= 64, "segment symbols");
+  int start[4] = {0, 0, 0, 0};   // first bit of segment j
+  int bits[4] = {0, 0, 0, 0};    // bits of segment j in one line
+  int width[4][16] = {};         // width of the k-th symbol of segment j (0: none)
+  int ndig[4][16] = {};          // codes of that symbol
+  constexpr SegTable() {
+    for (int j = 0; j < 4; ++j) {
+      start[j] = seg_start(L, NV, NL, j);
+      bits[j] = seg_bits(L, NV, j);
+      for (int k = 0; k < 16; ++k) {
+        const int p = j + 4 * k;
+        width[j][k] = p < num_syms(L, NV) ? sym_width(L, NV, p) : 0;
+        ndig[j][k] = p < num_syms(L, NV) ? sym_ndig(L, NV, p) : 0;
+      }
+    }
+  }
+};
+
+// value of a 4-entry table at a run-time index, as selects
+template <typename T>
+__host__ __device__ inline T pick4(int j, T a, T b, T c, T d) {
+  return j == 0 ? a : j == 1 ? b : j == 2 ? c : d;
+}
+
 }  // namespace semkv
