@@ -69,8 +69,7 @@ typedef struct semkv_config {
 
 /* Sizes derived from a configuration (all in bytes unless named otherwise).
  * Storage layout (the packed format):
- *  pools:  [batch][n_layers][n_kv_heads] units of unit_stride bytes (plus 1 KB
- *          of slack read by the decode staging loads); a unit is
+ *  pools:  [batch][n_layers][n_kv_heads] units of unit_stride bytes; a unit is
  *          cap_hi_tiles high-precision records then cap_lo_tiles
  *          low-precision records.  A record holds 64 token slots:
  *            K body (tile_bytes)  V body (tile_bytes)  K meta  V meta

@@ -1,26 +1,31 @@
 // decode.hip -- split-K GQA decode attention over the mixed-precision cache
 // (the decoding consumer of SemKV, Sec. 3.1 and Alg. 1), for gfx950.
 //
-// Grid: (split, kv head, sequence); a split is a run of 64-slot records of one
-// pool (so one level count per workgroup) or the fp16 tail of generated
-// tokens.  A workgroup is 4 waves; each wave takes every 4th record of the
-// split and keeps its own online-softmax state for the 4 query heads of the
-// kv head.  Per record:
-//   scores  C[16 tokens x 16 cols] += A[16 x 32] B[32 x 16] on MFMA
-//           (v_mfma_f32_16x16x32_f16): A holds base-L digits decoded from the
-//           packed K symbols as fp16 bit patterns d << 6 (the subnormal
-//           d * 2^-18; the matrix core keeps full fp32 accuracy for
-//           subnormal inputs only when their leading bit is at or above
-//           mantissa bit 5, measured on gfx950),
-//           B holds q of head h restricted to group g in column 4h+g.  The
-//           affine dequantization x = s c + z is folded out:
+// Work split: the tiles of one (sequence, kv head) unit -- its high pool, then
+// its low pool -- are cut into nsplit balanced runs, one per workgroup, with
+// nsplit chosen by the host so that the whole grid is resident at once.  A
+// workgroup is kDecodeWaves waves; wave w takes tiles w, w + kDecodeWaves, ...
+// of its run and keeps its own online-softmax state for the 4 query heads of
+// the kv head.  Records are staged through registers: the next record's
+// 16-byte pieces are loaded while the current one is computed from the wave's
+// LDS buffer, then written over it.  Per record:
+//   scores  C[16 rows (head, group) x 16 tokens] += A B on MFMA
+//           (v_mfma_f32_16x16x32_f16): A holds the query restricted to one
+//           metadata group per row, B the base-L digits of 16 tokens, decoded
+//           from the packed K symbols through LDS tables straight into fp16
+//           bit patterns d << 6 (the subnormal d * 2^-18: the matrix core
+//           keeps full fp32 accuracy for subnormal inputs only when their
+//           leading bit is at or above mantissa bit 5, measured on gfx950).
+//           The affine dequantization x = s c + z is folded out:
 //           q.x = s (q.c) + z (sum q) per group.
-//   softmax online, base 2; unnormalized p, per-record rescale.
+//   softmax online, base 2; unnormalized p, rescaled when the maximum moves.
 //   values  C[16 channels x 16 cols] += A[16 x 32 tokens] B[32 tokens x 16]
-//           with A the V digits (V symbols run along tokens) and B = p * s.
-// Waves merge in LDS; the last workgroup of each (sequence, kv head) merges the
-// splits (log-sum-exp) and, for the TurboQuant-MSE base, applies the inverse
-// random-sign Hadamard rotation.
+//           with A the V digits (V symbols run along tokens) and B = p * s
+//           split into fp16 high and low parts.
+// The last run also takes the fp16 tail of generated tokens.  The waves'
+// states merge in LDS into one partial per workgroup; the last workgroup of a
+// unit to finish merges the partials (log-sum-exp) and, for the TurboQuant-MSE
+// base, applies the inverse random-sign Hadamard rotation.
 #include <hip/hip_fp16.h>
 
 #include "semkv_internal.h"
@@ -33,7 +38,10 @@ typedef float float4v __attribute__((ext_vector_type(4)));
 typedef uint32_t uint4v __attribute__((ext_vector_type(4)));
 
 constexpr float kLog2e = 1.4426950408889634f;
-constexpr float kDigitScale = 262144.0f;   // 2^18: digit d is fed as d * 2^-18
+constexpr float kRsqrtD = 0.08838834764831845f;   // 1 / sqrt(128)
+constexpr float kDigitScale = 262144.0f;          // 2^18: digit d is fed as d * 2^-18
+constexpr int kThreads = 64 * kDecodeWaves;
+constexpr int kQPad = 160;                         // query rows, zero past channel 127
 
 // ------------------------------------------------------------ traits ----
 
@@ -66,6 +74,9 @@ struct Traits {
   static constexpr int NENT = L == 6 ? 216 : ipow(L, n);
   static constexpr int LUTDW = L == 6 ? 216 * 2 + 36 : NENT * EDW;
   static constexpr int LUTSTRIDE = (LUTDW + 63) / 64 * 64 + 16;   // replicas start 16 banks apart
+  // largest query channel an A-operand slot addresses (past 127: a zero pad)
+  static constexpr int MAXCH = n * (3 + 4 * (SPC * NCK - 1)) + n - 1;
+  static_assert(MAXCH < kQPad, "query padding");
 };
 
 template <int BASE, int L>
@@ -99,27 +110,10 @@ __host__ __device__ constexpr bool magic_exact(int L) {
   }
   return true;
 }
-static_assert(magic_exact(3) && magic_exact(5) && magic_exact(6), "digit extraction");
+static_assert(magic_exact(6), "digit extraction");
 
 __device__ inline uint32_t mulhi24(uint32_t a, uint32_t b) {
   return uint32_t((uint64_t(a & 0xFFFFFFu) * uint64_t(b & 0xFFFFFFu)) >> 32);
-}
-
-template <int L, int ND>
-__device__ inline void digits_of(uint32_t s, uint32_t d[ND]) {
-  if constexpr (L == 4) {
-#pragma unroll
-    for (int i = 0; i < ND; ++i) d[i] = (s >> (2 * i)) & 3u;
-  } else {
-    uint32_t s8 = s << 8;
-    uint32_t F[ND];
-    F[0] = s;
-#pragma unroll
-    for (int i = 1; i < ND; ++i) F[i] = mulhi24(s8, magic(L, i));
-#pragma unroll
-    for (int i = 0; i + 1 < ND; ++i) d[i] = F[i] - __umul24(uint32_t(L), F[i + 1]);
-    d[ND - 1] = F[ND - 1];
-  }
 }
 
 // bits [OFF, OFF+W) of a normalized segment
@@ -133,51 +127,50 @@ __device__ inline uint32_t field(const uint32_t (&seg)[NW]) {
   }
 }
 
-template <int NW>
-__device__ inline void load_segment(const uint8_t* body, int bitoff, uint32_t (&seg)[NW]) {
-  const uint32_t* p = reinterpret_cast<const uint32_t*>(body) + (bitoff >> 5);
-  uint32_t r[NW + 1];
-#pragma unroll
-  for (int k = 0; k <= NW; ++k) r[k] = p[k];
-  int sh = bitoff & 31;
-#pragma unroll
-  for (int k = 0; k < NW; ++k) seg[k] = __builtin_amdgcn_alignbit(r[k + 1], r[k], sh);
+// ------------------------------------------------------ decode tables ----
+
+// Dword e of the decode table: MFMA slots 2k, 2k+1 of symbol value v (codes as
+// d << 6); for L = 6, entries 0..431 map s mod 216 to slots 0-3 and 432..467
+// map s div 216 to slots 4, 5.
+template <int BASE, int L>
+__host__ __device__ constexpr uint32_t lut_entry(int e) {
+  using Tr = Traits<BASE, L>;
+  if (L == 6) {
+    if (e < 432) {
+      const int v = e / 2;
+      return (e & 1) ? (uint32_t(v / 36) << 6) : (uint32_t(v % 6) << 6) | (uint32_t(v / 6 % 6) << 22);
+    }
+    const int v = e - 432;
+    return (uint32_t(v % 6) << 6) | (uint32_t(v / 6) << 22);
+  }
+  const int v = e / Tr::EDW, k = e % Tr::EDW;
+  uint32_t w = 0;
+  for (int h = 0; h < 2; ++h) {
+    const int wsl = 2 * k + h, dg = slot_digit<BASE, L>(wsl);
+    uint32_t d = 0;
+    if (dg >= 0) {
+      uint32_t c = uint32_t(v);
+      for (int t = 0; t < dg; ++t) c /= uint32_t(L);
+      c %= uint32_t(L);
+      d = slot_plane<BASE, L>(wsl) ? (c >> 1) : (Tr::P == 2 ? (c & 1u) : c);
+    }
+    w |= (d << 6) << (16 * h);
+  }
+  return w;
 }
 
-// Decode tables in LDS (one replica per lane group), built once per workgroup.
+// The table with its 4 replicas (one per lane group), as the LDS copy holds it.
 template <int BASE, int L>
-__device__ void build_lut(uint32_t* lut) {
-  using Tr = Traits<BASE, L>;
-  for (int i = threadIdx.x; i < 4 * Tr::LUTDW; i += blockDim.x) {
-    const int rep = i / Tr::LUTDW, e = i % Tr::LUTDW;
-    uint32_t w = 0;
-    if (L == 6) {
-      if (e < 432) {                    // table A: s mod 216 -> codes 0, 1, 2
-        const int v = e / 2;
-        w = e & 1 ? (uint32_t(v / 36) << 6) : (uint32_t(v % 6) << 6) | (uint32_t(v / 6 % 6) << 22);
-      } else {                          // table B: s div 216 -> codes 3, 4
-        const int v = e - 432;
-        w = (uint32_t(v % 6) << 6) | (uint32_t(v / 6) << 22);
-      }
-    } else {
-      const int v = e / Tr::EDW, k = e % Tr::EDW;   // dword k: slots 2k, 2k+1
-      uint32_t half[2];
-      for (int h = 0; h < 2; ++h) {
-        const int wsl = 2 * k + h, dg = slot_digit<BASE, L>(wsl);
-        uint32_t d = 0;
-        if (dg >= 0) {
-          uint32_t c = uint32_t(v);
-          for (int t = 0; t < dg; ++t) c /= uint32_t(L);
-          c %= uint32_t(L);
-          d = slot_plane<BASE, L>(wsl) ? (c >> 1) : (Tr::P == 2 ? (c & 1u) : c);
-        }
-        half[h] = d << 6;
-      }
-      w = half[0] | (half[1] << 16);
-    }
-    lut[rep * Tr::LUTSTRIDE + e] = w;
+struct LutImage {
+  alignas(16) uint32_t w[4 * Traits<BASE, L>::LUTSTRIDE];
+  constexpr LutImage() : w{} {
+    for (int rep = 0; rep < 4; ++rep)
+      for (int e = 0; e < Traits<BASE, L>::LUTDW; ++e) w[rep * Traits<BASE, L>::LUTSTRIDE + e] = lut_entry<BASE, L>(e);
   }
-}
+};
+
+template <int BASE, int L>
+__device__ const LutImage<BASE, L> kLutImage = LutImage<BASE, L>();
 
 template <int BASE, int L, int K, int NW, int NS>
 __device__ inline uint32_t seg_symbol(const uint32_t (&seg)[NW], const uint32_t (&mask)[NS]) {
@@ -219,23 +212,6 @@ __device__ inline float4v contract(const uint32_t (&seg)[NW], const uint32_t (&m
   return acc;
 }
 
-// slot e of chunk c of lane group j -> position in the line (channel or
-// token) and plane, or -1 for a pad slot or a position past the line
-template <int BASE, int L>
-__device__ inline int slot_pos(int nvals, int j, int c, int e, int& plane) {
-  using Tr = Traits<BASE, L>;
-  const int k = Tr::SPC * c + e / Tr::STRIDE, w = e % Tr::STRIDE;
-  const int dig = slot_digit<BASE, L>(w);
-  plane = slot_plane<BASE, L>(w);
-  if (dig < 0) return -1;
-  const int p = j + 4 * k;
-  const int S = (nvals + Tr::n - 1) / Tr::n;
-  if (p >= S) return -1;
-  const int nd = nvals - Tr::n * p < Tr::n ? nvals - Tr::n * p : Tr::n;
-  if (dig >= nd) return -1;
-  return Tr::n * p + dig;
-}
-
 // masks of the symbols of segment j (zero past the line's last symbol)
 template <int L, int NVALS, int NLINES, int NS>
 __device__ inline void segment_masks(int j, uint32_t (&mask)[NS]) {
@@ -271,28 +247,14 @@ struct Geo {
   using Tr = Traits<BASE, L>;
   static constexpr int MB = meta_bytes(BASE, G);
   static constexpr int RB = 2 * Tr::TB + 2 * MB;
-  static constexpr int NLD = (RB + 1023) / 1024;            // 1 KB staging loads per record
+  static constexpr int NLD = (RB + 1023) / 1024;            // 1 KB staging pieces per record
   static constexpr int NG = BASE == 0 ? kD / G : 2;          // score rows per head
   static constexpr int NGV = BASE == 0 ? kD / G : 1;         // value groups
   static constexpr int NPL = Tr::P;                          // value planes (tq, 4 levels: 2)
   static constexpr bool LOPASS = NGV > 2;                    // low part in a second pass
-  static constexpr int PLSTRIDE = 2 * 4 * NGV * kPvTok;    // halves per plane
+  static constexpr int PLSTRIDE = 2 * 4 * NGV * kPvTok;      // halves per plane
   static constexpr int PV = (2 * NPL - 1) * PLSTRIDE + kPvTok;  // planes + zero block
-};
-
-template <int NLD, int PV, int LUT>
-struct SharedT {
-  alignas(16) uint8_t stage[4][2][NLD * 1024];   // two staged records per wave
-  alignas(16) uint32_t lut[4 * LUT];             // decode table, one replica per lane group
-  alignas(16) _Float16 pv[4][PV];               // per wave p*s weights, fp16 hi/lo
-  float q[4][kD];                                // query of the 4 heads (rotated for tq)
-  float zw[16];                                  // per (head, row group): sum of q
-  float zc[4][4][4];                             // per wave, head, group: sum p * zero
-  union {
-    struct { float m[4][4], l[4][4]; float o[4][4][kD]; } mg;
-    struct { float lg[4][kSlots]; float mx[4], sum[4]; float o[4][kD]; } tl;
-    struct { float mm[kMaxSplits * 4]; float ll[kMaxSplits * 4]; } mr;
-  } u;
+  static_assert(RB % 16 == 0, "record pieces");
 };
 
 template <int CTRL>
@@ -325,35 +287,88 @@ __device__ inline void lds_segment(const uint8_t* body, int bitoff, uint32_t (&s
   for (int k = 0; k < NW; ++k) seg[k] = __builtin_amdgcn_alignbit(r[k + 1], r[k], sh);
 }
 
-// Copy one record into a wave's LDS buffer with direct global->LDS loads
-// (16 bytes per lane per load; the last load may read past the record into
-// memory the pool allocation keeps as slack).
-template <int NLD>
-__device__ inline void stage_record(const uint8_t* rec, uint8_t* lds, int lane) {
+// ------------------------------------------------------- kernel layout ----
+
+template <int BASE, int LH, int LL, int G>
+struct Plan {
+  using GH = Geo<BASE, LH, G>;
+  using GL = Geo<BASE, LL, G>;
+  static constexpr int NLD = GH::NLD > GL::NLD ? GH::NLD : GL::NLD;
+  static constexpr int PV = ((GH::PV > GL::PV ? GH::PV : GL::PV) + 7) / 8 * 8;
+  static constexpr int LUTH = 4 * Traits<BASE, LH>::LUTSTRIDE;   // dwords of the high-pool tables
+  static constexpr int LUTL = 4 * Traits<BASE, LL>::LUTSTRIDE;
+  static constexpr int NGV = GH::NGV;
+  static_assert(GH::NGV == GL::NGV && GH::LOPASS == GL::LOPASS, "pools share the value columns");
+};
+
+struct Fin { float m[4], l[4]; float o[4][kD]; };             // one wave's state, merged form
+struct TailScratch { float lg[4][kSlots]; float mx[4], sum[4]; float o[4][kD]; };
+
+template <class PL>
+struct Shared {
+  alignas(16) uint8_t stage[kDecodeWaves][PL::NLD * 1024];   // per wave: one record, later its Fin
+  alignas(16) uint32_t lut[PL::LUTH + PL::LUTL];             // decode tables: high pool, low pool
+  alignas(16) _Float16 pv[kDecodeWaves][PL::PV];             // per wave p*s weights, fp16 hi/lo
+  alignas(16) _Float16 qh[4][kQPad];                         // fp16 query (affine base)
+  alignas(16) float qf[4][kQPad];                            // fp32 query, rotated for tq
+  float qorig[4][kD];                                        // query as given (fp16 tail)
+  Fin tfin;                                                  // the fp16 tail's state
+  TailScratch ts;
+  float zpart[4][4];
+  float zw[16];                                              // per (head, group): sum of q
+  float zc[kDecodeWaves][4][4];                              // per wave, head, group: sum p * zero
+  int last;
+};
+
+template <class PL>
+__device__ inline Fin* wave_fin(Shared<PL>& sm, int w) { return reinterpret_cast<Fin*>(sm.stage[w]); }
+
+template <int NGV>
+struct WaveState {
+  float m, l, z[NGV];
+  float4v o[8];
+};
+
+// ---------------------------------------------------------- staging ----
+
+// piece j of lane l is bytes [1024 j + 16 l, +16) of a record, read through a
+// buffer descriptor bounded by the record's size: pieces past its end read 0
+// without touching memory, so every record takes the same NMAX loads
+constexpr int kBufferWord3 = 0x00020000;   // raw 32-bit data format (gfx9 family)
+
+template <int BASE, int LH, int LL, int G, int NMAX>
+__device__ inline void load_tile(const PoolGeom& g, const uint8_t* unit, int tile, int nt0, uint4 (&r)[NMAX], int lane) {
+  using PL = Plan<BASE, LH, LL, G>;
+  const bool hi = tile < nt0;
+  const int rb = hi ? PL::GH::RB : PL::GL::RB;
+  const uint8_t* rec = hi ? unit + int64_t(tile) * PL::GH::RB : unit + g.lo_offset + int64_t(tile - nt0) * PL::GL::RB;
+  const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(rec), 0, rb, kBufferWord3);
 #pragma unroll
-  for (int j = 0; j < NLD; ++j)
-    __builtin_amdgcn_global_load_lds(rec + j * 1024 + lane * 16,
-                                     (__attribute__((address_space(3))) void*)(lds + j * 1024), 16, 0, 0);
+  for (int j = 0; j < NMAX; ++j) {
+    const uint4v v = __builtin_amdgcn_raw_buffer_load_b128(rs, j * 1024 + lane * 16, 0, 0);
+    r[j] = make_uint4(v.x, v.y, v.z, v.w);
+  }
 }
 
-template <int NLD>
-__device__ inline void wait_staged(bool one_more_in_flight) {
-  // vmcnt(NLD) while the next record's NLD loads are in flight, else vmcnt(0)
-  if (one_more_in_flight) __builtin_amdgcn_s_waitcnt(0x0F70 | (NLD & 15) | ((NLD >> 4) << 14));
-  else __builtin_amdgcn_s_waitcnt(0x0F70);
-  __asm__ volatile("" ::: "memory");   // no LDS read of the record moves above the wait
+template <int NMAX>
+__device__ inline void store_pieces(const uint4 (&r)[NMAX], uint8_t* lds, int lane) {
+#pragma unroll
+  for (int j = 0; j < NMAX; ++j) *reinterpret_cast<uint4*>(lds + j * 1024 + lane * 16) = r[j];
 }
 
-template <int BASE, int L, int G, class SH>
-__device__ void pool_split(const DecodeArgs& a, SH& sm, int pool, int t_begin, int t_end,
-                           int b, int kvh) {
+// ---------------------------------------------------- one pool's records ----
+
+template <int BASE, int LH, int LL, int G, int POOL, class PL>
+__device__ void run_pool(const DecodeArgs& a, Shared<PL>& sm, WaveState<PL::NGV>& st, const uint8_t* unit,
+                         int nt0, int first, int i0, int i1, int count, uint4 (&R)[PL::NLD]) {
+  constexpr int L = POOL ? LL : LH;
   using Tr = Traits<BASE, L>;
   using Ge = Geo<BASE, L, G>;
-  const PoolGeom& g = a.g;
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
   const int n = lane & 15, r = lane >> 4, kg = r;
+  uint8_t* rec = sm.stage[wave];
   // tq: mu = -m, 0, m (L = 3) or -b, -a, a, b (L = 4)
-  const float* mu = a.mu[pool];
+  const float* mu = a.mu[POOL];
   const float cS = BASE == 0 ? 1.0f : (L == 3 ? mu[2] / 128.0f : 1.0f / 128.0f);
   const float cZ = BASE == 0 ? 0.0f : (L == 3 ? -mu[2] / 128.0f : -mu[3] / 128.0f);
   const float wP[2] = {BASE == 0 ? 1.0f : (L == 3 ? 1.0f : mu[3] - mu[2]),
@@ -363,30 +378,31 @@ __device__ void pool_split(const DecodeArgs& a, SH& sm, int pool, int t_begin, i
   half8 Aq[Tr::NCK];
   {
     const int h = n >> 2, kq = n & 3;
+    const int cb = Tr::n * kg;                 // channel of digit 0 of this lane group's first symbol
 #pragma unroll
     for (int c = 0; c < Tr::NCK; ++c) {
       _Float16 v[8];
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        int pl;
-        const int ch = slot_pos<BASE, L>(kD, kg, c, e, pl);
+        const int k = Tr::SPC * c + e / Tr::STRIDE, w = e % Tr::STRIDE;
+        const int dig = slot_digit<BASE, L>(w), pl = slot_plane<BASE, L>(w);
         v[e] = _Float16(0.0f);
-        if (ch >= 0 && kq < Ge::NG) {
+        if (dig >= 0) {
+          const int ch = cb + Tr::n * 4 * k + dig;     // >= 128: a pad slot, the query reads 0
           if (BASE == 0) {
-            if (ch / G == kq) v[e] = _Float16(sm.q[h][ch]);
+            const _Float16 x = sm.qh[h][ch];
+            v[e] = (kq < Ge::NG && (ch >> __builtin_ctz(G)) == kq) ? x : _Float16(0.0f);
           } else {
-            const float w = wP[pl] * sm.q[h][ch];
-            const _Float16 hi = _Float16(w);
-            v[e] = kq == 0 ? hi : _Float16(w - float(hi));
+            const float x = wP[pl] * sm.qf[h][ch];
+            const _Float16 hi = _Float16(x);
+            v[e] = kq == 0 ? hi : (kq == 1 ? _Float16(x - float(hi)) : _Float16(0.0f));
           }
         }
       }
       Aq[c] = half8{v[0], v[1], v[2], v[3], v[4], v[5], v[6], v[7]};
     }
   }
-  build_lut<BASE, L>(sm.lut);
-  __syncthreads();                      // every wave reads all of the tables
-  const uint32_t* lut = sm.lut + kg * Tr::LUTSTRIDE;
+  const uint32_t* lut = sm.lut + (POOL ? PL::LUTH : 0) + kg * Tr::LUTSTRIDE;
   uint32_t kmask[Tr::NSK], vmask[Tr::NSV];
   segment_masks<L, kD, kSlots>(kg, kmask);
   segment_masks<L, kSlots, kD>(kg, vmask);
@@ -408,37 +424,16 @@ __device__ void pool_split(const DecodeArgs& a, SH& sm, int pool, int t_begin, i
   const int pvcol = (vg >= 0 ? (((vlo ? 1 : 0) * 4 + hv) * Ge::NGV + vg) * kPvTok : pvzero) + Tr::n * kg;
   const int pvlo_col = (vg >= 0 ? ((4 + hv) * Ge::NGV + vg) * kPvTok : pvzero) + Tr::n * kg;   // LOPASS
   for (int i = lane; i < Ge::PV; i += 64) pvw[i] = _Float16(0.0f);
+  const int64_t nrows = a.n_rows[POOL];
 
-  float m_run = -INFINITY, l_run = 0.0f;
-  float z_run[Ge::NGV];
-#pragma unroll
-  for (int i = 0; i < Ge::NGV; ++i) z_run[i] = 0.0f;
-  float4v acc_o[8];
-#pragma unroll
-  for (int cb = 0; cb < 8; ++cb) acc_o[cb] = float4v{0, 0, 0, 0};
-
-  const uint8_t* unit = g.pools + unit_offset(g, b, a.layer, kvh) + (pool ? g.lo_offset : 0);
-  const int64_t nrows = a.n_rows[pool];
-  uint8_t* buf0 = sm.stage[wave][0];
-  uint8_t* buf1 = sm.stage[wave][1];
-  const int first = t_begin + wave;
-  const int count = first < t_end ? (t_end - first + 3) / 4 : 0;
-  if (count > 0) stage_record<Ge::NLD>(unit + int64_t(first) * Ge::RB, buf0, lane);
-
-  for (int it = 0; it < count; ++it) {
-    const int tile = first + 4 * it;
-    uint8_t* rec = (it & 1) ? buf1 : buf0;
-    if (it + 1 < count) {
-      __asm__ volatile("" ::: "memory");
-      __builtin_amdgcn_s_waitcnt(0xC07F);                  // lgkmcnt(0): last reads of that buffer done
-      stage_record<Ge::NLD>(unit + int64_t(tile + 4) * Ge::RB, (it & 1) ? buf0 : buf1, lane);
-      wait_staged<Ge::NLD>(true);
-    } else {
-      wait_staged<Ge::NLD>(false);
-    }
+  for (int it = i0; it < i1; ++it) {
+    const int tile = first + kDecodeWaves * it;
+    const bool more = it + 1 < count;
+    if (more) load_tile<BASE, LH, LL, G>(a.g, unit, tile + kDecodeWaves, nt0, R, lane);
+    const int ptile = POOL ? tile - nt0 : tile;
     const uint8_t* kmeta = rec + 2 * Tr::TB;
     const uint8_t* vmeta = kmeta + Ge::MB;
-    const int nvalid = nrows - int64_t(tile) * kSlots < kSlots ? int(nrows - int64_t(tile) * kSlots) : kSlots;
+    const int nvalid = nrows - int64_t(ptile) * kSlots < kSlots ? int(nrows - int64_t(ptile) * kSlots) : kSlots;
 
     // ---- scores: C[(h, kq)][token] = q_h,kq . codes; lane holds token n, head r
     float lg[4];
@@ -462,17 +457,17 @@ __device__ void pool_split(const DecodeArgs& a, SH& sm, int pool, int t_begin, i
         const float rho = hf(*reinterpret_cast<const uint16_t*>(kmeta + t * 2));
         x = (acc[0] + acc[1]) * (rho * cS) + rho * cZ * zws[0] * (1.0f / kDigitScale);
       }
-      lg[blk] = t < nvalid ? x * (kDigitScale * kLog2e * 0.08838834764831845f) : -INFINITY;
+      lg[blk] = t < nvalid ? x * (kDigitScale * kLog2e * kRsqrtD) : -INFINITY;
     }
     // ---- online softmax (base 2) for head r over this record's 64 tokens
     float mt = fmaxf(fmaxf(lg[0], lg[1]), fmaxf(lg[2], lg[3]));
     mt = row_max16(mt);
-    const float m_new = fmaxf(m_run, mt);
-    const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-    m_run = m_new;
+    const float m_new = fmaxf(st.m, mt);
+    const float alpha = __builtin_amdgcn_exp2f(st.m - m_new);
+    st.m = m_new;
     float lsum = 0.0f;
 #pragma unroll
-    for (int i = 0; i < Ge::NGV; ++i) z_run[i] *= alpha;
+    for (int i = 0; i < Ge::NGV; ++i) st.z[i] *= alpha;
 #pragma unroll
     for (int blk = 0; blk < 4; ++blk) {
       const int t = 16 * blk + n;
@@ -486,7 +481,7 @@ __device__ void pool_split(const DecodeArgs& a, SH& sm, int pool, int t_begin, i
           const _Float16 hi = _Float16(x);
           pvw[((0 * 4 + hs) * Ge::NGV + i) * kPvTok + t] = hi;
           pvw[((1 * 4 + hs) * Ge::NGV + i) * kPvTok + t] = _Float16(x - float(hi));
-          z_run[i] += p * hf(m >> 16);
+          st.z[i] += p * hf(m >> 16);
         }
       } else {
         const float rho = hf(*reinterpret_cast<const uint16_t*>(vmeta + t * 2));
@@ -498,11 +493,11 @@ __device__ void pool_split(const DecodeArgs& a, SH& sm, int pool, int t_begin, i
           pvw[pl * PLSTRIDE + (0 * 4 + hs) * kPvTok + t] = hi;
           pvw[pl * PLSTRIDE + (1 * 4 + hs) * kPvTok + t] = _Float16(x - float(hi));
         }
-        z_run[0] += p * rho * cZ;
+        st.z[0] += p * rho * cZ;
       }
     }
-    l_run = l_run * alpha + lsum;
-    // acc_o columns belong to head n >> 2: fetch that head's alpha
+    st.l = st.l * alpha + lsum;
+    // o columns belong to head n >> 2: fetch that head's alpha
     {
       const float al[4] = {__builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, alpha), 0)),
                            __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, alpha), 16)),
@@ -511,7 +506,7 @@ __device__ void pool_split(const DecodeArgs& a, SH& sm, int pool, int t_begin, i
       if (al[0] != 1.0f || al[1] != 1.0f || al[2] != 1.0f || al[3] != 1.0f) {
         const float av = al[hv];
 #pragma unroll
-        for (int cb = 0; cb < 8; ++cb) acc_o[cb] *= av;
+        for (int cb = 0; cb < 8; ++cb) st.o[cb] *= av;
       }
     }
     // weights written above by other lanes of this wave are read below
@@ -542,30 +537,42 @@ __device__ void pool_split(const DecodeArgs& a, SH& sm, int pool, int t_begin, i
     for (int cb = 0; cb < 8; ++cb) {
       uint32_t seg[Tr::VSEGW];
       lds_segment<Tr::VSEGW>(vbody, voff0 + cb * vstep, seg);
-      acc_o[cb] = contract<BASE, L, Tr::VSEGW, Tr::NSV, Tr::NCV>(seg, vmask, Bp, acc_o[cb], lut);
-      if constexpr (Ge::LOPASS) acc_o[cb] = contract<BASE, L, Tr::VSEGW, Tr::NSV, Tr::NCV>(seg, vmask, Bl, acc_o[cb], lut);
+      st.o[cb] = contract<BASE, L, Tr::VSEGW, Tr::NSV, Tr::NCV>(seg, vmask, Bp, st.o[cb], lut);
+      if constexpr (Ge::LOPASS) st.o[cb] = contract<BASE, L, Tr::VSEGW, Tr::NSV, Tr::NCV>(seg, vmask, Bl, st.o[cb], lut);
     }
+    // the next record replaces this one in the wave's buffer (LDS serves a
+    // wave's accesses in order: the reads above come first)
+    if (more) store_pieces(R, rec, lane);
   }
+}
 
-  // ---- wave totals: sums over the tokens of a row; fold low columns into high ones
-  l_run = row_sum16(l_run);
+// A wave's state in merged form: sums over the tokens of a row, low columns
+// folded into high ones, the zero-point term added.
+template <int BASE, int G, class PL>
+__device__ void wave_finish(Shared<PL>& sm, WaveState<PL::NGV>& st) {
+  using Ge = typename PL::GH;
+  const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
+  const int n = lane & 15, r = lane >> 4, hs = r, hv = n >> 2, gg = n & 3;
+  st.l = row_sum16(st.l);
 #pragma unroll
-  for (int i = 0; i < Ge::NGV; ++i) z_run[i] = row_sum16(z_run[i]);
+  for (int i = 0; i < Ge::NGV; ++i) st.z[i] = row_sum16(st.z[i]);
   if constexpr (!Ge::LOPASS) {
 #pragma unroll
     for (int cb = 0; cb < 8; ++cb)
 #pragma unroll
       for (int i = 0; i < 4; ++i)
-        acc_o[cb][i] += Ge::NGV == 1 ? dpp<0xB1>(acc_o[cb][i]) : dpp<0x4E>(acc_o[cb][i]);   // quad xor 1 / xor 2
+        st.o[cb][i] += Ge::NGV == 1 ? dpp<0xB1>(st.o[cb][i]) : dpp<0x4E>(st.o[cb][i]);   // quad xor 1 / xor 2
   }
   if (n == 0) {
 #pragma unroll
-    for (int i = 0; i < Ge::NGV; ++i) sm.zc[wave][hs][i] = z_run[i];
+    for (int i = 0; i < Ge::NGV; ++i) sm.zc[wave][hs][i] = st.z[i];
   }
-  __syncthreads();
+  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  Fin* f = wave_fin(sm, wave);
   if (n == 0) {
-    sm.u.mg.m[wave][hs] = m_run;
-    sm.u.mg.l[wave][hs] = l_run;
+    f->m[hs] = st.m;
+    f->l[hs] = st.l;
   }
 #pragma unroll
   for (int cb = 0; cb < 8; ++cb)
@@ -573,9 +580,8 @@ __device__ void pool_split(const DecodeArgs& a, SH& sm, int pool, int t_begin, i
     for (int i = 0; i < 4; ++i) {
       const int ch = 16 * cb + 4 * r + i;
       const bool mine = BASE == 0 ? (ch / G == gg) : (gg == 0);
-      if (mine) sm.u.mg.o[wave][hv][ch] = acc_o[cb][i] * kDigitScale + sm.zc[wave][hv][BASE == 0 ? gg : 0];
+      if (mine) f->o[hv][ch] = st.o[cb][i] * kDigitScale + sm.zc[wave][hv][BASE == 0 ? gg : 0];
     }
-  __syncthreads();
 }
 
 // Partials cross workgroups (and XCDs, whose L2 caches are not coherent with
@@ -588,260 +594,314 @@ __device__ inline float ld_agent(const float* p) {
   return __hip_atomic_load(const_cast<float*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-template <class SH>
-__device__ void write_partial(const DecodeArgs& a, SH& sm, int b, int kvh, int split) {
-  const int tid = threadIdx.x, h = tid >> 6, c = (tid & 63) * 2;
-  float M = -INFINITY;
-#pragma unroll
-  for (int w = 0; w < 4; ++w) M = fmaxf(M, sm.u.mg.m[w][h]);
-  float Lsum = 0.0f, o0 = 0.0f, o1 = 0.0f;
-#pragma unroll
-  for (int w = 0; w < 4; ++w) {
-    float sc = sm.u.mg.m[w][h] == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(sm.u.mg.m[w][h] - M);
-    Lsum += sm.u.mg.l[w][h] * sc;
-    o0 += sm.u.mg.o[w][h][c] * sc;
-    o1 += sm.u.mg.o[w][h][c + 1] * sc;
+// one radix-2 stage of the unnormalized Walsh-Hadamard transform of the 4
+// rows of x (128 entries each), by the first 256 threads
+__device__ inline void fwht_stage(float (*x)[kQPad], int hs) {
+  const int tid = threadIdx.x, hh = tid >> 6, i = tid & 63;
+  float a = 0.0f, b = 0.0f;
+  int lo = 0, hi = 0;
+  if (hh < 4) {
+    lo = (i / hs) * 2 * hs + (i % hs);
+    hi = lo + hs;
+    a = x[hh][lo];
+    b = x[hh][hi];
   }
-  float* dst = a.ws + ((int64_t(b) * a.g.n_kv_heads + kvh) * a.nsplit + split) * 4 * kPartial + h * kPartial;
-  if ((tid & 63) == 0) {
-    st_agent(dst, M);
-    st_agent(dst + 1, Lsum);
+  __syncthreads();
+  if (hh < 4) {
+    x[hh][lo] = a + b;
+    x[hh][hi] = a - b;
   }
-  st_agent(dst + 4 + c, o0);
-  st_agent(dst + 5 + c, o1);
+  __syncthreads();
+}
+__device__ inline void fwht_stage(float (*x)[kD], int hs) {
+  const int tid = threadIdx.x, hh = tid >> 6, i = tid & 63;
+  float a = 0.0f, b = 0.0f;
+  int lo = 0, hi = 0;
+  if (hh < 4) {
+    lo = (i / hs) * 2 * hs + (i % hs);
+    hi = lo + hs;
+    a = x[hh][lo];
+    b = x[hh][hi];
+  }
+  __syncthreads();
+  if (hh < 4) {
+    x[hh][lo] = a + b;
+    x[hh][hi] = a - b;
+  }
+  __syncthreads();
 }
 
-// fp16 tail of generated tokens, plain vector arithmetic (at most 64 rows)
-template <int BASE, class SH>
-__device__ void tail_split(const DecodeArgs& a, SH& sm, float (*qorig)[kD], int b, int kvh) {
+// fp16 tail of generated tokens (at most 64 rows), plain vector arithmetic;
+// its state goes to sm.tfin.
+template <int BASE, class PL>
+__device__ void tail_split(const DecodeArgs& a, Shared<PL>& sm, int b, int kvh) {
   const PoolGeom& g = a.g;
   const int tid = threadIdx.x;
   const int nt = a.n_tail;
+  TailScratch& ts = sm.ts;
   const uint16_t* kt = a.tail + ((((int64_t(b) * g.n_layers + a.layer) * g.n_kv_heads + kvh) * 2) * kSlots) * kD;
   const uint16_t* vt = kt + kSlots * kD;
   if (tid < 4 * nt) {
-    int t = tid >> 2, h = tid & 3;
+    const int t = tid >> 2, h = tid & 3;
     float d = 0.0f;
-    for (int c = 0; c < kD; ++c) d += qorig[h][c] * hf(kt[t * kD + c]);
-    sm.u.tl.lg[h][t] = d * (kLog2e * 0.08838834764831845f);
+    for (int c = 0; c < kD; ++c) d += sm.qorig[h][c] * hf(kt[t * kD + c]);
+    ts.lg[h][t] = d * (kLog2e * kRsqrtD);
   }
   __syncthreads();
   if (tid < 4) {
     float M = -INFINITY;
-    for (int t = 0; t < nt; ++t) M = fmaxf(M, sm.u.tl.lg[tid][t]);
+    for (int t = 0; t < nt; ++t) M = fmaxf(M, ts.lg[tid][t]);
     float s = 0.0f;
     for (int t = 0; t < nt; ++t) {
-      float p = __builtin_amdgcn_exp2f(sm.u.tl.lg[tid][t] - M);
-      sm.u.tl.lg[tid][t] = p;
+      const float p = __builtin_amdgcn_exp2f(ts.lg[tid][t] - M);
+      ts.lg[tid][t] = p;
       s += p;
     }
-    sm.u.tl.mx[tid] = M;
-    sm.u.tl.sum[tid] = s;
+    ts.mx[tid] = M;
+    ts.sum[tid] = s;
   }
   __syncthreads();
+  const int h = tid >> 7, c = tid & 127;
   {
-    int h = tid >> 6, c = (tid & 63) * 2;
-    float o0 = 0.0f, o1 = 0.0f;
-    for (int t = 0; t < nt; ++t) {
-      float p = sm.u.tl.lg[h][t];
-      o0 += p * hf(vt[t * kD + c]);
-      o1 += p * hf(vt[t * kD + c + 1]);
-    }
+    float o = 0.0f;
+    for (int t = 0; t < nt; ++t) o += ts.lg[h][t] * hf(vt[t * kD + c]);
     if (BASE == 1) {                       // into the rotated domain: H (sign . o) / 128
       const uint32_t* sw = g.signs + (int64_t(a.layer) * g.n_kv_heads + kvh) * 4;
-      o0 = ((sw[c >> 5] >> (c & 31)) & 1u) ? -o0 : o0;
-      o1 = ((sw[(c + 1) >> 5] >> ((c + 1) & 31)) & 1u) ? -o1 : o1;
+      o = ((sw[c >> 5] >> (c & 31)) & 1u) ? -o : o;
     }
-    sm.u.tl.o[h][c] = o0;
-    sm.u.tl.o[h][c + 1] = o1;
+    ts.o[h][c] = o;
   }
   __syncthreads();
-  if (BASE == 1) {
-    for (int hs = 1; hs < kD; hs <<= 1) {  // 4 heads x 64 butterflies per stage
-      int h = tid >> 6, i = tid & 63;
-      int lo = (i / hs) * 2 * hs + (i % hs), hi = lo + hs;
-      float x = sm.u.tl.o[h][lo], y = sm.u.tl.o[h][hi];
-      __syncthreads();
-      sm.u.tl.o[h][lo] = x + y;
-      sm.u.tl.o[h][hi] = x - y;
-      __syncthreads();
-    }
+  if (BASE == 1)
+    for (int hs = 1; hs < kD; hs <<= 1) fwht_stage(ts.o, hs);
+  sm.tfin.o[h][c] = ts.o[h][c] * (BASE == 1 ? 1.0f / 128.0f : 1.0f);
+  if (c == 0) {
+    sm.tfin.m[h] = ts.mx[h];
+    sm.tfin.l[h] = ts.sum[h];
   }
-  // the tail partial enters the workgroup merge as wave 0; waves 1-3 are empty
-  {
-    int h = tid >> 6, c = (tid & 63) * 2;
-    float scale = BASE == 1 ? 1.0f / 128.0f : 1.0f;
-    float o0 = sm.u.tl.o[h][c] * scale, o1 = sm.u.tl.o[h][c + 1] * scale;
-    float M = sm.u.tl.mx[h], S = sm.u.tl.sum[h];
-    __syncthreads();                       // tl and mg share storage
-    if ((tid & 63) == 0)
-      for (int w = 0; w < 4; ++w) {
-        sm.u.mg.m[w][h] = w == 0 ? M : -INFINITY;
-        sm.u.mg.l[w][h] = w == 0 ? S : 0.0f;
-      }
-    for (int w = 0; w < 4; ++w) {
-      sm.u.mg.o[w][h][c] = w == 0 ? o0 : 0.0f;
-      sm.u.mg.o[w][h][c + 1] = w == 0 ? o1 : 0.0f;
-    }
-  }
-  __syncthreads();
 }
 
-template <int BASE, int LH, int LL, int G>
-__global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a) {
-  using GH = Geo<BASE, LH, G>;
-  using GL = Geo<BASE, LL, G>;
-  constexpr int NLD = GH::NLD > GL::NLD ? GH::NLD : GL::NLD;
-  constexpr int PV = GH::PV > GL::PV ? GH::PV : GL::PV;
-  constexpr int LUT = Traits<BASE, LH>::LUTSTRIDE > Traits<BASE, LL>::LUTSTRIDE ? Traits<BASE, LH>::LUTSTRIDE
-                                                                                 : Traits<BASE, LL>::LUTSTRIDE;
-  __shared__ SharedT<NLD, PV, LUT> sm;
-  __shared__ float qorig[4][kD];
-  const int split = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
-  const int tid = threadIdx.x;
-  const PoolGeom& g = a.g;
-  {
-    const int h = tid >> 6, c = (tid & 63) * 2;
-    const uint16_t* qp = a.q + ((int64_t(b) * g.n_kv_heads * 4) + kvh * 4 + h) * kD + c;
-    uint32_t w = *reinterpret_cast<const uint32_t*>(qp);
-    float x0 = hf(w & 0xFFFFu), x1 = hf(w >> 16);
-    qorig[h][c] = x0;
-    qorig[h][c + 1] = x1;
-    if (BASE == 1) {
-      const uint32_t* sw = g.signs + (int64_t(a.layer) * g.n_kv_heads + kvh) * 4;
-      x0 = ((sw[c >> 5] >> (c & 31)) & 1u) ? -x0 : x0;
-      x1 = ((sw[(c + 1) >> 5] >> ((c + 1) & 31)) & 1u) ? -x1 : x1;
-    }
-    sm.q[h][c] = x0;
-    sm.q[h][c + 1] = x1;
-  }
-  __syncthreads();
-  if (BASE == 1) {
-    for (int hs = 1; hs < kD; hs <<= 1) {
-      int h = tid >> 6, i = tid & 63;
-      int lo = (i / hs) * 2 * hs + (i % hs), hi = lo + hs;
-      float x = sm.q[h][lo], y = sm.q[h][hi];
-      __syncthreads();
-      sm.q[h][lo] = x + y;
-      sm.q[h][hi] = x - y;
-      __syncthreads();
-    }
-  }
-  if (tid < 16) {
-    int h = tid >> 2, gq = tid & 3;
-    float s = 0.0f;
-    if (BASE == 0) {
-      if (gq < kD / G)
-        for (int c = gq * G; c < (gq + 1) * G; ++c) s += sm.q[h][c];
-    } else if (gq == 0) {
-      for (int c = 0; c < kD; ++c) s += sm.q[h][c];
-    }
-    sm.zw[tid] = s;
-  }
-  __syncthreads();
-  if (split < a.ns[0] + a.ns[1]) {
-    const int pool = split < a.ns[0] ? 0 : 1;
-    const int s0 = pool ? split - a.ns[0] : split;
-    const int ntiles = int((a.n_rows[pool] + kSlots - 1) / kSlots);
-    const int t_begin = s0 * a.chunk;
-    const int t_end = t_begin + a.chunk < ntiles ? t_begin + a.chunk : ntiles;
-    if (pool == 0) pool_split<BASE, LH, G>(a, sm, 0, t_begin, t_end, b, kvh);
-    else pool_split<BASE, LL, G>(a, sm, 1, t_begin, t_end, b, kvh);
-  } else {
-    tail_split<BASE>(a, sm, qorig, b, kvh);
-  }
-  write_partial(a, sm, b, kvh, split);
-  // the last workgroup of this (sequence, kv head) merges the splits: every
-  // thread waits for its partial stores (workgroup release), then one counter
-  // increment per workgroup at agent scope
-  __shared__ int last;
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
-  __syncthreads();
-  if (tid == 0) {
-    uint32_t* ctr = a.counters + b * g.n_kv_heads + kvh;
-    uint32_t old = __hip_atomic_fetch_add(ctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    last = old == uint32_t(a.nsplit - 1);
-    if (last) __hip_atomic_store(ctr, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  }
-  __syncthreads();
-  if (!last) return;
-  merge_splits<BASE>(a, sm, b, kvh);
-}
-
-// Merge of the splits of one (sequence, kv head), run by the last workgroup
+// Merge of the partials of one (sequence, kv head), run by the last workgroup
 // to finish: log-sum-exp over the partials, then for the tq base the inverse
 // rotation o = sign . H o_rot.
-template <int BASE, class SH>
-__device__ void merge_splits(const DecodeArgs& a, SH& sm, int b, int kvh) {
-  const int tid = threadIdx.x, h = tid >> 6, c = (tid & 63) * 2;
+template <int BASE, class PL>
+__device__ void merge_splits(const DecodeArgs& a, Shared<PL>& sm, int b, int kvh) {
+  const int tid = threadIdx.x, h = tid >> 7, c = tid & 127;
   const int ns = a.nsplit;
   const float* unit = a.ws + (int64_t(b) * a.g.n_kv_heads + kvh) * ns * 4 * kPartial;
-  float* mm = sm.u.mr.mm;                 // [ns][4] maxima
-  float* ll = sm.u.mr.ll;                 // [ns][4] sums
-  for (int i = tid; i < ns * 4; i += 256) {
+  float* mm = reinterpret_cast<float*>(&sm.stage[0][0]);   // [ns][4] maxima
+  float* ll = mm + kMaxSplits * 4;                          // [ns][4] sums
+  static_assert(sizeof(sm.stage) >= 2 * kMaxSplits * 4 * sizeof(float), "merge scratch");
+  for (int i = tid; i < ns * 4; i += kThreads) {
     mm[i] = ld_agent(unit + i * kPartial);
     ll[i] = ld_agent(unit + i * kPartial + 1);
   }
   __syncthreads();
   float M = -INFINITY;
   for (int s = 0; s < ns; ++s) M = fmaxf(M, mm[s * 4 + h]);
-  float Lsum = 0.0f, o0 = 0.0f, o1 = 0.0f;
+  float Lsum = 0.0f, o = 0.0f;
   const float* op = unit + h * kPartial + 4 + c;
-  int s = 0;
-  for (; s + 4 <= ns; s += 4) {              // four splits' loads in flight
-    float x[4][2];
+  constexpr int kBatch = 16;                 // partial loads in flight per thread
+  for (int s0 = 0; s0 < ns; s0 += kBatch) {
+    float x[kBatch];
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      x[k][0] = ld_agent(op + (s + k) * 4 * kPartial);
-      x[k][1] = ld_agent(op + (s + k) * 4 * kPartial + 1);
-    }
+    for (int k = 0; k < kBatch; ++k) x[k] = s0 + k < ns ? ld_agent(op + (s0 + k) * 4 * kPartial) : 0.0f;
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      float m = mm[(s + k) * 4 + h];
-      float sc = m == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(m - M);
-      Lsum += ll[(s + k) * 4 + h] * sc;
-      o0 += x[k][0] * sc;
-      o1 += x[k][1] * sc;
+    for (int k = 0; k < kBatch; ++k) {
+      if (s0 + k < ns) {
+        const float m = mm[(s0 + k) * 4 + h];
+        const float sc = m == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(m - M);
+        Lsum += ll[(s0 + k) * 4 + h] * sc;
+        o += x[k] * sc;
+      }
     }
   }
-  for (; s < ns; ++s) {
-    float m = mm[s * 4 + h];
-    float sc = m == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(m - M);
-    Lsum += ll[s * 4 + h] * sc;
-    o0 += ld_agent(op + s * 4 * kPartial) * sc;
-    o1 += ld_agent(op + s * 4 * kPartial + 1) * sc;
-  }
-  o0 /= Lsum;
-  o1 /= Lsum;
+  o /= Lsum;
   if (BASE == 1) {
     __syncthreads();
-    sm.q[h][c] = o0;
-    sm.q[h][c + 1] = o1;
+    sm.qf[h][c] = o;
     __syncthreads();
-    for (int hs = 1; hs < kD; hs <<= 1) {
-      int i = tid & 63;
-      int lo = (i / hs) * 2 * hs + (i % hs), hi = lo + hs;
-      float xa = sm.q[h][lo], ya = sm.q[h][hi];
-      __syncthreads();
-      sm.q[h][lo] = xa + ya;
-      sm.q[h][hi] = xa - ya;
-      __syncthreads();
-    }
+    for (int hs = 1; hs < kD; hs <<= 1) fwht_stage(sm.qf, hs);
     const uint32_t* sw = a.g.signs + (int64_t(a.layer) * a.g.n_kv_heads + kvh) * 4;
-    o0 = ((sw[c >> 5] >> (c & 31)) & 1u) ? -sm.q[h][c] : sm.q[h][c];
-    o1 = ((sw[(c + 1) >> 5] >> ((c + 1) & 31)) & 1u) ? -sm.q[h][c + 1] : sm.q[h][c + 1];
+    o = ((sw[c >> 5] >> (c & 31)) & 1u) ? -sm.qf[h][c] : sm.qf[h][c];
   }
-  float2* dst = reinterpret_cast<float2*>(a.out + ((int64_t(b) * a.g.n_kv_heads + kvh) * 4 + h) * kD + c);
-  *dst = make_float2(o0, o1);
+  a.out[((int64_t(b) * a.g.n_kv_heads + kvh) * 4 + h) * kD + c] = o;
+}
+
+template <int BASE, int LH, int LL, int G>
+__global__ __launch_bounds__(kThreads) void decode_kernel(DecodeArgs a) {
+  using PL = Plan<BASE, LH, LL, G>;
+  __shared__ Shared<PL> sm;
+  const int split = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
+  const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
+  const PoolGeom& g = a.g;
+
+  // ---- this workgroup's run of tiles (high pool first), this wave's records
+  const int nt0 = int((a.n_rows[0] + kSlots - 1) / kSlots), nt1 = int((a.n_rows[1] + kSlots - 1) / kSlots);
+  const int nt = nt0 + nt1;
+  const int f0 = int(int64_t(split) * nt / a.nsplit), f1 = int(int64_t(split + 1) * nt / a.nsplit);
+  const int first = f0 + wave;
+  const int count = first < f1 ? (f1 - first + kDecodeWaves - 1) / kDecodeWaves : 0;
+  const int nhi_all = first < nt0 ? (nt0 - first + kDecodeWaves - 1) / kDecodeWaves : 0;
+  const int nhi = nhi_all < count ? nhi_all : count;
+  const uint8_t* unit = g.pools + unit_offset(g, b, a.layer, kvh);
+
+  // ---- query and decode tables, then the first record in flight
+  const int h = tid >> 7, c = tid & 127;
+  const uint16_t qbits = a.q[((int64_t(b) * g.n_kv_heads * 4) + kvh * 4 + h) * kD + c];
+  constexpr int NTH = (PL::LUTH / 4 + kThreads - 1) / kThreads, NTL = (PL::LUTL / 4 + kThreads - 1) / kThreads;
+  uint4 th[NTH], tl[NTL];
+  {
+    const uint4* sh = reinterpret_cast<const uint4*>(kLutImage<BASE, LH>.w);
+    const uint4* sl = reinterpret_cast<const uint4*>(kLutImage<BASE, LL>.w);
+#pragma unroll
+    for (int k = 0; k < NTH; ++k) th[k] = sh[tid + k * kThreads < PL::LUTH / 4 ? tid + k * kThreads : 0];
+#pragma unroll
+    for (int k = 0; k < NTL; ++k) tl[k] = sl[tid + k * kThreads < PL::LUTL / 4 ? tid + k * kThreads : 0];
+  }
+  // the wave's first record (a wave without records loads tile 0, unused)
+  uint4 R[PL::NLD];
+  load_tile<BASE, LH, LL, G>(g, unit, count > 0 ? first : 0, nt0, R, lane);
+  {
+    uint4* d = reinterpret_cast<uint4*>(sm.lut);
+#pragma unroll
+    for (int k = 0; k < NTH; ++k)
+      if (tid + k * kThreads < PL::LUTH / 4) d[tid + k * kThreads] = th[k];
+#pragma unroll
+    for (int k = 0; k < NTL; ++k)
+      if (tid + k * kThreads < PL::LUTL / 4) d[PL::LUTH / 4 + tid + k * kThreads] = tl[k];
+  }
+  {
+    const float x = hf(qbits);
+    sm.qorig[h][c] = x;
+    float xr = x;
+    if (BASE == 1) {
+      const uint32_t* sw = g.signs + (int64_t(a.layer) * g.n_kv_heads + kvh) * 4;
+      xr = ((sw[c >> 5] >> (c & 31)) & 1u) ? -x : x;
+    }
+    sm.qf[h][c] = xr;
+    sm.qh[h][c] = _Float16(x);
+    if (c < kQPad - kD) {
+      sm.qf[h][kD + c] = 0.0f;
+      sm.qh[h][kD + c] = _Float16(0.0f);
+    }
+  }
+  __syncthreads();
+  if (BASE == 1)                            // rotate: H (sign . q)
+    for (int hs = 1; hs < kD; hs <<= 1) fwht_stage(sm.qf, hs);
+  {
+    // per (head, group) sums of the query over segments of SEG lanes
+    constexpr int SEG = (BASE == 0 && G < 64) ? G : 64;
+    float x = sm.qf[h][c];
+#pragma unroll
+    for (int o = 1; o < SEG; o <<= 1) x += __shfl_xor(x, o);
+    if ((c % SEG) == 0) sm.zpart[h][c / SEG] = x;
+  }
+  __syncthreads();
+  if (tid < 16) {
+    const int hh = tid >> 2, gq = tid & 3;
+    float s = 0.0f;
+    if (BASE == 0) {
+      constexpr int SEG = G < 64 ? G : 64;
+      if (gq < kD / G)
+        for (int p = gq * G / SEG; p < (gq + 1) * G / SEG; ++p) s += sm.zpart[hh][p];
+    } else if (gq == 0) {
+      s = sm.zpart[hh][0] + sm.zpart[hh][1];
+    }
+    sm.zw[tid] = s;
+  }
+  __syncthreads();
+
+  // ---- this wave's records
+  WaveState<PL::NGV> st;
+  st.m = -INFINITY;
+  st.l = 0.0f;
+#pragma unroll
+  for (int i = 0; i < PL::NGV; ++i) st.z[i] = 0.0f;
+#pragma unroll
+  for (int cb = 0; cb < 8; ++cb) st.o[cb] = float4v{0, 0, 0, 0};
+  if (count > 0) store_pieces(R, sm.stage[wave], lane);
+  if (nhi > 0) run_pool<BASE, LH, LL, G, 0>(a, sm, st, unit, nt0, first, 0, nhi, count, R);
+  if (count > nhi) run_pool<BASE, LH, LL, G, 1>(a, sm, st, unit, nt0, first, nhi, count, count, R);
+  wave_finish<BASE, G>(sm, st);
+  __syncthreads();
+  const bool tail = split == a.nsplit - 1 && a.n_tail > 0;
+  if (tail) {
+    tail_split<BASE>(a, sm, b, kvh);
+    __syncthreads();
+  }
+
+  // ---- workgroup partial: merge of the waves' (and the tail's) states
+  {
+    float M = -INFINITY;
+#pragma unroll
+    for (int w = 0; w < kDecodeWaves; ++w) M = fmaxf(M, wave_fin(sm, w)->m[h]);
+    if (tail) M = fmaxf(M, sm.tfin.m[h]);
+    float Lsum = 0.0f, o = 0.0f;
+#pragma unroll
+    for (int w = 0; w < kDecodeWaves; ++w) {
+      const Fin* f = wave_fin(sm, w);
+      const float sc = f->m[h] == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(f->m[h] - M);
+      Lsum += f->l[h] * sc;
+      o += f->o[h][c] * sc;
+    }
+    if (tail) {
+      const float sc = sm.tfin.m[h] == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(sm.tfin.m[h] - M);
+      Lsum += sm.tfin.l[h] * sc;
+      o += sm.tfin.o[h][c] * sc;
+    }
+    float* dst = a.ws + ((int64_t(b) * g.n_kv_heads + kvh) * a.nsplit + split) * 4 * kPartial + h * kPartial;
+    if (c == 0) {
+      st_agent(dst, M);
+      st_agent(dst + 1, Lsum);
+    }
+    st_agent(dst + 4 + c, o);
+  }
+  // every thread's partial stores are complete (at the coherent level) before
+  // the workgroup's counter increment; the last workgroup reads them after it
+  __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
+  if (tid == 0) {
+    uint32_t* ctr = a.counters + b * g.n_kv_heads + kvh;
+    const uint32_t old = __hip_atomic_fetch_add(ctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    sm.last = old == uint32_t(a.nsplit - 1);
+    if (sm.last) __hip_atomic_store(ctr, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+  __syncthreads();
+  if (!sm.last) return;
+  merge_splits<BASE>(a, sm, b, kvh);
+}
+
+template <int BASE, int LH, int LL, int G>
+int occupancy() {
+  int n = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, decode_kernel<BASE, LH, LL, G>, kThreads, 0) != hipSuccess)
+    return 1;
+  return n > 0 ? n : 1;
 }
 
 template <int BASE, int LH, int LL>
 int launch_dec(const DecodeArgs& a, hipStream_t st) {
   dim3 grid(a.nsplit, a.g.n_kv_heads, a.g.batch);
-  if (BASE == 1 || a.g.G == 128) hipLaunchKernelGGL((decode_kernel<BASE, LH, LL, 128>), grid, dim3(256), 0, st, a);
-  else if (a.g.G == 64) hipLaunchKernelGGL((decode_kernel<BASE, LH, LL, 64>), grid, dim3(256), 0, st, a);
-  else hipLaunchKernelGGL((decode_kernel<BASE, LH, LL, 32>), grid, dim3(256), 0, st, a);
+  if constexpr (BASE == 1) {
+    hipLaunchKernelGGL((decode_kernel<BASE, LH, LL, 128>), grid, dim3(kThreads), 0, st, a);
+  } else {
+    if (a.g.G == 128) hipLaunchKernelGGL((decode_kernel<BASE, LH, LL, 128>), grid, dim3(kThreads), 0, st, a);
+    else if (a.g.G == 64) hipLaunchKernelGGL((decode_kernel<BASE, LH, LL, 64>), grid, dim3(kThreads), 0, st, a);
+    else hipLaunchKernelGGL((decode_kernel<BASE, LH, LL, 32>), grid, dim3(kThreads), 0, st, a);
+  }
   return hipGetLastError() == hipSuccess ? 0 : -5;
+}
+
+template <int BASE, int LH, int LL>
+int occ_dec(int G) {
+  if constexpr (BASE == 1) {
+    return occupancy<BASE, LH, LL, 128>();
+  } else {
+    if (G == 128) return occupancy<BASE, LH, LL, 128>();
+    if (G == 64) return occupancy<BASE, LH, LL, 64>();
+    return occupancy<BASE, LH, LL, 32>();
+  }
 }
 
 }  // namespace
@@ -856,6 +916,17 @@ int launch_decode(const DecodeArgs& a, hipStream_t s) {
   if (B == 0 && LH == 6 && LL == 3) return launch_dec<0, 6, 3>(a, s);
   if (B == 1 && LH == 4 && LL == 3) return launch_dec<1, 4, 3>(a, s);
   return -2;
+}
+
+int decode_blocks_per_cu(int base, int LH, int LL, int G) {
+  if (base == 0 && LH == 6 && LL == 5) return occ_dec<0, 6, 5>(G);
+  if (base == 0 && LH == 5 && LL == 4) return occ_dec<0, 5, 4>(G);
+  if (base == 0 && LH == 6 && LL == 4) return occ_dec<0, 6, 4>(G);
+  if (base == 0 && LH == 4 && LL == 3) return occ_dec<0, 4, 3>(G);
+  if (base == 0 && LH == 5 && LL == 3) return occ_dec<0, 5, 3>(G);
+  if (base == 0 && LH == 6 && LL == 3) return occ_dec<0, 6, 3>(G);
+  if (base == 1 && LH == 4 && LL == 3) return occ_dec<1, 4, 3>(G);
+  return 1;
 }
 
 }  // namespace semkv

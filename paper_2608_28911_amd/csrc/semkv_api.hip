@@ -4,6 +4,10 @@
 #include <math.h>
 #include <string.h>
 
+#include <array>
+#include <map>
+#include <mutex>
+
 #include "semkv.h"
 #include "semkv_internal.h"
 
@@ -84,20 +88,37 @@ double bisect(F f, double lo, double hi) {
   return 0.5 * (lo + hi);
 }
 
-// Decode split plan: tiles per split (a multiple of 4, one per wave) chosen
-// so the grid has about 1024 workgroups.
-void plan(const semkv_cache* c, int n_tail, int* chunk, int ns[2], int* nsplit) {
-  int64_t nt0 = (c->n_hi + kSlots - 1) / kSlots, nt1 = (c->n_lo + kSlots - 1) / kSlots;
-  int64_t total = int64_t(c->cfg.batch) * c->cfg.n_kv_heads * (nt0 + nt1);
-  int64_t ch = (total + 1023) / 1024;
-  const int64_t cap = kMaxSplits - 3;        // two partial chunks and the tail
-  if (ch < (nt0 + nt1 + cap - 1) / cap) ch = (nt0 + nt1 + cap - 1) / cap;
-  ch = (ch + 3) / 4 * 4;
-  if (ch < 4) ch = 4;
-  *chunk = int(ch);
-  ns[0] = int((nt0 + ch - 1) / ch);
-  ns[1] = int((nt1 + ch - 1) / ch);
-  *nsplit = ns[0] + ns[1] + (n_tail > 0 ? 1 : 0);
+// Workgroups the device holds at once for this cache's decode kernel (compute
+// units x workgroups per unit), looked up once per device and level pair.
+int64_t decode_slots(const semkv_config& k) {
+  static std::mutex mu;
+  static std::map<std::array<int, 5>, int64_t> known;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 256;
+  const std::array<int, 5> key{dev, k.base, k.L_hi, k.L_lo, k.group};
+  std::lock_guard<std::mutex> lock(mu);
+  auto it = known.find(key);
+  if (it != known.end()) return it->second;
+  int cus = 0;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1) cus = 256;
+  const int64_t slots = int64_t(cus) * decode_blocks_per_cu(k.base, k.L_hi, k.L_lo, k.group);
+  known[key] = slots;
+  return slots;
+}
+
+// Decode split plan: the tiles of each (sequence, kv head) unit, high pool
+// then low pool, are cut into nsplit balanced runs, one workgroup each, so
+// that the whole grid is resident at once and every wave has a record.  The
+// fp16 tail rides with the last run.  0: nothing cached.
+int plan(const semkv_cache* c, int n_tail) {
+  const int64_t nt = (c->n_hi + kSlots - 1) / kSlots + (c->n_lo + kSlots - 1) / kSlots;
+  if (nt == 0) return n_tail > 0 ? 1 : 0;
+  const int64_t units = int64_t(c->cfg.batch) * c->cfg.n_kv_heads;
+  int64_t ns = decode_slots(c->cfg) / units;
+  if (ns > nt / kDecodeWaves) ns = nt / kDecodeWaves;
+  if (ns > kMaxSplits) ns = kMaxSplits;
+  if (ns < 1) ns = 1;
+  return int(ns);
 }
 
 // workspace: [b][kvh] uint32 counters (padded to 256 bytes), then the partials
@@ -182,12 +203,13 @@ int semkv_cache_sizes(const semkv_config* cfg, semkv_sizes* out) {
   out->record_bytes_lo = record_bytes(k.base, k.L_lo, k.group);
   out->unit_stride = out->cap_hi_tiles * out->record_bytes_hi + out->cap_lo_tiles * out->record_bytes_lo;
   int64_t units = int64_t(k.batch) * k.n_layers * k.n_kv_heads;
-  out->pool_bytes = size_t(units * out->unit_stride) + kStageSlack;   // staging loads read past the last record
+  out->pool_bytes = size_t(units * out->unit_stride);
   out->tail_bytes = size_t(units * 2 * kSlots * kD * 2);
   out->tail_score_bytes = size_t(k.batch) * kSlots * 4;
   out->flag_words = (k.max_prompt + k.max_new + 31) / 32 + 1;
   out->flag_bytes = size_t(k.batch * out->flag_words * 4);
-  int64_t max_split = out->cap_hi_tiles + out->cap_lo_tiles + 1;
+  int64_t max_split = out->cap_hi_tiles + out->cap_lo_tiles;
+  if (max_split > kMaxSplits) max_split = kMaxSplits;
   out->workspace_bytes = workspace_need(k, int(max_split));
   return SEMKV_OK;
 }
@@ -359,9 +381,7 @@ int semkv_flush(semkv_cache* c, hipStream_t stream) {
 
 int semkv_workspace_bytes(const semkv_cache* c, size_t* bytes) {
   if (!c || !bytes) return SEMKV_EINVAL;
-  int chunk, ns[2], nsplit;
-  plan(c, 1, &chunk, ns, &nsplit);
-  *bytes = workspace_need(c->cfg, nsplit);
+  *bytes = workspace_need(c->cfg, plan(c, 1));
   return SEMKV_OK;
 }
 
@@ -374,8 +394,7 @@ int semkv_decode_attn(const semkv_cache* c, int32_t layer, const uint16_t* q, fl
   int n_tail = c->n_scored + (((c->appended[layer >> 5] >> (layer & 31)) & 1u) ? 1 : 0);
   DecodeArgs a;
   memset(&a, 0, sizeof(a));
-  int chunk, ns[2], nsplit;
-  plan(c, n_tail, &chunk, ns, &nsplit);
+  const int nsplit = plan(c, n_tail);
   if (nsplit == 0) return SEMKV_ESTATE;      // nothing cached yet
   if (ws_bytes < workspace_need(k, nsplit)) return SEMKV_EINVAL;
   a.g = geom(c);
@@ -388,9 +407,6 @@ int semkv_decode_attn(const semkv_cache* c, int32_t layer, const uint16_t* q, fl
   a.n_rows[0] = c->n_hi;
   a.n_rows[1] = c->n_lo;
   a.n_tail = n_tail;
-  a.chunk = chunk;
-  a.ns[0] = ns[0];
-  a.ns[1] = ns[1];
   a.nsplit = nsplit;
   memcpy(a.mu[0], c->mu_hi, sizeof(a.mu[0]));
   memcpy(a.mu[1], c->mu_lo, sizeof(a.mu[1]));

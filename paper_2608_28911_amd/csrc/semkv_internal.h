@@ -69,21 +69,21 @@ struct DecodeArgs {
   float* out;              // [b][Hq][128]
   int32_t layer;
   int64_t n_rows[2];       // rows in the high / low pool
-  int32_t n_tail;          // fp16 tail rows visible to this layer
-  int32_t chunk;           // tiles per split
-  int32_t ns[2];           // splits over the high / low pool
-  int32_t nsplit;          // splits per unit (ns[0] + ns[1] + tail)
+  int32_t n_tail;          // fp16 tail rows visible to this layer (taken by the last split)
+  int32_t nsplit;          // balanced runs of tiles per unit, one workgroup each
   float mu[2][16];         // tq codebooks
 };
 
 constexpr int kPartial = 132;  // m, l, 2 pad, o[128]
 constexpr int kMaxSplits = 256;   // splits per (sequence, kv head)
-constexpr int kStageSlack = 1024; // bytes after the last record that staging loads may read
+constexpr int kDecodeWaves = 8;   // waves per decode workgroup
 
 int launch_rank(const RankArgs& a, int batch, hipStream_t s);
 int launch_quantize(const QuantArgs& a, hipStream_t s);
 int launch_append(const AppendArgs& a, hipStream_t s);
 int launch_close(const CloseArgs& a, hipStream_t s);
 int launch_decode(const DecodeArgs& a, hipStream_t s);
+// decode workgroups one compute unit holds at once for this cache's kernel
+int decode_blocks_per_cu(int base, int L_hi, int L_lo, int G);
 
 }  // namespace semkv

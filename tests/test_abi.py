@@ -56,7 +56,7 @@ def test_sizes_match_the_format(abi):
         assert s.record_bytes_lo == O.record_bytes(base, L_lo, G)
         K = 2048 * 26 // 100
         assert s.cap_hi_tiles == -(-(K + 128) // 64) and s.cap_lo_tiles == -(-(2048 - K + 128) // 64)
-        assert s.pool_bytes == 2 * 8 * s.unit_stride + 1024     # staging slack past the last unit
+        assert s.pool_bytes == 2 * 8 * s.unit_stride
 
 
 @pytest.mark.parametrize("bad,status", [
