@@ -28,6 +28,34 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, AMD published peak
+PROFILE = os.path.join(ROOT, "profiles", "decode_kernel_llama8b_b1_t32768.md")
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2608_28911_amd", "csrc", f)
+                  for f in ("decode.hip", "semkv_internal.h", "semkv_fmt.h")]
+
+
+def kernel_source_hash():
+    import hashlib
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic():
+    """HBM bytes per decode launch from the committed counter runs (FETCH_SIZE +
+    WRITE_SIZE, calibrated against a copy of known size), or None when the
+    kernel sources changed since they were taken."""
+    try:
+        with open(PROFILE) as fh:
+            for line in fh:
+                if line.startswith("traffic_bytes_per_launch:"):
+                    f = line.split()
+                    if f[3] == kernel_source_hash():
+                        return int(f[1])
+    except (OSError, IndexError, ValueError):
+        pass
+    return None
 
 
 def parse():
@@ -39,6 +67,8 @@ def parse():
     ap.add_argument("--group", type=int, default=None, help="override the affine metadata group")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="budget of the oracle sample")
+    ap.add_argument("--copy-probe-mib", type=int, default=0,
+                    help="run a device fill and copy of this many MiB first (hardware counter calibration)")
     return ap.parse_args()
 
 
@@ -165,6 +195,14 @@ def main():
     del K, V
     torch.cuda.empty_cache()
 
+    if args.copy_probe_mib > 0:      # known traffic for counter calibration
+        nb = args.copy_probe_mib << 20
+        src = torch.empty(nb, dtype=torch.uint8, device=dev).fill_(1)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+
     # ---- decode: all timed steps captured in one graph
     ws = cache.workspace()
 
@@ -230,7 +268,8 @@ def main():
         "quantize_pack_ms": round(quant_ms, 3),
         "rank_us": round(rank_us, 1),
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                     "frac": round(achieved / HBM_PEAK_GBS, 4),
+                     "traffic": measured_traffic() if cfgw.name == "llama8b_kv_b1_t32768_affine" else None,
                      "kernel": "decode_kernel", "bytes_per_launch": int(alg)},
     }
     if not args.no_cpu_baseline:

@@ -201,15 +201,16 @@ __device__ inline half8 chunk_operand(const uint32_t (&seg)[NW], const uint32_t 
   return __builtin_bit_cast(half8, r);
 }
 
+// MFMA operands of all NC chunks of a segment: every table read is issued
+// before the first product needs one (LDS returns them in order)
 template <int BASE, int L, int NW, int NS, int NC>
-__device__ inline float4v contract(const uint32_t (&seg)[NW], const uint32_t (&mask)[NS],
-                                   const half8 (&B)[NC], float4v acc, const uint32_t* lut) {
+__device__ inline void chunk_operands(const uint32_t (&seg)[NW], const uint32_t (&mask)[NS], const uint32_t* lut,
+                                      half8 (&A)[NC]) {
   static_assert(NC <= 11, "chunks");
-#define SEMKV_C(C) if constexpr (C < NC) acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(chunk_operand<BASE, L, C, NW, NS>(seg, mask, lut), B[C], acc, 0, 0, 0);
-  SEMKV_C(0) SEMKV_C(1) SEMKV_C(2) SEMKV_C(3) SEMKV_C(4) SEMKV_C(5)
-  SEMKV_C(6) SEMKV_C(7) SEMKV_C(8) SEMKV_C(9) SEMKV_C(10)
-#undef SEMKV_C
-  return acc;
+#define SEMKV_O(C) if constexpr (C < NC) A[C] = chunk_operand<BASE, L, C, NW, NS>(seg, mask, lut);
+  SEMKV_O(0) SEMKV_O(1) SEMKV_O(2) SEMKV_O(3) SEMKV_O(4) SEMKV_O(5)
+  SEMKV_O(6) SEMKV_O(7) SEMKV_O(8) SEMKV_O(9) SEMKV_O(10)
+#undef SEMKV_O
 }
 
 // masks of the symbols of segment j (zero past the line's last symbol)
@@ -298,6 +299,7 @@ struct Plan {
   static constexpr int LUTH = 4 * Traits<BASE, LH>::LUTSTRIDE;   // dwords of the high-pool tables
   static constexpr int LUTL = 4 * Traits<BASE, LL>::LUTSTRIDE;
   static constexpr int NGV = GH::NGV;
+  static constexpr int NCKH = Traits<BASE, LH>::NCK, NCKL = Traits<BASE, LL>::NCK;
   static_assert(GH::NGV == GL::NGV && GH::LOPASS == GL::LOPASS, "pools share the value columns");
 };
 
@@ -314,8 +316,8 @@ struct Shared {
   float qorig[4][kD];                                        // query as given (fp16 tail)
   Fin tfin;                                                  // the fp16 tail's state
   TailScratch ts;
-  float zpart[4][4];
-  float zw[16];                                              // per (head, group): sum of q
+  alignas(16) uint4 aq[PL::NCKH + PL::NCKL][64];             // score A operands, per pool and lane
+  float zpart[4][4];                                         // per head: sums of q over 32/64 channels
   float zc[kDecodeWaves][4][4];                              // per wave, head, group: sum p * zero
   int last;
 };
@@ -356,6 +358,44 @@ __device__ inline void store_pieces(const uint4 (&r)[NMAX], uint8_t* lds, int la
   for (int j = 0; j < NMAX; ++j) *reinterpret_cast<uint4*>(lds + j * 1024 + lane * 16) = r[j];
 }
 
+// Score A operands of one pool for all 64 lane contexts, by the workgroup:
+// lane (n = 4h + kq, kg) chunk c slot e holds the query of head h at the
+// channel the slot addresses (zero past channel 127), restricted to metadata
+// group kq (affine) or split into an fp16 high (kq = 0) and low (kq = 1) part
+// of the plane-weighted query (tq).
+template <int BASE, int L, int G, int POOL, class PL>
+__device__ void build_aq(const DecodeArgs& a, Shared<PL>& sm) {
+  using Tr = Traits<BASE, L>;
+  using Ge = Geo<BASE, L, G>;
+  const float* mu = a.mu[POOL];
+  const float wP[2] = {BASE == 0 ? 1.0f : (L == 3 ? 1.0f : mu[3] - mu[2]),
+                       BASE == 0 ? 1.0f : (L == 3 ? 1.0f : mu[2] + mu[3])};
+  for (int item = threadIdx.x; item < Tr::NCK * 64; item += kThreads) {
+    const int c = item >> 6, ln = item & 63;
+    const int n = ln & 15, kg = ln >> 4, h = n >> 2, kq = n & 3;
+    const int cb = Tr::n * kg;
+    _Float16 v[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int k = Tr::SPC * c + e / Tr::STRIDE, w = e % Tr::STRIDE;
+      const int dig = slot_digit<BASE, L>(w), pl = slot_plane<BASE, L>(w);
+      v[e] = _Float16(0.0f);
+      if (dig >= 0) {
+        const int ch = cb + Tr::n * 4 * k + dig;         // >= 128: a pad slot, the query reads 0
+        if (BASE == 0) {
+          if (kq < Ge::NG && (ch >> __builtin_ctz(G)) == kq) v[e] = sm.qh[h][ch];
+        } else {
+          const float x = wP[pl] * sm.qf[h][ch];
+          const _Float16 hi = _Float16(x);
+          v[e] = kq == 0 ? hi : (kq == 1 ? _Float16(x - float(hi)) : _Float16(0.0f));
+        }
+      }
+    }
+    const uint4v u = __builtin_bit_cast(uint4v, half8{v[0], v[1], v[2], v[3], v[4], v[5], v[6], v[7]});
+    sm.aq[(POOL ? PL::NCKH : 0) + c][ln] = make_uint4(u.x, u.y, u.z, u.w);
+  }
+}
+
 // ---------------------------------------------------- one pool's records ----
 
 template <int BASE, int LH, int LL, int G, int POOL, class PL>
@@ -374,33 +414,12 @@ __device__ void run_pool(const DecodeArgs& a, Shared<PL>& sm, WaveState<PL::NGV>
   const float wP[2] = {BASE == 0 ? 1.0f : (L == 3 ? 1.0f : mu[3] - mu[2]),
                        BASE == 0 ? 1.0f : (L == 3 ? 1.0f : mu[2] + mu[3])};
 
-  // ---- score A operand: row 4h + kq of lane row n; slot -> channel of lane group kg
+  // ---- score A operand (built once per workgroup)
   half8 Aq[Tr::NCK];
-  {
-    const int h = n >> 2, kq = n & 3;
-    const int cb = Tr::n * kg;                 // channel of digit 0 of this lane group's first symbol
 #pragma unroll
-    for (int c = 0; c < Tr::NCK; ++c) {
-      _Float16 v[8];
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const int k = Tr::SPC * c + e / Tr::STRIDE, w = e % Tr::STRIDE;
-        const int dig = slot_digit<BASE, L>(w), pl = slot_plane<BASE, L>(w);
-        v[e] = _Float16(0.0f);
-        if (dig >= 0) {
-          const int ch = cb + Tr::n * 4 * k + dig;     // >= 128: a pad slot, the query reads 0
-          if (BASE == 0) {
-            const _Float16 x = sm.qh[h][ch];
-            v[e] = (kq < Ge::NG && (ch >> __builtin_ctz(G)) == kq) ? x : _Float16(0.0f);
-          } else {
-            const float x = wP[pl] * sm.qf[h][ch];
-            const _Float16 hi = _Float16(x);
-            v[e] = kq == 0 ? hi : (kq == 1 ? _Float16(x - float(hi)) : _Float16(0.0f));
-          }
-        }
-      }
-      Aq[c] = half8{v[0], v[1], v[2], v[3], v[4], v[5], v[6], v[7]};
-    }
+  for (int c = 0; c < Tr::NCK; ++c) {
+    const uint4 v = sm.aq[(POOL ? PL::NCKH : 0) + c][lane];
+    Aq[c] = __builtin_bit_cast(half8, uint4v{v.x, v.y, v.z, v.w});
   }
   const uint32_t* lut = sm.lut + (POOL ? PL::LUTH : 0) + kg * Tr::LUTSTRIDE;
   uint32_t kmask[Tr::NSK], vmask[Tr::NSV];
@@ -410,9 +429,21 @@ __device__ void run_pool(const DecodeArgs& a, Shared<PL>& sm, WaveState<PL::NGV>
   const int voff0 = seg_off<L, kSlots, kD>(kg, n), vstep = 16 * seg_line_bits<L, kSlots, kD>(kg);
   // softmax lanes: token n of each 16-token block, head r
   const int hs = r;
-  float zws[Ge::NG];
+  float zws[Ge::NG];                         // sum of q over each metadata group of head hs
+  {
+    constexpr int SEG = (BASE == 0 && G < 64) ? G : 64;
 #pragma unroll
-  for (int i = 0; i < Ge::NG; ++i) zws[i] = sm.zw[hs * 4 + i];
+    for (int i = 0; i < Ge::NG; ++i) {
+      float z = 0.0f;
+      if (BASE == 0) {
+#pragma unroll
+        for (int p = i * G / SEG; p < (i + 1) * G / SEG; ++p) z += sm.zpart[hs][p];
+      } else if (i == 0) {
+        z = sm.zpart[hs][0] + sm.zpart[hs][1];
+      }
+      zws[i] = z;
+    }
+  }
   // value B operand lanes: column n = 4h + gg
   const int hv = n >> 2, gg = n & 3;
   const int vg = gg < Ge::NGV ? gg : (!Ge::LOPASS && gg < 2 * Ge::NGV ? gg - Ge::NGV : -1);
@@ -437,14 +468,19 @@ __device__ void run_pool(const DecodeArgs& a, Shared<PL>& sm, WaveState<PL::NGV>
 
     // ---- scores: C[(h, kq)][token] = q_h,kq . codes; lane holds token n, head r
     float lg[4];
+    // all four K segments in one round trip
+    uint32_t kseg[4][Tr::KSEGW];
+#pragma unroll
+    for (int blk = 0; blk < 4; ++blk) lds_segment<Tr::KSEGW>(rec, koff0 + blk * kstep, kseg[blk]);
 #pragma unroll
     for (int blk = 0; blk < 4; ++blk) {
-      uint32_t seg[Tr::KSEGW];
-      lds_segment<Tr::KSEGW>(rec, koff0 + blk * kstep, seg);
+      // every table read of the block is in flight before its first product
+      half8 Bk[Tr::NCK];
+      chunk_operands<BASE, L, Tr::KSEGW, Tr::NSK, Tr::NCK>(kseg[blk], kmask, lut, Bk);
+      __builtin_amdgcn_sched_barrier(0);
       float4v acc = float4v{0, 0, 0, 0};
-#define SEMKV_S(C) if constexpr (C < Tr::NCK) acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(Aq[C], chunk_operand<BASE, L, C, Tr::KSEGW, Tr::NSK>(seg, kmask, lut), acc, 0, 0, 0);
-      SEMKV_S(0) SEMKV_S(1) SEMKV_S(2) SEMKV_S(3) SEMKV_S(4) SEMKV_S(5) SEMKV_S(6) SEMKV_S(7) SEMKV_S(8) SEMKV_S(9) SEMKV_S(10)
-#undef SEMKV_S
+#pragma unroll
+      for (int ch = 0; ch < Tr::NCK; ++ch) acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(Aq[ch], Bk[ch], acc, 0, 0, 0);
       const int t = 16 * blk + n;
       float x = 0.0f;
       if (BASE == 0) {
@@ -533,12 +569,20 @@ __device__ void run_pool(const DecodeArgs& a, Shared<PL>& sm, WaveState<PL::NGV>
       if constexpr (Ge::LOPASS) Bl[c] = half8{w[0], w[1], w[2], w[3], w[4], w[5], w[6], w[7]};
     }
     const uint8_t* vbody = rec + Tr::TB;
+    uint32_t vseg[8][Tr::VSEGW];
+#pragma unroll
+    for (int cb = 0; cb < 8; ++cb) lds_segment<Tr::VSEGW>(vbody, voff0 + cb * vstep, vseg[cb]);
 #pragma unroll
     for (int cb = 0; cb < 8; ++cb) {
-      uint32_t seg[Tr::VSEGW];
-      lds_segment<Tr::VSEGW>(vbody, voff0 + cb * vstep, seg);
-      st.o[cb] = contract<BASE, L, Tr::VSEGW, Tr::NSV, Tr::NCV>(seg, vmask, Bp, st.o[cb], lut);
-      if constexpr (Ge::LOPASS) st.o[cb] = contract<BASE, L, Tr::VSEGW, Tr::NSV, Tr::NCV>(seg, vmask, Bl, st.o[cb], lut);
+      half8 Av[Tr::NCV];
+      chunk_operands<BASE, L, Tr::VSEGW, Tr::NSV, Tr::NCV>(vseg[cb], vmask, lut, Av);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int ch = 0; ch < Tr::NCV; ++ch) st.o[cb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(Av[ch], Bp[ch], st.o[cb], 0, 0, 0);
+      if constexpr (Ge::LOPASS) {
+#pragma unroll
+        for (int ch = 0; ch < Tr::NCV; ++ch) st.o[cb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(Av[ch], Bl[ch], st.o[cb], 0, 0, 0);
+      }
     }
     // the next record replaces this one in the wave's buffer (LDS serves a
     // wave's accesses in order: the reads above come first)
@@ -692,20 +736,37 @@ __device__ void merge_splits(const DecodeArgs& a, Shared<PL>& sm, int b, int kvh
   float* mm = reinterpret_cast<float*>(&sm.stage[0][0]);   // [ns][4] maxima
   float* ll = mm + kMaxSplits * 4;                          // [ns][4] sums
   static_assert(sizeof(sm.stage) >= 2 * kMaxSplits * 4 * sizeof(float), "merge scratch");
-  for (int i = tid; i < ns * 4; i += kThreads) {
-    mm[i] = ld_agent(unit + i * kPartial);
-    ll[i] = ld_agent(unit + i * kPartial + 1);
+  static_assert(kMaxSplits * 4 <= 2 * kThreads, "two (split, head) pairs per thread");
+  // one round of loads: this thread's (split, head) maxima and sums, and its
+  // channel of the first kBatch partials
+  constexpr int kBatch = 32;
+  float mv[2], lv[2], x[kBatch];
+#pragma unroll
+  for (int k = 0; k < 2; ++k) {
+    const int i = tid + k * kThreads;
+    mv[k] = i < ns * 4 ? ld_agent(unit + i * kPartial) : 0.0f;
+    lv[k] = i < ns * 4 ? ld_agent(unit + i * kPartial + 1) : 0.0f;
+  }
+  const float* op = unit + h * kPartial + 4 + c;
+#pragma unroll
+  for (int k = 0; k < kBatch; ++k) x[k] = k < ns ? ld_agent(op + k * 4 * kPartial) : 0.0f;
+#pragma unroll
+  for (int k = 0; k < 2; ++k) {
+    const int i = tid + k * kThreads;
+    if (i < ns * 4) {
+      mm[i] = mv[k];
+      ll[i] = lv[k];
+    }
   }
   __syncthreads();
   float M = -INFINITY;
   for (int s = 0; s < ns; ++s) M = fmaxf(M, mm[s * 4 + h]);
   float Lsum = 0.0f, o = 0.0f;
-  const float* op = unit + h * kPartial + 4 + c;
-  constexpr int kBatch = 16;                 // partial loads in flight per thread
   for (int s0 = 0; s0 < ns; s0 += kBatch) {
-    float x[kBatch];
+    if (s0 > 0) {
 #pragma unroll
-    for (int k = 0; k < kBatch; ++k) x[k] = s0 + k < ns ? ld_agent(op + (s0 + k) * 4 * kPartial) : 0.0f;
+      for (int k = 0; k < kBatch; ++k) x[k] = s0 + k < ns ? ld_agent(op + (s0 + k) * 4 * kPartial) : 0.0f;
+    }
 #pragma unroll
     for (int k = 0; k < kBatch; ++k) {
       if (s0 + k < ns) {
@@ -790,26 +851,15 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeArgs a) {
   if (BASE == 1)                            // rotate: H (sign . q)
     for (int hs = 1; hs < kD; hs <<= 1) fwht_stage(sm.qf, hs);
   {
-    // per (head, group) sums of the query over segments of SEG lanes
+    // per head: sums of the query over aligned runs of SEG channels
     constexpr int SEG = (BASE == 0 && G < 64) ? G : 64;
     float x = sm.qf[h][c];
 #pragma unroll
     for (int o = 1; o < SEG; o <<= 1) x += __shfl_xor(x, o);
     if ((c % SEG) == 0) sm.zpart[h][c / SEG] = x;
   }
-  __syncthreads();
-  if (tid < 16) {
-    const int hh = tid >> 2, gq = tid & 3;
-    float s = 0.0f;
-    if (BASE == 0) {
-      constexpr int SEG = G < 64 ? G : 64;
-      if (gq < kD / G)
-        for (int p = gq * G / SEG; p < (gq + 1) * G / SEG; ++p) s += sm.zpart[hh][p];
-    } else if (gq == 0) {
-      s = sm.zpart[hh][0] + sm.zpart[hh][1];
-    }
-    sm.zw[tid] = s;
-  }
+  build_aq<BASE, LH, G, 0>(a, sm);
+  build_aq<BASE, LL, G, 1>(a, sm);
   __syncthreads();
 
   // ---- this wave's records
