@@ -19,6 +19,25 @@ constexpr int kMaxBodyWords = 2672 / 4; // largest body: L = 6
 __device__ inline float h2f(uint16_t b) { return __half2float(__ushort_as_half(b)); }
 __device__ inline uint16_t f2h(float f) { return __half_as_ushort(__float2half_rn(f)); }
 
+// Correctly rounded fp32 square root of a >= 0.  The hardware result is within
+// one ulp; the neighbour whose rounding interval holds sqrt(a) is chosen by
+// comparing a with the squared interval ends, which are exact in double (a
+// 25-bit midpoint squares to at most 50 bits).  sqrt is never exactly halfway
+// between two floats, so no tie arises.
+__device__ inline float sqrt_rn(float a) {
+  float r = __builtin_sqrtf(a);
+  if (!(a > 0.0f) || !(a < INFINITY)) return r;
+  const double ad = double(a);
+#pragma unroll
+  for (int k = 0; k < 2; ++k) {
+    const float dn = __uint_as_float(__float_as_uint(r) - 1u), up = __uint_as_float(__float_as_uint(r) + 1u);
+    const double lo = 0.5 * (double(dn) + double(r)), hi = 0.5 * (double(r) + double(up));
+    if (ad < lo * lo) r = dn;
+    else if (ad >= hi * hi) r = up;
+  }
+  return r;
+}
+
 __device__ inline void load_quarter(const uint16_t* src, float x[32]) {
   const uint4* p = reinterpret_cast<const uint4*>(src);
 #pragma unroll
@@ -110,7 +129,7 @@ __device__ uint16_t tq_quarter(const float x[32], int q, const uint32_t* sw, con
   for (int h = 16; h >= 1; h >>= 1)
 #pragma unroll
     for (int i = 0; i < h; ++i) a[i] = a[i] + a[i + h];
-  uint16_t r16 = f2h(__fsqrt_rn(a[0]));
+  uint16_t r16 = f2h(sqrt_rn(a[0]));
   if ((r16 & 0x7FFFu) == 0x7C00u) r16 = 0x7BFFu;       // saturate to 65504
   int lane = __lane_id();
   r16 = uint16_t(__shfl(int(r16), lane & ~3));

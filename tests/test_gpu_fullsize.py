@@ -1,0 +1,136 @@
+"""GPU parity at the full size of each benchmark workload, in the launch
+configuration bench.py times: full batch, kv heads and context, so the rank
+kernel sees every sequence and a decode launch has the benchmark's grid (the
+grid does not depend on the layer count; one or two layers stand in for 32).
+
+Checked against the oracle: slot lists and flags of every sequence bit-exact;
+the packed records of sampled (sequence, layer, kv head) units bit-exact;
+decode attention of the sampled units within 2e-3 max-abs.  Units that are not
+sampled hold filler rows (the rows of a sampled unit of the same layer); their
+values cannot affect a sampled unit's records or outputs."""
+import numpy as np
+import pytest
+
+from oracle import oracle as O
+from tests import gpu_util as U
+from workloads import get_config, synth
+
+pytestmark = pytest.mark.gpu
+
+
+def _layer_kv_gpu(cfgw, l, T, sampled):
+    """fp16 [B, H, T, 128] K and V on the device: synthetic rows for the
+    sampled units of layer l, the first sampled unit's rows elsewhere."""
+    import torch
+    B, H = cfgw.batch, cfgw.n_kv_heads
+    mine = [(b, h) for (b, ll, h) in sampled if ll == l]
+    assert mine, "every layer needs a sampled unit"
+    K = torch.empty((B, H, T, 128), dtype=torch.float16, device="cuda")
+    V = torch.empty_like(K)
+    k0, v0 = synth.unit_kv(cfgw, l, mine[0][0], mine[0][1], T)
+    K[:] = torch.from_numpy(k0).cuda()
+    V[:] = torch.from_numpy(v0).cuda()
+    for (b, h) in mine[1:]:
+        k, v = synth.unit_kv(cfgw, l, b, h, T)
+        K[b, h] = torch.from_numpy(k).cuda()
+        V[b, h] = torch.from_numpy(v).cuda()
+    return K, V
+
+
+def _prefill_and_check(cfgw, n_layers, sampled, max_new=0):
+    import torch
+    T = cfgw.prompt_len
+    cache = U.make_cache(cfgw, T, n_layers=n_layers, max_new=max_new)
+    scores = synth.all_scores(cfgw, T)
+    hi, lo = cache.rank(torch.from_numpy(scores).cuda())
+    for l in range(n_layers):
+        K, V = _layer_kv_gpu(cfgw, l, T, sampled)
+        cache.quantize_pack(l, K, V, hi, lo)
+        del K, V
+    torch.cuda.synchronize()
+    assert cache.status() == 0
+    hi, lo = hi.cpu().numpy(), lo.cpu().numpy()
+    flags = []
+    for b in range(cfgw.batch):
+        f, ohi, olo = O.rank(scores[b], cfgw.r_num, cfgw.r_den)
+        assert np.array_equal(hi[b], ohi) and np.array_equal(lo[b], olo), "slot lists, seq %d" % b
+        assert np.array_equal(U.flags_bits(cache, b, T), f), "flags, seq %d" % b
+        flags.append(f)
+    oracle = {}
+    K_hi = O.top_count(T, cfgw.r_num, cfgw.r_den)
+    for (b, l, h) in sampled:
+        u = U.oracle_unit(cfgw, l, b, h, flags[b], T)
+        for p, n in ((0, K_hi), (1, T - K_hi)):
+            got = U.gpu_records(cache, b, l, h, p, n)
+            want = u.records(p)
+            if not np.array_equal(got, want):
+                bad = np.flatnonzero(got != want)
+                raise AssertionError("unit %s pool %d: %d bytes differ, first at %d" % ((b, l, h), p, bad.size, bad[0]))
+        oracle[(b, l, h)] = u
+    return cache, oracle
+
+
+def _check_decode(cache, cfgw, oracle, step=0):
+    import torch
+    for l in sorted({l for (_, l, _) in oracle}):
+        q = synth.query(cfgw, l, step)
+        out = cache.decode_attn(l, torch.from_numpy(q).cuda()).cpu().numpy()
+        for (b, ll, h), u in oracle.items():
+            if ll == l:
+                want = u.attend(q[b, 4 * h:4 * h + 4].astype(np.float64))
+                U.assert_attention_close(out[b, 4 * h:4 * h + 4], want, "unit %s" % ((b, l, h),))
+
+
+def test_llama8b_b1_t32768_affine_full_size():
+    cfgw = get_config("llama8b_kv_b1_t32768_affine")
+    cache, oracle = _prefill_and_check(cfgw, 2, [(0, 0, 0), (0, 1, 5)])
+    _check_decode(cache, cfgw, oracle)
+
+
+def test_batched_b16_t16384_dirichlet_full_size():
+    cfgw = get_config("llama8b_kv_b16_t16384_affine_dirichlet")
+    cache, oracle = _prefill_and_check(cfgw, 1, [(0, 0, 2), (15, 0, 7), (9, 0, 0)])
+    _check_decode(cache, cfgw, oracle)
+
+
+def test_tq_b1_t131072_full_size():
+    cfgw = get_config("llama8b_kv_b1_t131072_tq")
+    cache, oracle = _prefill_and_check(cfgw, 1, [(0, 0, 6)])
+    _check_decode(cache, cfgw, oracle)
+
+
+def test_mistral_b4_t32768_generation_full_size():
+    """Prompt of 32768 tokens in 4 sequences, then 130 generated tokens
+    (two closed blocks and an fp16 tail of 2) through the deferred path."""
+    import torch
+    cfgw = get_config("mistral7b_kv_b4_t32768_gen2048_deferred")
+    n_gen = 130
+    sampled = [(0, 0, 1), (3, 0, 6)]
+    cache, oracle = _prefill_and_check(cfgw, 1, sampled, max_new=cfgw.n_gen)
+    B, H = cfgw.batch, cfgw.n_kv_heads
+    gen = {(b, h): synth.unit_gen_kv(cfgw, 0, b, h, n_gen) for (b, _, h) in sampled}
+    gscore = synth.gen_scores(cfgw, n_gen)
+    filler = gen[(sampled[0][0], sampled[0][2])]
+    for i in range(n_gen):
+        k = np.empty((B, H, 128), np.float16)
+        v = np.empty((B, H, 128), np.float16)
+        k[:], v[:] = filler[0][i], filler[1][i]
+        for (b, h), (gk, gv) in gen.items():
+            k[b, h], v[b, h] = gk[i], gv[i]
+        cache.append_kv(0, torch.from_numpy(k).cuda(), torch.from_numpy(v).cuda())
+        for (b, _, h), u in oracle.items():
+            u.append_kv(gen[(b, h)][0][i], gen[(b, h)][1][i])
+        if i == 100:                       # mid-block: 37 rows in the fp16 tail
+            _check_decode(cache, cfgw, oracle, step=i)
+        cache.append_commit(torch.from_numpy(gscore[i]).cuda())
+        for (b, _, h), u in oracle.items():
+            u.commit(gscore[i][b])
+    torch.cuda.synchronize()
+    assert cache.status() == 0
+    _check_decode(cache, cfgw, oracle, step=n_gen)
+    for (b, l, h), u in oracle.items():
+        for p in (0, 1):
+            n = u.count(p)
+            assert n == (cache.c.n_hi if p == 0 else cache.c.n_lo)
+            got = U.gpu_records(cache, b, l, h, p, n)
+            assert np.array_equal(got, u.records(p)), "unit %s pool %d after generation" % ((b, l, h), p)

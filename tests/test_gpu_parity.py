@@ -135,3 +135,21 @@ def test_status_word_reports_nan_and_inf():
     s2 = synth.all_scores(cfgw, T)
     U.prefill(cache2, cfgw, T, scores=s2, kv=lambda l: (K, V))
     assert cache2.status() & 2
+
+
+def test_tq_norm_rounding_edge_rows():
+    """Rows whose norm sits at an fp16 rounding edge (a square root one ulp off
+    would store a different norm): packed records bit-exact."""
+    import torch
+    from tests.norm_edge import edge_rows
+    cfgw = get_config(4, n_layers=1, n_kv_heads=1, n_q_heads=4)
+    T = 256
+    X = edge_rows(2 * T).reshape(2, T, 128)
+    K, V = X[0][None, None], X[1][None, None]
+    cache = U.make_cache(cfgw, T, max_new=0)
+    s = synth.all_scores(cfgw, T)
+    U.prefill(cache, cfgw, T, scores=s, kv=lambda l: (K, V))
+    f, _, _ = O.rank(s[0], cfgw.r_num, cfgw.r_den)
+    u = U.oracle_unit(cfgw, 0, 0, 0, f, T, kv=lambda l: (K, V))
+    for p in (0, 1):
+        assert np.array_equal(U.gpu_records(cache, 0, 0, 0, p, u.count(p)), u.records(p)), "pool %d" % p

@@ -144,3 +144,13 @@ def test_nonfinite_input_is_reported():
         O.quantize_rows(X, 0, 5, 128)
     with pytest.raises(O.OracleError):
         O.quantize_rows(X, 1, 3, 128, np.zeros(4, np.uint32))
+
+
+def test_tq_norm_is_correctly_rounded_at_fp16_edges():
+    """rho = RN16(RN32(sqrt(sum of squares))) on rows built to sit within one
+    fp32 ulp of an fp16 rounding midpoint (Sec. 4.9: the stored norm)."""
+    from tests.norm_edge import correctly_rounded_norm_f16, edge_rows
+    X = edge_rows(64)
+    sw = np.zeros(4, np.uint32)
+    _, rho = O.quantize_rows(X, 1, 4, sign_words=sw)
+    assert np.array_equal(np.asarray(rho, np.uint16).reshape(-1), correctly_rounded_norm_f16(X))
