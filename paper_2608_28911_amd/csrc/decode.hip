@@ -4,8 +4,7 @@
 // Work split: the tiles of one (sequence, kv head) unit -- its high pool, then
 // its low pool -- are cut into nsplit balanced runs, one per workgroup, with
 // nsplit chosen by the host so that the whole grid is resident at once.  A
-// workgroup is kDecodeWaves waves; wave w takes tiles w, w + kDecodeWaves, ...
-// of its run and keeps its own online-softmax state for the 4 query heads of
+// workgroup is NW = 8 waves; wave w takes tiles w, w + NW, ... of its run and keeps its own online-softmax state for the 4 query heads of
 // the kv head.  Records are staged through registers: the next record's
 // 16-byte pieces are loaded while the current one is computed from the wave's
 // LDS buffer, then written over it.  Per record:
@@ -40,7 +39,6 @@ typedef uint32_t uint4v __attribute__((ext_vector_type(4)));
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kRsqrtD = 0.08838834764831845f;   // 1 / sqrt(128)
 constexpr float kDigitScale = 262144.0f;          // 2^18: digit d is fed as d * 2^-18
-constexpr int kThreads = 64 * kDecodeWaves;
 constexpr int kQPad = 160;                         // query rows, zero past channel 127
 
 // ------------------------------------------------------------ traits ----
@@ -69,10 +67,11 @@ struct Traits {
   static constexpr int KSEGW = (NSK * W + 31) / 32;          // normalized dwords of a K segment
   static constexpr int VSEGW = (NSV * W + 31) / 32;
   // decode table: symbol -> MFMA operand dwords (codes pre-shifted to d << 6).
-  // L = 6 splits a symbol into s mod 216 (3 codes) and s div 216 (2 codes).
+  // L = 6 splits a symbol into s mod 216 (3 codes) and s div 216 (2 codes),
+  // two dwords per entry in both parts.
   static constexpr int EDW = STRIDE / 2;                     // dwords per table entry
   static constexpr int NENT = L == 6 ? 216 : ipow(L, n);
-  static constexpr int LUTDW = L == 6 ? 216 * 2 + 36 : NENT * EDW;
+  static constexpr int LUTDW = L == 6 ? 216 * 2 + 36 * 2 : NENT * EDW;
   static constexpr int LUTSTRIDE = (LUTDW + 63) / 64 * 64 + 16;   // replicas start 16 banks apart
   // largest query channel an A-operand slot addresses (past 127: a zero pad)
   static constexpr int MAXCH = n * (3 + 4 * (SPC * NCK - 1)) + n - 1;
@@ -116,6 +115,14 @@ __device__ inline uint32_t mulhi24(uint32_t a, uint32_t b) {
   return uint32_t((uint64_t(a & 0xFFFFFFu) * uint64_t(b & 0xFFFFFFu)) >> 32);
 }
 
+// a * b + c on 24-bit signed a, b: one full-rate v_mad_i32_i24 (left to
+// itself the compiler widens this to a 64-bit multiply-add)
+__device__ inline uint32_t mad_i24(uint32_t a, int b, uint32_t c) {
+  uint32_t r;
+  __asm__("v_mad_i32_i24 %0, %1, %2, %3" : "=v"(r) : "v"(a), "s"(b), "v"(c));
+  return r;
+}
+
 // bits [OFF, OFF+W) of a normalized segment
 template <int OFF, int W, int NW>
 __device__ inline uint32_t field(const uint32_t (&seg)[NW]) {
@@ -130,8 +137,8 @@ __device__ inline uint32_t field(const uint32_t (&seg)[NW]) {
 // ------------------------------------------------------ decode tables ----
 
 // Dword e of the decode table: MFMA slots 2k, 2k+1 of symbol value v (codes as
-// d << 6); for L = 6, entries 0..431 map s mod 216 to slots 0-3 and 432..467
-// map s div 216 to slots 4, 5.
+// d << 6); for L = 6, dwords 0..431 map s mod 216 to slots 0-3 and 432..503
+// map s div 216 to slots 4-7 (6 and 7 are zero pads).
 template <int BASE, int L>
 __host__ __device__ constexpr uint32_t lut_entry(int e) {
   using Tr = Traits<BASE, L>;
@@ -140,8 +147,8 @@ __host__ __device__ constexpr uint32_t lut_entry(int e) {
       const int v = e / 2;
       return (e & 1) ? (uint32_t(v / 36) << 6) : (uint32_t(v % 6) << 6) | (uint32_t(v / 6 % 6) << 22);
     }
-    const int v = e - 432;
-    return (uint32_t(v % 6) << 6) | (uint32_t(v / 6) << 22);
+    const int v = (e - 432) / 2;
+    return ((e - 432) & 1) ? 0u : (uint32_t(v % 6) << 6) | (uint32_t(v / 6) << 22);
   }
   const int v = e / Tr::EDW, k = e % Tr::EDW;
   uint32_t w = 0;
@@ -187,9 +194,10 @@ __device__ inline half8 chunk_operand(const uint32_t (&seg)[NW], const uint32_t 
   if constexpr (L == 6) {
     const uint32_t v = seg_symbol<BASE, L, C, NW, NS>(seg, mask);
     const uint32_t hi = mulhi24(v << 8, magic(6, 3));      // v div 216
-    const uint32_t lo = v - 216u * hi;
+    const uint32_t lo = mad_i24(hi, -216, v);               // v mod 216
     const uint2 a = *reinterpret_cast<const uint2*>(lut + 2 * lo);
-    r = uint4v{a.x, a.y, lut[432 + hi], 0u};
+    const uint2 b = *reinterpret_cast<const uint2*>(lut + 432 + 2 * hi);
+    r = uint4v{a.x, a.y, b.x, b.y};
   } else if constexpr (Tr::SPC == 2) {
     const uint2 a = *reinterpret_cast<const uint2*>(lut + 2 * seg_symbol<BASE, L, 2 * C, NW, NS>(seg, mask));
     const uint2 b = *reinterpret_cast<const uint2*>(lut + 2 * seg_symbol<BASE, L, 2 * C + 1, NW, NS>(seg, mask));
@@ -301,6 +309,17 @@ struct Plan {
   static constexpr int NGV = GH::NGV;
   static constexpr int NCKH = Traits<BASE, LH>::NCK, NCKL = Traits<BASE, LL>::NCK;
   static_assert(GH::NGV == GL::NGV && GH::LOPASS == GL::LOPASS, "pools share the value columns");
+  // LDS of a workgroup of nw waves (the Shared layout below, with margin)
+  static constexpr int lds_bytes(int nw) {
+    return nw * (NLD * 1024 + PV * 2 + 64) + (LUTH + LUTL) * 4 + (NCKH + NCKL) * 64 * 16 +
+           4 * kQPad * 6 + 4 * kD * 4 + 2080 + 3104 + 256;
+  }
+  // 8 waves: 2 per SIMD, one workgroup per compute unit (12 waves, 3 per SIMD,
+  // measured no faster: the record work is bound by the compute unit's issue
+  // rate, not by latency)
+  static constexpr int NW = 8;
+  static_assert(lds_bytes(NW) <= 160 * 1024, "LDS");
+  static constexpr int NT = 64 * NW;
 };
 
 struct Fin { float m[4], l[4]; float o[4][kD]; };             // one wave's state, merged form
@@ -308,9 +327,9 @@ struct TailScratch { float lg[4][kSlots]; float mx[4], sum[4]; float o[4][kD]; }
 
 template <class PL>
 struct Shared {
-  alignas(16) uint8_t stage[kDecodeWaves][PL::NLD * 1024];   // per wave: one record, later its Fin
+  alignas(16) uint8_t stage[PL::NW][PL::NLD * 1024];         // per wave: one record, later its Fin
   alignas(16) uint32_t lut[PL::LUTH + PL::LUTL];             // decode tables: high pool, low pool
-  alignas(16) _Float16 pv[kDecodeWaves][PL::PV];             // per wave p*s weights, fp16 hi/lo
+  alignas(16) _Float16 pv[PL::NW][PL::PV];                   // per wave p*s weights, fp16 hi/lo
   alignas(16) _Float16 qh[4][kQPad];                         // fp16 query (affine base)
   alignas(16) float qf[4][kQPad];                            // fp32 query, rotated for tq
   float qorig[4][kD];                                        // query as given (fp16 tail)
@@ -318,7 +337,7 @@ struct Shared {
   TailScratch ts;
   alignas(16) uint4 aq[PL::NCKH + PL::NCKL][64];             // score A operands, per pool and lane
   float zpart[4][4];                                         // per head: sums of q over 32/64 channels
-  float zc[kDecodeWaves][4][4];                              // per wave, head, group: sum p * zero
+  float zc[PL::NW][4][4];                                    // per wave, head, group: sum p * zero
   int last;
 };
 
@@ -370,7 +389,7 @@ __device__ void build_aq(const DecodeArgs& a, Shared<PL>& sm) {
   const float* mu = a.mu[POOL];
   const float wP[2] = {BASE == 0 ? 1.0f : (L == 3 ? 1.0f : mu[3] - mu[2]),
                        BASE == 0 ? 1.0f : (L == 3 ? 1.0f : mu[2] + mu[3])};
-  for (int item = threadIdx.x; item < Tr::NCK * 64; item += kThreads) {
+  for (int item = threadIdx.x; item < Tr::NCK * 64; item += PL::NT) {
     const int c = item >> 6, ln = item & 63;
     const int n = ln & 15, kg = ln >> 4, h = n >> 2, kq = n & 3;
     const int cb = Tr::n * kg;
@@ -414,7 +433,7 @@ __device__ void run_pool(const DecodeArgs& a, Shared<PL>& sm, WaveState<PL::NGV>
   const float wP[2] = {BASE == 0 ? 1.0f : (L == 3 ? 1.0f : mu[3] - mu[2]),
                        BASE == 0 ? 1.0f : (L == 3 ? 1.0f : mu[2] + mu[3])};
 
-  // ---- score A operand (built once per workgroup)
+  // ---- score A operands (built once per workgroup)
   half8 Aq[Tr::NCK];
 #pragma unroll
   for (int c = 0; c < Tr::NCK; ++c) {
@@ -458,9 +477,9 @@ __device__ void run_pool(const DecodeArgs& a, Shared<PL>& sm, WaveState<PL::NGV>
   const int64_t nrows = a.n_rows[POOL];
 
   for (int it = i0; it < i1; ++it) {
-    const int tile = first + kDecodeWaves * it;
+    const int tile = first + PL::NW * it;
     const bool more = it + 1 < count;
-    if (more) load_tile<BASE, LH, LL, G>(a.g, unit, tile + kDecodeWaves, nt0, R, lane);
+    if (more) load_tile<BASE, LH, LL, G>(a.g, unit, tile + PL::NW, nt0, R, lane);
     const int ptile = POOL ? tile - nt0 : tile;
     const uint8_t* kmeta = rec + 2 * Tr::TB;
     const uint8_t* vmeta = kmeta + Ge::MB;
@@ -468,29 +487,50 @@ __device__ void run_pool(const DecodeArgs& a, Shared<PL>& sm, WaveState<PL::NGV>
 
     // ---- scores: C[(h, kq)][token] = q_h,kq . codes; lane holds token n, head r
     float lg[4];
-    // all four K segments in one round trip
+    // all four K segments and the lane's metadata words in one round trip
     uint32_t kseg[4][Tr::KSEGW];
 #pragma unroll
     for (int blk = 0; blk < 4; ++blk) lds_segment<Tr::KSEGW>(rec, koff0 + blk * kstep, kseg[blk]);
+    constexpr int NKM = BASE == 0 ? Ge::NG : 1, NVM = BASE == 0 ? Ge::NGV : 1;
+    uint32_t km[4][NKM], vm[4][NVM];
 #pragma unroll
     for (int blk = 0; blk < 4; ++blk) {
-      // every table read of the block is in flight before its first product
-      half8 Bk[Tr::NCK];
-      chunk_operands<BASE, L, Tr::KSEGW, Tr::NSK, Tr::NCK>(kseg[blk], kmask, lut, Bk);
+      const int t = 16 * blk + n;
+#pragma unroll
+      for (int i = 0; i < NKM; ++i)
+        km[blk][i] = BASE == 0 ? *reinterpret_cast<const uint32_t*>(kmeta + (i * kSlots + t) * 4)
+                               : uint32_t(*reinterpret_cast<const uint16_t*>(kmeta + t * 2));
+#pragma unroll
+      for (int i = 0; i < NVM; ++i)
+        vm[blk][i] = BASE == 0 ? *reinterpret_cast<const uint32_t*>(vmeta + (i * kSlots + t) * 4)
+                               : uint32_t(*reinterpret_cast<const uint16_t*>(vmeta + t * 2));
+    }
+    // software pipeline: the next block's table reads are in flight during
+    // the current block's products
+    half8 Bk[2][Tr::NCK];
+    chunk_operands<BASE, L, Tr::KSEGW, Tr::NSK, Tr::NCK>(kseg[0], kmask, lut, Bk[0]);
+    float4v acck[4];
+#pragma unroll
+    for (int blk = 0; blk < 4; ++blk) {
+      if (blk + 1 < 4) chunk_operands<BASE, L, Tr::KSEGW, Tr::NSK, Tr::NCK>(kseg[blk + 1], kmask, lut, Bk[(blk + 1) & 1]);
       __builtin_amdgcn_sched_barrier(0);
       float4v acc = float4v{0, 0, 0, 0};
 #pragma unroll
-      for (int ch = 0; ch < Tr::NCK; ++ch) acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(Aq[ch], Bk[ch], acc, 0, 0, 0);
+      for (int ch = 0; ch < Tr::NCK; ++ch) acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(Aq[ch], Bk[blk & 1][ch], acc, 0, 0, 0);
+      acck[blk] = acc;
+      __builtin_amdgcn_sched_barrier(0);
+    }
+#pragma unroll
+    for (int blk = 0; blk < 4; ++blk) {
+      const float4v acc = acck[blk];
       const int t = 16 * blk + n;
       float x = 0.0f;
       if (BASE == 0) {
 #pragma unroll
-        for (int i = 0; i < Ge::NG; ++i) {
-          const uint32_t m = *reinterpret_cast<const uint32_t*>(kmeta + (i * kSlots + t) * 4);
-          x += acc[i] * hf(m & 0xFFFFu) + hf(m >> 16) * zws[i] * (1.0f / kDigitScale);
-        }
+        for (int i = 0; i < Ge::NG; ++i)
+          x += acc[i] * hf(km[blk][i] & 0xFFFFu) + hf(km[blk][i] >> 16) * zws[i] * (1.0f / kDigitScale);
       } else {
-        const float rho = hf(*reinterpret_cast<const uint16_t*>(kmeta + t * 2));
+        const float rho = hf(uint16_t(km[blk][0]));
         x = (acc[0] + acc[1]) * (rho * cS) + rho * cZ * zws[0] * (1.0f / kDigitScale);
       }
       lg[blk] = t < nvalid ? x * (kDigitScale * kLog2e * kRsqrtD) : -INFINITY;
@@ -512,7 +552,7 @@ __device__ void run_pool(const DecodeArgs& a, Shared<PL>& sm, WaveState<PL::NGV>
       if (BASE == 0) {
 #pragma unroll
         for (int i = 0; i < Ge::NGV; ++i) {
-          const uint32_t m = *reinterpret_cast<const uint32_t*>(vmeta + (i * kSlots + t) * 4);
+          const uint32_t m = vm[blk][i];
           const float x = p * hf(m & 0xFFFFu);
           const _Float16 hi = _Float16(x);
           pvw[((0 * 4 + hs) * Ge::NGV + i) * kPvTok + t] = hi;
@@ -520,7 +560,7 @@ __device__ void run_pool(const DecodeArgs& a, Shared<PL>& sm, WaveState<PL::NGV>
           st.z[i] += p * hf(m >> 16);
         }
       } else {
-        const float rho = hf(*reinterpret_cast<const uint16_t*>(vmeta + t * 2));
+        const float rho = hf(uint16_t(vm[blk][0]));
         const float ps = p * rho * cS;
 #pragma unroll
         for (int pl = 0; pl < Ge::NPL; ++pl) {
@@ -572,17 +612,19 @@ __device__ void run_pool(const DecodeArgs& a, Shared<PL>& sm, WaveState<PL::NGV>
     uint32_t vseg[8][Tr::VSEGW];
 #pragma unroll
     for (int cb = 0; cb < 8; ++cb) lds_segment<Tr::VSEGW>(vbody, voff0 + cb * vstep, vseg[cb]);
+    half8 Av[2][Tr::NCV];
+    chunk_operands<BASE, L, Tr::VSEGW, Tr::NSV, Tr::NCV>(vseg[0], vmask, lut, Av[0]);
 #pragma unroll
     for (int cb = 0; cb < 8; ++cb) {
-      half8 Av[Tr::NCV];
-      chunk_operands<BASE, L, Tr::VSEGW, Tr::NSV, Tr::NCV>(vseg[cb], vmask, lut, Av);
+      if (cb + 1 < 8) chunk_operands<BASE, L, Tr::VSEGW, Tr::NSV, Tr::NCV>(vseg[cb + 1], vmask, lut, Av[(cb + 1) & 1]);
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-      for (int ch = 0; ch < Tr::NCV; ++ch) st.o[cb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(Av[ch], Bp[ch], st.o[cb], 0, 0, 0);
+      for (int ch = 0; ch < Tr::NCV; ++ch) st.o[cb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(Av[cb & 1][ch], Bp[ch], st.o[cb], 0, 0, 0);
       if constexpr (Ge::LOPASS) {
 #pragma unroll
-        for (int ch = 0; ch < Tr::NCV; ++ch) st.o[cb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(Av[ch], Bl[ch], st.o[cb], 0, 0, 0);
+        for (int ch = 0; ch < Tr::NCV; ++ch) st.o[cb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(Av[cb & 1][ch], Bl[ch], st.o[cb], 0, 0, 0);
       }
+      __builtin_amdgcn_sched_barrier(0);
     }
     // the next record replaces this one in the wave's buffer (LDS serves a
     // wave's accesses in order: the reads above come first)
@@ -636,6 +678,10 @@ __device__ inline void st_agent(float* p, float v) {
 }
 __device__ inline float ld_agent(const float* p) {
   return __hip_atomic_load(const_cast<float*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ inline uint64_t ld_agent64(const float* p) {   // two adjacent floats, 8-byte aligned
+  return __hip_atomic_load(reinterpret_cast<uint64_t*>(const_cast<float*>(p)), __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // one radix-2 stage of the unnormalized Walsh-Hadamard transform of the 4
@@ -706,7 +752,7 @@ __device__ void tail_split(const DecodeArgs& a, Shared<PL>& sm, int b, int kvh) 
   }
   __syncthreads();
   const int h = tid >> 7, c = tid & 127;
-  {
+  if (tid < 4 * kD) {
     float o = 0.0f;
     for (int t = 0; t < nt; ++t) o += ts.lg[h][t] * hf(vt[t * kD + c]);
     if (BASE == 1) {                       // into the rotated domain: H (sign . o) / 128
@@ -718,10 +764,12 @@ __device__ void tail_split(const DecodeArgs& a, Shared<PL>& sm, int b, int kvh) 
   __syncthreads();
   if (BASE == 1)
     for (int hs = 1; hs < kD; hs <<= 1) fwht_stage(ts.o, hs);
-  sm.tfin.o[h][c] = ts.o[h][c] * (BASE == 1 ? 1.0f / 128.0f : 1.0f);
-  if (c == 0) {
-    sm.tfin.m[h] = ts.mx[h];
-    sm.tfin.l[h] = ts.sum[h];
+  if (tid < 4 * kD) {
+    sm.tfin.o[h][c] = ts.o[h][c] * (BASE == 1 ? 1.0f / 128.0f : 1.0f);
+    if (c == 0) {
+      sm.tfin.m[h] = ts.mx[h];
+      sm.tfin.l[h] = ts.sum[h];
+    }
   }
 }
 
@@ -733,65 +781,55 @@ __device__ void merge_splits(const DecodeArgs& a, Shared<PL>& sm, int b, int kvh
   const int tid = threadIdx.x, h = tid >> 7, c = tid & 127;
   const int ns = a.nsplit;
   const float* unit = a.ws + (int64_t(b) * a.g.n_kv_heads + kvh) * ns * 4 * kPartial;
-  float* mm = reinterpret_cast<float*>(&sm.stage[0][0]);   // [ns][4] maxima
-  float* ll = mm + kMaxSplits * 4;                          // [ns][4] sums
-  static_assert(sizeof(sm.stage) >= 2 * kMaxSplits * 4 * sizeof(float), "merge scratch");
-  static_assert(kMaxSplits * 4 <= 2 * kThreads, "two (split, head) pairs per thread");
-  // one round of loads: this thread's (split, head) maxima and sums, and its
-  // channel of the first kBatch partials
+  // every thread reads, for its head, each split's (max, sum) pair and its
+  // channel of the split's output: one round of loads for up to kBatch splits
   constexpr int kBatch = 32;
-  float mv[2], lv[2], x[kBatch];
-#pragma unroll
-  for (int k = 0; k < 2; ++k) {
-    const int i = tid + k * kThreads;
-    mv[k] = i < ns * 4 ? ld_agent(unit + i * kPartial) : 0.0f;
-    lv[k] = i < ns * 4 ? ld_agent(unit + i * kPartial + 1) : 0.0f;
-  }
-  const float* op = unit + h * kPartial + 4 + c;
-#pragma unroll
-  for (int k = 0; k < kBatch; ++k) x[k] = k < ns ? ld_agent(op + k * 4 * kPartial) : 0.0f;
-#pragma unroll
-  for (int k = 0; k < 2; ++k) {
-    const int i = tid + k * kThreads;
-    if (i < ns * 4) {
-      mm[i] = mv[k];
-      ll[i] = lv[k];
-    }
-  }
-  __syncthreads();
-  float M = -INFINITY;
-  for (int s = 0; s < ns; ++s) M = fmaxf(M, mm[s * 4 + h]);
-  float Lsum = 0.0f, o = 0.0f;
-  for (int s0 = 0; s0 < ns; s0 += kBatch) {
-    if (s0 > 0) {
-#pragma unroll
-      for (int k = 0; k < kBatch; ++k) x[k] = s0 + k < ns ? ld_agent(op + (s0 + k) * 4 * kPartial) : 0.0f;
-    }
+  const bool mine = tid < 4 * kD;            // one thread per (head, channel)
+  float M = -INFINITY, Lsum = 0.0f, o = 0.0f;
+  for (int s0 = 0; mine && s0 < ns; s0 += kBatch) {
+    float mv[kBatch], lv[kBatch], x[kBatch];
 #pragma unroll
     for (int k = 0; k < kBatch; ++k) {
+      mv[k] = -INFINITY;
+      lv[k] = x[k] = 0.0f;
       if (s0 + k < ns) {
-        const float m = mm[(s0 + k) * 4 + h];
-        const float sc = m == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(m - M);
-        Lsum += ll[(s0 + k) * 4 + h] * sc;
-        o += x[k] * sc;
+        const float* ph = unit + ((s0 + k) * 4 + h) * kPartial;
+        const uint64_t ml = ld_agent64(ph);
+        mv[k] = __uint_as_float(uint32_t(ml));
+        lv[k] = __uint_as_float(uint32_t(ml >> 32));
+        x[k] = ld_agent(ph + 4 + c);
       }
     }
+    float Mn = M;
+#pragma unroll
+    for (int k = 0; k < kBatch; ++k) Mn = fmaxf(Mn, mv[k]);
+    const float keep = M == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(M - Mn);
+    Lsum *= keep;
+    o *= keep;
+#pragma unroll
+    for (int k = 0; k < kBatch; ++k) {
+      const float sc = mv[k] == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(mv[k] - Mn);
+      Lsum += lv[k] * sc;
+      o += x[k] * sc;
+    }
+    M = Mn;
   }
-  o /= Lsum;
+  o = mine ? o / Lsum : 0.0f;
   if (BASE == 1) {
     __syncthreads();
-    sm.qf[h][c] = o;
+    if (mine) sm.qf[h][c] = o;
     __syncthreads();
     for (int hs = 1; hs < kD; hs <<= 1) fwht_stage(sm.qf, hs);
     const uint32_t* sw = a.g.signs + (int64_t(a.layer) * a.g.n_kv_heads + kvh) * 4;
-    o = ((sw[c >> 5] >> (c & 31)) & 1u) ? -sm.qf[h][c] : sm.qf[h][c];
+    if (mine) o = ((sw[c >> 5] >> (c & 31)) & 1u) ? -sm.qf[h][c] : sm.qf[h][c];
   }
-  a.out[((int64_t(b) * a.g.n_kv_heads + kvh) * 4 + h) * kD + c] = o;
+  if (mine) a.out[((int64_t(b) * a.g.n_kv_heads + kvh) * 4 + h) * kD + c] = o;
 }
 
 template <int BASE, int LH, int LL, int G>
-__global__ __launch_bounds__(kThreads) void decode_kernel(DecodeArgs a) {
+__global__ __launch_bounds__((Plan<BASE, LH, LL, G>::NT)) void decode_kernel(DecodeArgs a) {
   using PL = Plan<BASE, LH, LL, G>;
+  constexpr int NW = PL::NW, NT = PL::NT;
   __shared__ Shared<PL> sm;
   const int split = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
   const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
@@ -802,23 +840,25 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeArgs a) {
   const int nt = nt0 + nt1;
   const int f0 = int(int64_t(split) * nt / a.nsplit), f1 = int(int64_t(split + 1) * nt / a.nsplit);
   const int first = f0 + wave;
-  const int count = first < f1 ? (f1 - first + kDecodeWaves - 1) / kDecodeWaves : 0;
-  const int nhi_all = first < nt0 ? (nt0 - first + kDecodeWaves - 1) / kDecodeWaves : 0;
+  const int count = first < f1 ? (f1 - first + NW - 1) / NW : 0;
+  const int nhi_all = first < nt0 ? (nt0 - first + NW - 1) / NW : 0;
   const int nhi = nhi_all < count ? nhi_all : count;
   const uint8_t* unit = g.pools + unit_offset(g, b, a.layer, kvh);
 
-  // ---- query and decode tables, then the first record in flight
-  const int h = tid >> 7, c = tid & 127;
-  const uint16_t qbits = a.q[((int64_t(b) * g.n_kv_heads * 4) + kvh * 4 + h) * kD + c];
-  constexpr int NTH = (PL::LUTH / 4 + kThreads - 1) / kThreads, NTL = (PL::LUTL / 4 + kThreads - 1) / kThreads;
+  // ---- query and decode tables, then the first record in flight; the query
+  // work takes the first 4 x 128 threads, one per (head, channel)
+  const bool qt = tid < 4 * kD;
+  const int h = qt ? tid >> 7 : 0, c = tid & 127;
+  const uint16_t qbits = qt ? a.q[((int64_t(b) * g.n_kv_heads * 4) + kvh * 4 + h) * kD + c] : uint16_t(0);
+  constexpr int NTH = (PL::LUTH / 4 + NT - 1) / NT, NTL = (PL::LUTL / 4 + NT - 1) / NT;
   uint4 th[NTH], tl[NTL];
   {
     const uint4* sh = reinterpret_cast<const uint4*>(kLutImage<BASE, LH>.w);
     const uint4* sl = reinterpret_cast<const uint4*>(kLutImage<BASE, LL>.w);
 #pragma unroll
-    for (int k = 0; k < NTH; ++k) th[k] = sh[tid + k * kThreads < PL::LUTH / 4 ? tid + k * kThreads : 0];
+    for (int k = 0; k < NTH; ++k) th[k] = sh[tid + k * NT < PL::LUTH / 4 ? tid + k * NT : 0];
 #pragma unroll
-    for (int k = 0; k < NTL; ++k) tl[k] = sl[tid + k * kThreads < PL::LUTL / 4 ? tid + k * kThreads : 0];
+    for (int k = 0; k < NTL; ++k) tl[k] = sl[tid + k * NT < PL::LUTL / 4 ? tid + k * NT : 0];
   }
   // the wave's first record (a wave without records loads tile 0, unused)
   uint4 R[PL::NLD];
@@ -827,12 +867,12 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeArgs a) {
     uint4* d = reinterpret_cast<uint4*>(sm.lut);
 #pragma unroll
     for (int k = 0; k < NTH; ++k)
-      if (tid + k * kThreads < PL::LUTH / 4) d[tid + k * kThreads] = th[k];
+      if (tid + k * NT < PL::LUTH / 4) d[tid + k * NT] = th[k];
 #pragma unroll
     for (int k = 0; k < NTL; ++k)
-      if (tid + k * kThreads < PL::LUTL / 4) d[PL::LUTH / 4 + tid + k * kThreads] = tl[k];
+      if (tid + k * NT < PL::LUTL / 4) d[PL::LUTH / 4 + tid + k * NT] = tl[k];
   }
-  {
+  if (qt) {
     const float x = hf(qbits);
     sm.qorig[h][c] = x;
     float xr = x;
@@ -850,8 +890,9 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeArgs a) {
   __syncthreads();
   if (BASE == 1)                            // rotate: H (sign . q)
     for (int hs = 1; hs < kD; hs <<= 1) fwht_stage(sm.qf, hs);
-  {
-    // per head: sums of the query over aligned runs of SEG channels
+  if (qt) {
+    // per head: sums of the query over aligned runs of SEG channels (the
+    // query threads are whole waves)
     constexpr int SEG = (BASE == 0 && G < 64) ? G : 64;
     float x = sm.qf[h][c];
 #pragma unroll
@@ -882,14 +923,14 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeArgs a) {
   }
 
   // ---- workgroup partial: merge of the waves' (and the tail's) states
-  {
+  if (qt) {
     float M = -INFINITY;
 #pragma unroll
-    for (int w = 0; w < kDecodeWaves; ++w) M = fmaxf(M, wave_fin(sm, w)->m[h]);
+    for (int w = 0; w < NW; ++w) M = fmaxf(M, wave_fin(sm, w)->m[h]);
     if (tail) M = fmaxf(M, sm.tfin.m[h]);
     float Lsum = 0.0f, o = 0.0f;
 #pragma unroll
-    for (int w = 0; w < kDecodeWaves; ++w) {
+    for (int w = 0; w < NW; ++w) {
       const Fin* f = wave_fin(sm, w);
       const float sc = f->m[h] == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(f->m[h] - M);
       Lsum += f->l[h] * sc;
@@ -923,9 +964,12 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(DecodeArgs a) {
 }
 
 template <int BASE, int LH, int LL, int G>
+int waves_of() { return Plan<BASE, LH, LL, G>::NW; }
+
+template <int BASE, int LH, int LL, int G>
 int occupancy() {
   int n = 0;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, decode_kernel<BASE, LH, LL, G>, kThreads, 0) != hipSuccess)
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, decode_kernel<BASE, LH, LL, G>, Plan<BASE, LH, LL, G>::NT, 0) != hipSuccess)
     return 1;
   return n > 0 ? n : 1;
 }
@@ -934,23 +978,23 @@ template <int BASE, int LH, int LL>
 int launch_dec(const DecodeArgs& a, hipStream_t st) {
   dim3 grid(a.nsplit, a.g.n_kv_heads, a.g.batch);
   if constexpr (BASE == 1) {
-    hipLaunchKernelGGL((decode_kernel<BASE, LH, LL, 128>), grid, dim3(kThreads), 0, st, a);
+    hipLaunchKernelGGL((decode_kernel<BASE, LH, LL, 128>), grid, dim3(Plan<BASE, LH, LL, 128>::NT), 0, st, a);
   } else {
-    if (a.g.G == 128) hipLaunchKernelGGL((decode_kernel<BASE, LH, LL, 128>), grid, dim3(kThreads), 0, st, a);
-    else if (a.g.G == 64) hipLaunchKernelGGL((decode_kernel<BASE, LH, LL, 64>), grid, dim3(kThreads), 0, st, a);
-    else hipLaunchKernelGGL((decode_kernel<BASE, LH, LL, 32>), grid, dim3(kThreads), 0, st, a);
+    if (a.g.G == 128) hipLaunchKernelGGL((decode_kernel<BASE, LH, LL, 128>), grid, dim3(Plan<BASE, LH, LL, 128>::NT), 0, st, a);
+    else if (a.g.G == 64) hipLaunchKernelGGL((decode_kernel<BASE, LH, LL, 64>), grid, dim3(Plan<BASE, LH, LL, 64>::NT), 0, st, a);
+    else hipLaunchKernelGGL((decode_kernel<BASE, LH, LL, 32>), grid, dim3(Plan<BASE, LH, LL, 32>::NT), 0, st, a);
   }
   return hipGetLastError() == hipSuccess ? 0 : -5;
 }
 
 template <int BASE, int LH, int LL>
-int occ_dec(int G) {
+int occ_dec(int G, bool waves) {
   if constexpr (BASE == 1) {
-    return occupancy<BASE, LH, LL, 128>();
+    return waves ? waves_of<BASE, LH, LL, 128>() : occupancy<BASE, LH, LL, 128>();
   } else {
-    if (G == 128) return occupancy<BASE, LH, LL, 128>();
-    if (G == 64) return occupancy<BASE, LH, LL, 64>();
-    return occupancy<BASE, LH, LL, 32>();
+    if (G == 128) return waves ? waves_of<BASE, LH, LL, 128>() : occupancy<BASE, LH, LL, 128>();
+    if (G == 64) return waves ? waves_of<BASE, LH, LL, 64>() : occupancy<BASE, LH, LL, 64>();
+    return waves ? waves_of<BASE, LH, LL, 32>() : occupancy<BASE, LH, LL, 32>();
   }
 }
 
@@ -968,15 +1012,18 @@ int launch_decode(const DecodeArgs& a, hipStream_t s) {
   return -2;
 }
 
-int decode_blocks_per_cu(int base, int LH, int LL, int G) {
-  if (base == 0 && LH == 6 && LL == 5) return occ_dec<0, 6, 5>(G);
-  if (base == 0 && LH == 5 && LL == 4) return occ_dec<0, 5, 4>(G);
-  if (base == 0 && LH == 6 && LL == 4) return occ_dec<0, 6, 4>(G);
-  if (base == 0 && LH == 4 && LL == 3) return occ_dec<0, 4, 3>(G);
-  if (base == 0 && LH == 5 && LL == 3) return occ_dec<0, 5, 3>(G);
-  if (base == 0 && LH == 6 && LL == 3) return occ_dec<0, 6, 3>(G);
-  if (base == 1 && LH == 4 && LL == 3) return occ_dec<1, 4, 3>(G);
-  return 1;
+static int decode_query(int base, int LH, int LL, int G, bool waves) {
+  if (base == 0 && LH == 6 && LL == 5) return occ_dec<0, 6, 5>(G, waves);
+  if (base == 0 && LH == 5 && LL == 4) return occ_dec<0, 5, 4>(G, waves);
+  if (base == 0 && LH == 6 && LL == 4) return occ_dec<0, 6, 4>(G, waves);
+  if (base == 0 && LH == 4 && LL == 3) return occ_dec<0, 4, 3>(G, waves);
+  if (base == 0 && LH == 5 && LL == 3) return occ_dec<0, 5, 3>(G, waves);
+  if (base == 0 && LH == 6 && LL == 3) return occ_dec<0, 6, 3>(G, waves);
+  if (base == 1 && LH == 4 && LL == 3) return occ_dec<1, 4, 3>(G, waves);
+  return waves ? 8 : 1;
 }
+
+int decode_blocks_per_cu(int base, int LH, int LL, int G) { return decode_query(base, LH, LL, G, false); }
+int decode_waves(int base, int LH, int LL, int G) { return decode_query(base, LH, LL, G, true); }
 
 }  // namespace semkv

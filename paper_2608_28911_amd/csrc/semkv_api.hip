@@ -115,7 +115,8 @@ int plan(const semkv_cache* c, int n_tail) {
   if (nt == 0) return n_tail > 0 ? 1 : 0;
   const int64_t units = int64_t(c->cfg.batch) * c->cfg.n_kv_heads;
   int64_t ns = decode_slots(c->cfg) / units;
-  if (ns > nt / kDecodeWaves) ns = nt / kDecodeWaves;
+  const int nw = decode_waves(c->cfg.base, c->cfg.L_hi, c->cfg.L_lo, c->cfg.group);
+  if (ns > nt / nw) ns = nt / nw;
   if (ns > kMaxSplits) ns = kMaxSplits;
   if (ns < 1) ns = 1;
   return int(ns);

@@ -76,14 +76,15 @@ struct DecodeArgs {
 
 constexpr int kPartial = 132;  // m, l, 2 pad, o[128]
 constexpr int kMaxSplits = 256;   // splits per (sequence, kv head)
-constexpr int kDecodeWaves = 8;   // waves per decode workgroup
 
 int launch_rank(const RankArgs& a, int batch, hipStream_t s);
 int launch_quantize(const QuantArgs& a, hipStream_t s);
 int launch_append(const AppendArgs& a, hipStream_t s);
 int launch_close(const CloseArgs& a, hipStream_t s);
 int launch_decode(const DecodeArgs& a, hipStream_t s);
-// decode workgroups one compute unit holds at once for this cache's kernel
+// decode workgroups one compute unit holds at once for this cache's kernel,
+// and the waves of one such workgroup (a wave takes every NW-th tile of a run)
 int decode_blocks_per_cu(int base, int L_hi, int L_lo, int G);
+int decode_waves(int base, int L_hi, int L_lo, int G);
 
 }  // namespace semkv
