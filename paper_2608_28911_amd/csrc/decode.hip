@@ -671,18 +671,13 @@ __device__ void wave_finish(Shared<PL>& sm, WaveState<PL::NGV>& st) {
 }
 
 // Partials cross workgroups (and XCDs, whose L2 caches are not coherent with
-// each other): they are written and read with agent-scope atomic accesses,
-// which go to the coherent level without any cache write-back or invalidate.
+// each other): they are written with agent-scope atomic stores and read with
+// the same coherent cache policy (sc1), so neither side needs a cache
+// write-back or invalidate.
 __device__ inline void st_agent(float* p, float v) {
   __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-__device__ inline float ld_agent(const float* p) {
-  return __hip_atomic_load(const_cast<float*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ inline uint64_t ld_agent64(const float* p) {   // two adjacent floats, 8-byte aligned
-  return __hip_atomic_load(reinterpret_cast<uint64_t*>(const_cast<float*>(p)), __ATOMIC_RELAXED,
-                           __HIP_MEMORY_SCOPE_AGENT);
-}
+
 
 // one radix-2 stage of the unnormalized Walsh-Hadamard transform of the 4
 // rows of x (128 entries each), by the first 256 threads
@@ -778,26 +773,35 @@ __device__ void tail_split(const DecodeArgs& a, Shared<PL>& sm, int b, int kvh) 
 // rotation o = sign . H o_rot.
 template <int BASE, class PL>
 __device__ void merge_splits(const DecodeArgs& a, Shared<PL>& sm, int b, int kvh) {
-  const int tid = threadIdx.x, h = tid >> 7, c = tid & 127;
+  const int tid = threadIdx.x;
   const int ns = a.nsplit;
   const float* unit = a.ws + (int64_t(b) * a.g.n_kv_heads + kvh) * ns * 4 * kPartial;
-  // every thread reads, for its head, each split's (max, sum) pair and its
-  // channel of the split's output: one round of loads for up to kBatch splits
-  constexpr int kBatch = 32;
-  const bool mine = tid < 4 * kD;            // one thread per (head, channel)
-  float M = -INFINITY, Lsum = 0.0f, o = 0.0f;
-  for (int s0 = 0; mine && s0 < ns; s0 += kBatch) {
-    float mv[kBatch], lv[kBatch], x[kBatch];
+  // thread (head h, quarter q, channel quad cq) takes the splits s = q, q+4,
+  // ... with 16-byte loads at the coherent level (cache policy sc1, as the
+  // agent-scope loads), then the four quarters merge in LDS
+  const bool mine = tid < 4 * kD;
+  const int h = (tid >> 7) & 3, q = (tid >> 5) & 3, cq = tid & 31;
+  const __amdgpu_buffer_rsrc_t rs =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(unit), 0, ns * 4 * kPartial * 4, kBufferWord3);
+  constexpr int kCoherent = 16;              // sc1
+  constexpr int kBatch = 8;
+  float M = -INFINITY, Lsum = 0.0f;
+  float4v o = float4v{0, 0, 0, 0};
+  for (int s0 = q; mine && s0 < ns; s0 += 4 * kBatch) {
+    float mv[kBatch], lv[kBatch];
+    float4v x[kBatch];
 #pragma unroll
     for (int k = 0; k < kBatch; ++k) {
+      const int sp = s0 + 4 * k;
       mv[k] = -INFINITY;
-      lv[k] = x[k] = 0.0f;
-      if (s0 + k < ns) {
-        const float* ph = unit + ((s0 + k) * 4 + h) * kPartial;
-        const uint64_t ml = ld_agent64(ph);
-        mv[k] = __uint_as_float(uint32_t(ml));
-        lv[k] = __uint_as_float(uint32_t(ml >> 32));
-        x[k] = ld_agent(ph + 4 + c);
+      lv[k] = 0.0f;
+      x[k] = float4v{0, 0, 0, 0};
+      if (sp < ns) {
+        const int off = (sp * 4 + h) * kPartial * 4;
+        const auto ml = __builtin_amdgcn_raw_buffer_load_b64(rs, off, 0, kCoherent);
+        mv[k] = __uint_as_float(ml[0]);
+        lv[k] = __uint_as_float(ml[1]);
+        x[k] = __builtin_bit_cast(float4v, __builtin_amdgcn_raw_buffer_load_b128(rs, off + 16 + 16 * cq, 0, kCoherent));
       }
     }
     float Mn = M;
@@ -814,16 +818,41 @@ __device__ void merge_splits(const DecodeArgs& a, Shared<PL>& sm, int b, int kvh
     }
     M = Mn;
   }
-  o = mine ? o / Lsum : 0.0f;
+  struct Quarters { float m[4][4], l[4][4]; float4v o[4][4][32]; };
+  static_assert(sizeof(Quarters) <= sizeof(sm.stage), "merge scratch");
+  Quarters& qs = *reinterpret_cast<Quarters*>(&sm.stage[0][0]);
+  if (mine) {
+    if (cq == 0) {
+      qs.m[h][q] = M;
+      qs.l[h][q] = Lsum;
+    }
+    qs.o[h][q][cq] = o;
+  }
+  __syncthreads();
+  const int hc = tid >> 7, c = tid & 127;
+  float r = 0.0f;
+  if (mine) {
+    float Mx = -INFINITY;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) Mx = fmaxf(Mx, qs.m[hc][k]);
+    float L = 0.0f, O = 0.0f;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const float sc = qs.m[hc][k] == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(qs.m[hc][k] - Mx);
+      L += qs.l[hc][k] * sc;
+      O += qs.o[hc][k][c >> 2][c & 3] * sc;
+    }
+    r = O / L;
+  }
   if (BASE == 1) {
     __syncthreads();
-    if (mine) sm.qf[h][c] = o;
+    if (mine) sm.qf[hc][c] = r;
     __syncthreads();
     for (int hs = 1; hs < kD; hs <<= 1) fwht_stage(sm.qf, hs);
     const uint32_t* sw = a.g.signs + (int64_t(a.layer) * a.g.n_kv_heads + kvh) * 4;
-    if (mine) o = ((sw[c >> 5] >> (c & 31)) & 1u) ? -sm.qf[h][c] : sm.qf[h][c];
+    if (mine) r = ((sw[c >> 5] >> (c & 31)) & 1u) ? -sm.qf[hc][c] : sm.qf[hc][c];
   }
-  if (mine) a.out[((int64_t(b) * a.g.n_kv_heads + kvh) * 4 + h) * kD + c] = o;
+  if (mine) a.out[((int64_t(b) * a.g.n_kv_heads + kvh) * 4 + hc) * kD + c] = r;
 }
 
 template <int BASE, int LH, int LL, int G>
