@@ -38,8 +38,12 @@ __device__ inline float sqrt_rn(float a) {
   return r;
 }
 
-__device__ inline void load_quarter(const uint16_t* src, float x[32]) {
+// A row quarter (32 fp16 values) as fp32, and whether any is inf or NaN (the
+// largest magnitude bit pattern, by a packed 16-bit max, reaches 0x7C00).
+__device__ inline void load_quarter(const uint16_t* src, float x[32], bool& nonfinite) {
+  typedef uint16_t u16x2 __attribute__((ext_vector_type(2)));
   const uint4* p = reinterpret_cast<const uint4*>(src);
+  u16x2 big = u16x2{0, 0};
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
     uint4 w = p[k];
@@ -48,22 +52,22 @@ __device__ inline void load_quarter(const uint16_t* src, float x[32]) {
     for (int e = 0; e < 4; ++e) {
       x[8 * k + 2 * e] = h2f(uint16_t(d[e] & 0xFFFFu));
       x[8 * k + 2 * e + 1] = h2f(uint16_t(d[e] >> 16));
+      big = __builtin_elementwise_max(big, __builtin_bit_cast(u16x2, d[e] & 0x7FFF7FFFu));
     }
   }
+  nonfinite |= big.x >= 0x7C00u || big.y >= 0x7C00u;
 }
 
 // Asymmetric affine quantizer (Sec. 4.1) of one row quarter; the min/max of a
 // group of G channels is combined over the G/32 lanes holding it.  Returns
 // {scale, zero} as fp16 bits (low half = scale).
 template <int L>
-__device__ uint32_t affine_quarter(const float x[32], int G, uint8_t* code, bool& bad) {
+__device__ uint32_t affine_quarter(const float x[32], int G, uint32_t code[8]) {
   float mn = x[0], mx = x[0];
-  bool nf = false;
 #pragma unroll
   for (int i = 0; i < 32; ++i) {
     mn = fminf(mn, x[i]);
     mx = fmaxf(mx, x[i]);
-    nf |= !isfinite(x[i]);
   }
   if (G >= 64) {
     mn = fminf(mn, __shfl_xor(mn, 1));
@@ -77,13 +81,18 @@ __device__ uint32_t affine_quarter(const float x[32], int G, uint8_t* code, bool
   uint16_t s16 = f2h(__fdiv_rn(mx - mn, float(L - 1)));
   float sf = h2f(s16);
   float inv = sf == 0.0f ? 0.0f : __fdiv_rn(1.0f, sf);
+  // rint, clamp to [0, L-1] (NaN -> 0), then one convert-and-insert per code
 #pragma unroll
-  for (int i = 0; i < 32; ++i) {
-    float c = rintf((x[i] - zero) * inv);
-    c = fminf(fmaxf(c, 0.0f), float(L - 1));
-    code[i] = uint8_t(c);
+  for (int k = 0; k < 8; ++k) {
+    uint32_t w = 0;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      float c = rintf((x[4 * k + e] - zero) * inv);
+      c = fminf(fmaxf(c, 0.0f), float(L - 1));
+      w = __builtin_amdgcn_cvt_pk_u8_f32(c, e, w);
+    }
+    code[k] = w;
   }
-  bad |= nf;
   return uint32_t(s16) | (uint32_t(f2h(zero)) << 16);
 }
 
@@ -92,15 +101,13 @@ __device__ uint32_t affine_quarter(const float x[32], int G, uint8_t* code, bool
 // tree, one fp16 scalar, and Lloyd-Max threshold codes.  Returns rho bits.
 template <int L>
 __device__ uint16_t tq_quarter(const float x[32], int q, const uint32_t* sw, const float* tau,
-                               uint8_t* code, bool& bad) {
+                               uint32_t code[8]) {
   float u[32], a[32];
-  bool nf = false;
   uint32_t sbits = sw[q];
 #pragma unroll
   for (int i = 0; i < 32; ++i) {
     u[i] = ((sbits >> i) & 1u) ? -x[i] : x[i];
     a[i] = x[i] * x[i];
-    nf |= !isfinite(x[i]);
   }
 #pragma unroll
   for (int h = 1; h < 32; h <<= 1)
@@ -138,29 +145,33 @@ __device__ uint16_t tq_quarter(const float x[32], int q, const uint32_t* sw, con
 #pragma unroll
   for (int k = 0; k < L - 1; ++k) thr[k] = rf * tau[k];
 #pragma unroll
-  for (int i = 0; i < 32; ++i) {
-    int c = 0;
+  for (int k = 0; k < 8; ++k) {
+    uint32_t w = 0;
 #pragma unroll
-    for (int k = 0; k < L - 1; ++k) c += u[i] > thr[k] ? 1 : 0;
-    code[i] = uint8_t(c);
+    for (int e = 0; e < 4; ++e) {
+      uint32_t c = 0;
+#pragma unroll
+      for (int t = 0; t < L - 1; ++t) c += u[4 * k + e] > thr[t] ? 1u : 0u;
+      w |= c << (8 * e);
+    }
+    code[k] = w;
   }
-  bad |= nf;
   return r16;
 }
 
 // Quantize the quarter row held by this lane and write its metadata.
 template <int BASE, int L>
 __device__ void quantize_quarter(const PoolGeom& g, const float x[32], int q, int layer, int kvh,
-                                 const float* tau, uint8_t* code, uint8_t* meta_dst, int slot,
-                                 bool valid, bool& bad) {
+                                 const float* tau, uint32_t code[8], uint8_t* meta_dst, int slot,
+                                 bool valid) {
   if (BASE == 0) {
-    uint32_t m = affine_quarter<L>(x, g.G, code, bad);
+    uint32_t m = affine_quarter<L>(x, g.G, code);
     int per = g.G / 32;
     if (q % per == 0)
       reinterpret_cast<uint32_t*>(meta_dst)[(q / per) * kSlots + slot] = valid ? m : 0u;
   } else {
     const uint32_t* sw = g.signs + (int64_t(layer) * g.n_kv_heads + kvh) * 4;
-    uint16_t r = tq_quarter<L>(x, q, sw, tau, code, bad);
+    uint16_t r = tq_quarter<L>(x, q, sw, tau, code);
     if (q == 0) reinterpret_cast<uint16_t*>(meta_dst)[slot] = valid ? r : uint16_t(0);
   }
 }
@@ -283,19 +294,19 @@ __device__ void prefill_record(const QuantArgs& a, Lds& s, int pool, int tile, i
   bool bad = false;
   const int64_t base_off = int64_t(l) * a.sL + int64_t(b) * a.sB + int64_t(h) * a.sH + int64_t(tok) * a.sT + 32 * q;
   float x[32];
-  uint8_t code[32];
+  uint32_t code[8];
 #pragma unroll
   for (int kv = 0; kv < 2; ++kv) {
     if (valid) {
-      load_quarter((kv ? a.V : a.K) + base_off, x);
+      load_quarter((kv ? a.V : a.K) + base_off, x, bad);
     } else {
 #pragma unroll
       for (int i = 0; i < 32; ++i) x[i] = 0.0f;
     }
-    quantize_quarter<BASE, L>(g, x, q, l, h, g.tau[pool], code, rec + 2 * tb + kv * g.meta_bytes, r, valid, bad);
-    uint8_t* dst = (kv ? s.cv : s.ck) + r * kPitch + 32 * q;
+    quantize_quarter<BASE, L>(g, x, q, l, h, g.tau[pool], code, rec + 2 * tb + kv * g.meta_bytes, r, valid);
+    uint32_t* dst = reinterpret_cast<uint32_t*>((kv ? s.cv : s.ck) + r * kPitch + 32 * q);
 #pragma unroll
-    for (int i = 0; i < 32; ++i) dst[i] = valid ? code[i] : uint8_t(0);
+    for (int i = 0; i < 8; ++i) dst[i] = valid ? code[i] : 0u;
   }
   if (bad && valid) atomicOr(g.status, 2);
   __syncthreads();
@@ -352,19 +363,19 @@ __device__ void close_record(const CloseArgs& a, Lds& s, const int* row_of, int 
   if (fresh) {
     const uint16_t* src = a.tail + ((((int64_t(b) * g.n_layers + l) * g.n_kv_heads + h) * 2) * kSlots + row) * kD + 32 * q;
     float x[32];
-    uint8_t code[32];
+    uint32_t code[8];
 #pragma unroll
     for (int kv = 0; kv < 2; ++kv) {
       if (valid) {
-        load_quarter(src + kv * kSlots * kD, x);
+        load_quarter(src + kv * kSlots * kD, x, bad);
       } else {
 #pragma unroll
         for (int i = 0; i < 32; ++i) x[i] = 0.0f;
       }
-      quantize_quarter<BASE, L>(g, x, q, l, h, g.tau[pool], code, rec + 2 * tb + kv * g.meta_bytes, r, valid, bad);
-      uint8_t* dst = (kv ? s.cv : s.ck) + r * kPitch + 32 * q;
+      quantize_quarter<BASE, L>(g, x, q, l, h, g.tau[pool], code, rec + 2 * tb + kv * g.meta_bytes, r, valid);
+      uint32_t* dst = reinterpret_cast<uint32_t*>((kv ? s.cv : s.ck) + r * kPitch + 32 * q);
 #pragma unroll
-      for (int i = 0; i < 32; ++i) dst[i] = valid ? code[i] : uint8_t(0);
+      for (int i = 0; i < 8; ++i) dst[i] = valid ? code[i] : 0u;
     }
   }
   if (bad && valid) atomicOr(g.status, 2);
