@@ -178,45 +178,51 @@ __device__ void quantize_quarter(const PoolGeom& g, const float x[32], int q, in
 
 // OR the bits of one segment into an LDS body.  The segment holds symbols
 // p = j, j+4, ... of a line of NV codes: code p*n+i of the line is at
-// codes[(p*n+i)*stride].
-template <int L, int NV, int NL>
-__device__ void pack_segment(const uint8_t* codes, int stride, int line, int j, uint32_t* body) {
+// codes[(p*n+i)*stride].  J is compile-time: the symbols' widths and bit
+// positions are constants, the line's offset is applied by one funnel shift
+// per word.
+template <int L, int NV, int NL, int J>
+__device__ __forceinline__ void pack_segment_j(const uint8_t* codes, int stride, int line, uint32_t* body) {
   constexpr int n = sym_digits(L);
-  constexpr int S = num_syms(L, NV);
   constexpr SegTable<L, NV, NL> t{};
-  uint64_t lo = 0, hi = 0;
+  constexpr int BITS = t.bits[J];
+  constexpr int NWD = (BITS + 31) / 32 + 1;             // words, one spare for the shift
+  uint32_t w[NWD];
+#pragma unroll
+  for (int k = 0; k < NWD; ++k) w[k] = 0u;
   int nb = 0;
 #pragma unroll
-  for (int k = 0; 4 * k < S; ++k) {
-    const int p = j + 4 * k;
-    const int w = pick4(j, t.width[0][k], t.width[1][k], t.width[2][k], t.width[3][k]);
-    const int nd = pick4(j, t.ndig[0][k], t.ndig[1][k], t.ndig[2][k], t.ndig[3][k]);
-    if (w > 0) {
+  for (int k = 0; k < 16; ++k) {
+    const int wd = t.width[J][k], nd = t.ndig[J][k];
+    if (wd > 0) {
+      const int p = J + 4 * k;
       uint32_t v = 0;
 #pragma unroll
       for (int i = n - 1; i >= 0; --i)
         if (i < nd) v = v * L + codes[(n * p + i) * stride];
-      if (nb < 64) {
-        lo |= uint64_t(v) << nb;
-        if (nb + w > 64) hi |= uint64_t(v) >> (64 - nb);
-      } else {
-        hi |= uint64_t(v) << (nb - 64);
-      }
-      nb += w;
+      w[nb >> 5] |= v << (nb & 31);
+      if ((nb & 31) + wd > 32) w[(nb >> 5) + 1] |= v >> (32 - (nb & 31));
+      nb += wd;
     }
   }
-  const int off = pick4(j, t.start[0], t.start[1], t.start[2], t.start[3]) +
-                  line * pick4(j, t.bits[0], t.bits[1], t.bits[2], t.bits[3]);
-  int w0 = off >> 5, sh = off & 31;
-  uint32_t s[4] = {uint32_t(lo), uint32_t(lo >> 32), uint32_t(hi), uint32_t(hi >> 32)};
-  uint32_t o[5];
-  o[0] = s[0] << sh;
+  const int off = t.start[J] + line * BITS;
+  const int w0 = off >> 5, sh = off & 31;
 #pragma unroll
-  for (int k = 1; k < 4; ++k) o[k] = (s[k] << sh) | (sh ? s[k - 1] >> (32 - sh) : 0u);
-  o[4] = sh ? s[3] >> (32 - sh) : 0u;
-#pragma unroll
-  for (int k = 0; k < 5; ++k)
-    if (32 * k < sh + nb && o[k]) atomicOr(&body[w0 + k], o[k]);
+  for (int k = 0; k < NWD; ++k) {
+    const uint32_t lo = k ? w[k - 1] : 0u;
+    const uint32_t o = sh ? __builtin_amdgcn_alignbit(w[k], lo, 32 - sh) : w[k];
+    if (32 * k < sh + BITS && o) atomicOr(&body[w0 + k], o);
+  }
+}
+
+template <int L, int NV, int NL>
+__device__ __forceinline__ void pack_segment(const uint8_t* codes, int stride, int line, int j, uint32_t* body) {
+  switch (j) {                                          // j is the same for a whole wave
+    case 0: pack_segment_j<L, NV, NL, 0>(codes, stride, line, body); break;
+    case 1: pack_segment_j<L, NV, NL, 1>(codes, stride, line, body); break;
+    case 2: pack_segment_j<L, NV, NL, 2>(codes, stride, line, body); break;
+    default: pack_segment_j<L, NV, NL, 3>(codes, stride, line, body); break;
+  }
 }
 
 // Decode one segment of an LDS body back into codes (used to extend a
@@ -249,7 +255,7 @@ __device__ void unpack_segment(const uint32_t* body, int line, int j, uint8_t* c
 }
 
 template <int L>
-__device__ void pack_record(const uint8_t* ck, const uint8_t* cv, uint32_t* bk, uint32_t* bv) {
+__device__ __forceinline__ void pack_record(const uint8_t* ck, const uint8_t* cv, uint32_t* bk, uint32_t* bv) {
   int tid = threadIdx.x;
   pack_segment<L, kD, kSlots>(ck + (tid & 63) * kPitch, 1, tid & 63, tid >> 6, bk);
 #pragma unroll
