@@ -69,10 +69,10 @@ struct Traits {
   // decode table: symbol -> MFMA operand dwords (codes pre-shifted to d << 6).
   // L = 6 splits a symbol into s mod 216 (3 codes) and s div 216 (2 codes),
   // two dwords per entry in both parts.
-  static constexpr int EDW = STRIDE / 2;                     // dwords per table entry
-  static constexpr int NENT = L == 6 ? 216 : ipow(L, n);
-  static constexpr int LUTDW = L == 6 ? 216 * 2 + 36 * 2 : NENT * EDW;
-  static constexpr int LUTSTRIDE = (LUTDW + 63) / 64 * 64 + 16;   // replicas start 16 banks apart
+  static constexpr int EDW = STRIDE / 2;                     // operand dwords per symbol
+  static constexpr int TED = L == 6 ? 2 : EDW;               // dwords per table entry
+  static constexpr int NENT = L == 6 ? 216 + 36 : ipow(L, n);   // entries (L = 6: both parts)
+  static constexpr int LUTDW = NENT * TED;                   // dwords of one copy
   // largest query channel an A-operand slot addresses (past 127: a zero pad)
   static constexpr int MAXCH = n * (3 + 4 * (SPC * NCK - 1)) + n - 1;
   static_assert(MAXCH < kQPad, "query padding");
@@ -166,44 +166,141 @@ __host__ __device__ constexpr uint32_t lut_entry(int e) {
   return w;
 }
 
-// The table with its 4 replicas (one per lane group), as the LDS copy holds it.
+// One copy of the table; the workgroup spreads it into interleaved replicas
+// in LDS (entry e of replica r at entry slot e * R + r): the lanes of a wave
+// that LDS serves together read R different banks whatever entries they
+// look up, where a single copy costs ~2.4x in bank conflicts (measured).
 template <int BASE, int L>
 struct LutImage {
-  alignas(16) uint32_t w[4 * Traits<BASE, L>::LUTSTRIDE];
+  alignas(16) uint32_t w[Traits<BASE, L>::LUTDW];
   constexpr LutImage() : w{} {
-    for (int rep = 0; rep < 4; ++rep)
-      for (int e = 0; e < Traits<BASE, L>::LUTDW; ++e) w[rep * Traits<BASE, L>::LUTSTRIDE + e] = lut_entry<BASE, L>(e);
+    for (int e = 0; e < Traits<BASE, L>::LUTDW; ++e) w[e] = lut_entry<BASE, L>(e);
   }
 };
 
 template <int BASE, int L>
 __device__ const LutImage<BASE, L> kLutImage = LutImage<BASE, L>();
 
-template <int BASE, int L, int K, int NW, int NS>
-__device__ inline uint32_t seg_symbol(const uint32_t (&seg)[NW], const uint32_t (&mask)[NS]) {
+// 16-byte piece q of the replicated LDS table (R >= 2: a piece lies in one
+// entry, repeated when entries are 8 bytes)
+template <int BASE, int L, int R>
+__device__ inline uint4 lut_chunk(int q) {
   using Tr = Traits<BASE, L>;
-  if constexpr (K < NS) return field<K * Tr::W, Tr::W, NW>(seg) & mask[K];
-  else return 0u;
+  static_assert(R >= 2 && (R & (R - 1)) == 0, "replicas");
+  if constexpr (Tr::TED == 4) {
+    return reinterpret_cast<const uint4*>(kLutImage<BASE, L>.w)[q / R];
+  } else {
+    const uint2 v = reinterpret_cast<const uint2*>(kLutImage<BASE, L>.w)[(2 * q) / R];
+    return make_uint4(v.x, v.y, v.x, v.y);
+  }
+}
+
+// Bits [OFF, OFF+W) of a normalized segment moved to bit S; the bits around
+// them are junk (the caller masks them off).
+template <int OFF, int W, int S, int NW>
+__device__ inline uint32_t field_at(const uint32_t (&seg)[NW]) {
+  constexpr int w = OFF / 32, sh = OFF % 32;
+  if constexpr (sh + W <= 32) {
+    if constexpr (sh >= S) return sh == S ? seg[w] : seg[w] >> (sh - S);
+    else return seg[w] << (S - sh);
+  } else {
+    static_assert(sh >= S, "field position");
+    return __builtin_amdgcn_alignbit(seg[w + 1], seg[w], sh - S);
+  }
+}
+
+// (a << s) | c and (a & b) | c as single instructions (the compiler turns the
+// OR of disjoint bits into an add and re-associates the table's base address
+// into it, which costs an instruction per symbol)
+__device__ inline uint32_t lshl_or(uint32_t a, int s, uint32_t c) {
+  uint32_t r;
+  __asm__("v_lshl_or_b32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "s"(s), "v"(c));
+  return r;
+}
+__device__ inline uint32_t and_or(uint32_t a, uint32_t b, uint32_t c) {
+  uint32_t r;
+  __asm__("v_and_or_b32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+  return r;
+}
+
+// (symbol K of a segment) << S | lbase; a symbol past the line's last is 0.
+// FULL has bit K set when symbol K has the full width in every segment (its
+// lane mask is then a constant).
+template <int BASE, int L, int S, uint32_t FULL, int K, int NW, int NS>
+__device__ inline uint32_t sym_addr(const uint32_t (&seg)[NW], const uint32_t (&maskS)[NS], uint32_t lbase) {
+  using Tr = Traits<BASE, L>;
+  if constexpr (K >= NS) {
+    return lbase;
+  } else {
+    constexpr int OFF = K * Tr::W, sh = OFF % 32;
+    if constexpr (((FULL >> K) & 1u) && sh + Tr::W <= 32)
+      return lshl_or((seg[OFF / 32] >> sh) & ((1u << Tr::W) - 1u), S, lbase);
+    else
+      return and_or(field_at<OFF, Tr::W, S, NW>(seg), maskS[K], lbase);
+  }
+}
+
+// bit K set when symbol K of a line of NVALS codes has the full width in all
+// four segments
+template <int L, int NVALS, int NLINES>
+__host__ __device__ constexpr uint32_t full_symbols() {
+  constexpr SegTable<L, NVALS, NLINES> t{};
+  uint32_t f = 0;
+  for (int k = 0; k < 16; ++k) {
+    bool all = true;
+    for (int j = 0; j < 4; ++j) all = all && t.width[j][k] == width_of(L, sym_digits(L));
+    if (all) f |= 1u << k;
+  }
+  return f;
+}
+
+// A lane's view of its pool's LDS tables: entry e of its replica is at byte
+// (e << S) + lbase of t; for L = 6 the s div 216 part starts at hbase.
+struct LutRef {
+  const uint8_t* t;
+  uint32_t lbase, hbase;
+};
+
+__host__ __device__ constexpr int ilog2(int x) { return x <= 1 ? 0 : 1 + ilog2(x / 2); }
+
+// floor(v / 216) for v < 6^5 as the high word of x * M with x = (v << S) + b,
+// b < 2^S a multiple of 8 (the lane's replica offset): one multiplier found by
+// search for S = 7; otherwise b must be 0 and M = ceil(2^(32-S) / 216)
+__host__ __device__ constexpr uint32_t magic216(int S, bool with_base) {
+  return with_base ? (S == 7 ? 155345u : 0u) : uint32_t(((uint64_t(1) << (32 - S)) + 215) / 216);
+}
+__host__ __device__ constexpr bool magic216_exact(int S, bool with_base) {
+  const uint64_t M = magic216(S, with_base);
+  if (M == 0 || M >= (1u << 24) || (7775u << S) + (1u << S) >= (1u << 24)) return false;
+  const uint64_t bmax = with_base ? (1u << S) - 8 : 0;     // x * M is monotonic in b
+  for (uint64_t v = 0; v < 7776; ++v)
+    if (((v << S) * M) >> 32 != v / 216 || (((v << S) + bmax) * M) >> 32 != v / 216) return false;
+  return true;
 }
 
 // MFMA operand of chunk C of a segment (symbols SPC*C ..), read from the tables
-template <int BASE, int L, int C, int NW, int NS>
-__device__ inline half8 chunk_operand(const uint32_t (&seg)[NW], const uint32_t (&mask)[NS], const uint32_t* lut) {
+template <int BASE, int L, int S, uint32_t FULL, int C, int NW, int NS>
+__device__ inline half8 chunk_operand(const uint32_t (&seg)[NW], const uint32_t (&maskS)[NS], const LutRef& lr) {
   using Tr = Traits<BASE, L>;
   uint4v r;
   if constexpr (L == 6) {
-    const uint32_t v = seg_symbol<BASE, L, C, NW, NS>(seg, mask);
-    const uint32_t hi = mulhi24(v << 8, magic(6, 3));      // v div 216
-    const uint32_t lo = mad_i24(hi, -216, v);               // v mod 216
-    const uint2 a = *reinterpret_cast<const uint2*>(lut + 2 * lo);
-    const uint2 b = *reinterpret_cast<const uint2*>(lut + 432 + 2 * hi);
+    constexpr bool WB = magic216_exact(S, true);
+    static_assert(WB || magic216_exact(S, false), "digit split");
+    uint32_t x;                                                          // (v << S) + lbase
+    if constexpr (WB) x = sym_addr<BASE, L, S, FULL, C, NW, NS>(seg, maskS, lr.lbase);
+    else x = sym_addr<BASE, L, S, FULL, C, NW, NS>(seg, maskS, 0u);
+    const uint32_t hi = mulhi24(x, magic216(S, WB));                     // v div 216
+    if constexpr (!WB) x = and_or(x, 0xFFFFFFFFu, lr.lbase);
+    const uint32_t lo = mad_i24(hi, -(216 << S), x);                     // ((v mod 216) << S) + lbase
+    const uint2 a = *reinterpret_cast<const uint2*>(lr.t + lo);
+    const uint2 b = *reinterpret_cast<const uint2*>(lr.t + ((hi << S) + lr.hbase));
     r = uint4v{a.x, a.y, b.x, b.y};
   } else if constexpr (Tr::SPC == 2) {
-    const uint2 a = *reinterpret_cast<const uint2*>(lut + 2 * seg_symbol<BASE, L, 2 * C, NW, NS>(seg, mask));
-    const uint2 b = *reinterpret_cast<const uint2*>(lut + 2 * seg_symbol<BASE, L, 2 * C + 1, NW, NS>(seg, mask));
+    const uint2 a = *reinterpret_cast<const uint2*>(lr.t + sym_addr<BASE, L, S, FULL, 2 * C, NW, NS>(seg, maskS, lr.lbase));
+    const uint2 b = *reinterpret_cast<const uint2*>(lr.t + sym_addr<BASE, L, S, FULL, 2 * C + 1, NW, NS>(seg, maskS, lr.lbase));
     r = uint4v{a.x, a.y, b.x, b.y};
   } else {
-    const uint4 a = *reinterpret_cast<const uint4*>(lut + 4 * seg_symbol<BASE, L, C, NW, NS>(seg, mask));
+    const uint4 a = *reinterpret_cast<const uint4*>(lr.t + sym_addr<BASE, L, S, FULL, C, NW, NS>(seg, maskS, lr.lbase));
     r = uint4v{a.x, a.y, a.z, a.w};
   }
   return __builtin_bit_cast(half8, r);
@@ -211,11 +308,11 @@ __device__ inline half8 chunk_operand(const uint32_t (&seg)[NW], const uint32_t 
 
 // MFMA operands of all NC chunks of a segment: every table read is issued
 // before the first product needs one (LDS returns them in order)
-template <int BASE, int L, int NW, int NS, int NC>
-__device__ inline void chunk_operands(const uint32_t (&seg)[NW], const uint32_t (&mask)[NS], const uint32_t* lut,
+template <int BASE, int L, int S, uint32_t FULL, int NW, int NS, int NC>
+__device__ inline void chunk_operands(const uint32_t (&seg)[NW], const uint32_t (&maskS)[NS], const LutRef& lr,
                                       half8 (&A)[NC]) {
   static_assert(NC <= 11, "chunks");
-#define SEMKV_O(C) if constexpr (C < NC) A[C] = chunk_operand<BASE, L, C, NW, NS>(seg, mask, lut);
+#define SEMKV_O(C) if constexpr (C < NC) A[C] = chunk_operand<BASE, L, S, FULL, C, NW, NS>(seg, maskS, lr);
   SEMKV_O(0) SEMKV_O(1) SEMKV_O(2) SEMKV_O(3) SEMKV_O(4) SEMKV_O(5)
   SEMKV_O(6) SEMKV_O(7) SEMKV_O(8) SEMKV_O(9) SEMKV_O(10)
 #undef SEMKV_O
@@ -304,22 +401,34 @@ struct Plan {
   using GL = Geo<BASE, LL, G>;
   static constexpr int NLD = GH::NLD > GL::NLD ? GH::NLD : GL::NLD;
   static constexpr int PV = ((GH::PV > GL::PV ? GH::PV : GL::PV) + 7) / 8 * 8;
-  static constexpr int LUTH = 4 * Traits<BASE, LH>::LUTSTRIDE;   // dwords of the high-pool tables
-  static constexpr int LUTL = 4 * Traits<BASE, LL>::LUTSTRIDE;
   static constexpr int NGV = GH::NGV;
   static constexpr int NCKH = Traits<BASE, LH>::NCK, NCKL = Traits<BASE, LL>::NCK;
   static_assert(GH::NGV == GL::NGV && GH::LOPASS == GL::LOPASS, "pools share the value columns");
-  // LDS of a workgroup of nw waves (the Shared layout below, with margin)
-  static constexpr int lds_bytes(int nw) {
-    return nw * (NLD * 1024 + PV * 2 + 64) + (LUTH + LUTL) * 4 + (NCKH + NCKL) * 64 * 16 +
-           4 * kQPad * 6 + 4 * kD * 4 + 2080 + 3104 + 256;
+  // LDS of a workgroup of nw waves with rh / rl table replicas (the Shared
+  // layout below, with margin)
+  static constexpr int lds_bytes(int nw, int rh, int rl) {
+    return nw * (NLD * 1024 + PV * 2 + 64) + (Traits<BASE, LH>::LUTDW * rh + Traits<BASE, LL>::LUTDW * rl) * 4 +
+           (NCKH + NCKL) * 64 * 16 + 4 * kQPad * 6 + 4 * kD * 4 + 2080 + 3104 + 256;
   }
   // 8 waves: 2 per SIMD, one workgroup per compute unit (12 waves, 3 per SIMD,
   // measured no faster: the record work is bound by the compute unit's issue
   // rate, not by latency)
   static constexpr int NW = 8;
-  static_assert(lds_bytes(NW) <= 160 * 1024, "LDS");
   static constexpr int NT = 64 * NW;
+  // table replicas per pool: the most that fit, the low pool (the larger
+  // share of the tokens) first (32: a conflict-free lookup of any entries;
+  // LDS serves a 64-bit read 32 lanes at a time)
+  static constexpr int pick_replicas(bool hi) {
+    constexpr int opts[10][2] = {{32, 32}, {16, 32}, {8, 32}, {16, 16}, {8, 16}, {8, 8}, {4, 8}, {4, 4}, {2, 4}, {2, 2}};
+    for (const auto& o : opts)
+      if (lds_bytes(NW, o[0], o[1]) <= 160 * 1024) return hi ? o[0] : o[1];
+    return 0;
+  }
+  static constexpr int RH = pick_replicas(true), RL = pick_replicas(false);
+  static_assert(RH >= 2 && RL >= 2, "LDS");
+  static constexpr int LUTH = Traits<BASE, LH>::LUTDW * RH;  // dwords of the high-pool tables
+  static constexpr int LUTL = Traits<BASE, LL>::LUTDW * RL;
+  static_assert(Traits<BASE, LH>::NENT + Traits<BASE, LL>::NENT <= NT, "table spreading");
 };
 
 struct Fin { float m[4], l[4]; float o[4][kD]; };             // one wave's state, merged form
@@ -327,8 +436,10 @@ struct TailScratch { float lg[4][kSlots]; float mx[4], sum[4]; float o[4][kD]; }
 
 template <class PL>
 struct Shared {
+  // decode tables (high pool, low pool) first: their offsets fit the 16-bit
+  // immediate offset of an LDS read, so a lookup needs no base add
+  alignas(16) uint32_t lut[PL::LUTH + PL::LUTL];
   alignas(16) uint8_t stage[PL::NW][PL::NLD * 1024];         // per wave: one record, later its Fin
-  alignas(16) uint32_t lut[PL::LUTH + PL::LUTL];             // decode tables: high pool, low pool
   alignas(16) _Float16 pv[PL::NW][PL::PV];                   // per wave p*s weights, fp16 hi/lo
   alignas(16) _Float16 qh[4][kQPad];                         // fp16 query (affine base)
   alignas(16) float qf[4][kQPad];                            // fp32 query, rotated for tq
@@ -440,10 +551,20 @@ __device__ void run_pool(const DecodeArgs& a, Shared<PL>& sm, WaveState<PL::NGV>
     const uint4 v = sm.aq[(POOL ? PL::NCKH : 0) + c][lane];
     Aq[c] = __builtin_bit_cast(half8, uint4v{v.x, v.y, v.z, v.w});
   }
-  const uint32_t* lut = sm.lut + (POOL ? PL::LUTH : 0) + kg * Tr::LUTSTRIDE;
+  // tables: the lane's replica; entries 2^S bytes apart
+  constexpr int NR = POOL ? PL::RL : PL::RH;
+  constexpr int S = ilog2(NR * Tr::TED * 4);
+  static_assert((1 << S) == NR * Tr::TED * 4, "entry stride");
+  constexpr uint32_t KFULL = full_symbols<L, kD, kSlots>(), VFULL = full_symbols<L, kSlots, kD>();
+  const uint32_t lb = uint32_t((lane & (NR - 1)) * Tr::TED * 4);
+  const LutRef lut{reinterpret_cast<const uint8_t*>(sm.lut + (POOL ? PL::LUTH : 0)), lb, lb + (216u << S)};
   uint32_t kmask[Tr::NSK], vmask[Tr::NSV];
   segment_masks<L, kD, kSlots>(kg, kmask);
   segment_masks<L, kSlots, kD>(kg, vmask);
+#pragma unroll
+  for (int k = 0; k < Tr::NSK; ++k) kmask[k] <<= S;
+#pragma unroll
+  for (int k = 0; k < Tr::NSV; ++k) vmask[k] <<= S;
   const int koff0 = seg_off<L, kD, kSlots>(kg, n), kstep = 16 * seg_line_bits<L, kD, kSlots>(kg);
   const int voff0 = seg_off<L, kSlots, kD>(kg, n), vstep = 16 * seg_line_bits<L, kSlots, kD>(kg);
   // softmax lanes: token n of each 16-token block, head r
@@ -508,11 +629,11 @@ __device__ void run_pool(const DecodeArgs& a, Shared<PL>& sm, WaveState<PL::NGV>
     // software pipeline: the next block's table reads are in flight during
     // the current block's products
     half8 Bk[2][Tr::NCK];
-    chunk_operands<BASE, L, Tr::KSEGW, Tr::NSK, Tr::NCK>(kseg[0], kmask, lut, Bk[0]);
+    chunk_operands<BASE, L, S, KFULL, Tr::KSEGW, Tr::NSK, Tr::NCK>(kseg[0], kmask, lut, Bk[0]);
     float4v acck[4];
 #pragma unroll
     for (int blk = 0; blk < 4; ++blk) {
-      if (blk + 1 < 4) chunk_operands<BASE, L, Tr::KSEGW, Tr::NSK, Tr::NCK>(kseg[blk + 1], kmask, lut, Bk[(blk + 1) & 1]);
+      if (blk + 1 < 4) chunk_operands<BASE, L, S, KFULL, Tr::KSEGW, Tr::NSK, Tr::NCK>(kseg[blk + 1], kmask, lut, Bk[(blk + 1) & 1]);
       __builtin_amdgcn_sched_barrier(0);
       float4v acc = float4v{0, 0, 0, 0};
 #pragma unroll
@@ -613,10 +734,10 @@ __device__ void run_pool(const DecodeArgs& a, Shared<PL>& sm, WaveState<PL::NGV>
 #pragma unroll
     for (int cb = 0; cb < 8; ++cb) lds_segment<Tr::VSEGW>(vbody, voff0 + cb * vstep, vseg[cb]);
     half8 Av[2][Tr::NCV];
-    chunk_operands<BASE, L, Tr::VSEGW, Tr::NSV, Tr::NCV>(vseg[0], vmask, lut, Av[0]);
+    chunk_operands<BASE, L, S, VFULL, Tr::VSEGW, Tr::NSV, Tr::NCV>(vseg[0], vmask, lut, Av[0]);
 #pragma unroll
     for (int cb = 0; cb < 8; ++cb) {
-      if (cb + 1 < 8) chunk_operands<BASE, L, Tr::VSEGW, Tr::NSV, Tr::NCV>(vseg[cb + 1], vmask, lut, Av[(cb + 1) & 1]);
+      if (cb + 1 < 8) chunk_operands<BASE, L, S, VFULL, Tr::VSEGW, Tr::NSV, Tr::NCV>(vseg[cb + 1], vmask, lut, Av[(cb + 1) & 1]);
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int ch = 0; ch < Tr::NCV; ++ch) st.o[cb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(Av[cb & 1][ch], Bp[ch], st.o[cb], 0, 0, 0);
@@ -860,6 +981,7 @@ __global__ __launch_bounds__((Plan<BASE, LH, LL, G>::NT)) void decode_kernel(Dec
   using PL = Plan<BASE, LH, LL, G>;
   constexpr int NW = PL::NW, NT = PL::NT;
   __shared__ Shared<PL> sm;
+  static_assert(sizeof(Shared<PL>) <= 160 * 1024, "LDS");
   const int split = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
   const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
   const PoolGeom& g = a.g;
@@ -881,14 +1003,10 @@ __global__ __launch_bounds__((Plan<BASE, LH, LL, G>::NT)) void decode_kernel(Dec
   const uint16_t qbits = qt ? a.q[((int64_t(b) * g.n_kv_heads * 4) + kvh * 4 + h) * kD + c] : uint16_t(0);
   constexpr int NTH = (PL::LUTH / 4 + NT - 1) / NT, NTL = (PL::LUTL / 4 + NT - 1) / NT;
   uint4 th[NTH], tl[NTL];
-  {
-    const uint4* sh = reinterpret_cast<const uint4*>(kLutImage<BASE, LH>.w);
-    const uint4* sl = reinterpret_cast<const uint4*>(kLutImage<BASE, LL>.w);
 #pragma unroll
-    for (int k = 0; k < NTH; ++k) th[k] = sh[tid + k * NT < PL::LUTH / 4 ? tid + k * NT : 0];
+  for (int k = 0; k < NTH; ++k) th[k] = lut_chunk<BASE, LH, PL::RH>(tid + k * NT < PL::LUTH / 4 ? tid + k * NT : 0);
 #pragma unroll
-    for (int k = 0; k < NTL; ++k) tl[k] = sl[tid + k * NT < PL::LUTL / 4 ? tid + k * NT : 0];
-  }
+  for (int k = 0; k < NTL; ++k) tl[k] = lut_chunk<BASE, LL, PL::RL>(tid + k * NT < PL::LUTL / 4 ? tid + k * NT : 0);
   // the wave's first record (a wave without records loads tile 0, unused)
   uint4 R[PL::NLD];
   load_tile<BASE, LH, LL, G>(g, unit, count > 0 ? first : 0, nt0, R, lane);
