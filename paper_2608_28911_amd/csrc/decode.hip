@@ -641,6 +641,14 @@ __device__ void run_pool(const DecodeArgs& a, Shared<PL>& sm, WaveState<PL::NGV>
       acck[blk] = acc;
       __builtin_amdgcn_sched_barrier(0);
     }
+    // the value segments and the first value operands do not depend on the
+    // softmax: their LDS round trips overlap it
+    const uint8_t* vbody = rec + Tr::TB;
+    uint32_t vseg[8][Tr::VSEGW];
+#pragma unroll
+    for (int cb = 0; cb < 8; ++cb) lds_segment<Tr::VSEGW>(vbody, voff0 + cb * vstep, vseg[cb]);
+    half8 Av[2][Tr::NCV];
+    chunk_operands<BASE, L, S, VFULL, Tr::VSEGW, Tr::NSV, Tr::NCV>(vseg[0], vmask, lut, Av[0]);
 #pragma unroll
     for (int blk = 0; blk < 4; ++blk) {
       const float4v acc = acck[blk];
@@ -729,12 +737,6 @@ __device__ void run_pool(const DecodeArgs& a, Shared<PL>& sm, WaveState<PL::NGV>
       Bp[c] = half8{v[0], v[1], v[2], v[3], v[4], v[5], v[6], v[7]};
       if constexpr (Ge::LOPASS) Bl[c] = half8{w[0], w[1], w[2], w[3], w[4], w[5], w[6], w[7]};
     }
-    const uint8_t* vbody = rec + Tr::TB;
-    uint32_t vseg[8][Tr::VSEGW];
-#pragma unroll
-    for (int cb = 0; cb < 8; ++cb) lds_segment<Tr::VSEGW>(vbody, voff0 + cb * vstep, vseg[cb]);
-    half8 Av[2][Tr::NCV];
-    chunk_operands<BASE, L, S, VFULL, Tr::VSEGW, Tr::NSV, Tr::NCV>(vseg[0], vmask, lut, Av[0]);
 #pragma unroll
     for (int cb = 0; cb < 8; ++cb) {
       if (cb + 1 < 8) chunk_operands<BASE, L, S, VFULL, Tr::VSEGW, Tr::NSV, Tr::NCV>(vseg[cb + 1], vmask, lut, Av[(cb + 1) & 1]);
