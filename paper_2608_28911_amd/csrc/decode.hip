@@ -88,6 +88,13 @@ __host__ __device__ constexpr int slot_digit(int w) {
 }
 template <int BASE, int L>
 __host__ __device__ constexpr int slot_plane(int w) { return (BASE == 1 && L == 4) ? w % 2 : 0; }
+// the slot (within a symbol's STRIDE slots) of code d, plane 0
+template <int BASE, int L>
+__host__ __device__ constexpr int digit_slot(int d) {
+  for (int w = 0; w < 8; ++w)
+    if (slot_digit<BASE, L>(w) == d && slot_plane<BASE, L>(w) == 0) return w;
+  return -1;
+}
 
 // floor(s / L^i) for every symbol s < L^n as (s*2^8 * M) >> 32 with
 // M = ceil(2^24 / L^i): one 24-bit high multiply.
@@ -343,11 +350,6 @@ __device__ inline int seg_line_bits(int j) {
 
 __device__ inline float hf(uint16_t b) { return __half2float(__ushort_as_half(b)); }
 
-// fp16 weight arrays of one wave: [plane][hi|lo][head][group][80 token slots]
-// (slots 64..79 stay zero: chunk slots past the last token read them), then a
-// zero block that unused columns read at every plane offset.
-constexpr int kPvTok = 80;
-
 template <int BASE, int L, int G>
 struct Geo {
   using Tr = Traits<BASE, L>;
@@ -358,8 +360,17 @@ struct Geo {
   static constexpr int NGV = BASE == 0 ? kD / G : 1;         // value groups
   static constexpr int NPL = Tr::P;                          // value planes (tq, 4 levels: 2)
   static constexpr bool LOPASS = NGV > 2;                    // low part in a second pass
-  static constexpr int PLSTRIDE = 2 * 4 * NGV * kPvTok;      // halves per plane
-  static constexpr int PV = (2 * NPL - 1) * PLSTRIDE + kPvTok;  // planes + zero block
+  // fp16 weights of one wave, in value B-operand order: [pass][chunk][lane
+  // group][column][8 slots], so a lane reads a chunk's operand at once.  A
+  // pass has the columns (head, high|low, group) in use (8 or 16; with 4
+  // groups the low parts take a second pass); lanes of unused columns read
+  // the zero slot group at the end.  Pad slots and slots past token 63 are
+  // never written and stay zero.
+  static constexpr int NPASS = LOPASS ? 2 : 1;
+  static constexpr int NCOL = LOPASS ? 16 : 8 * NGV;
+  static constexpr int CHB = 4 * NCOL * 8;                   // halves per chunk
+  static constexpr int PASSB = Tr::NCV * CHB;                // halves per pass
+  static constexpr int PV = NPASS * PASSB + 8;
   static_assert(RB % 16 == 0, "record pieces");
 };
 
@@ -412,8 +423,9 @@ struct Plan {
   }
   // 8 waves: 2 per SIMD, one workgroup per compute unit (12 waves, 3 per SIMD,
   // measured no faster: the record work is bound by the compute unit's issue
-  // rate, not by latency)
-  static constexpr int NW = 8;
+  // rate, not by latency); 4 where 8 do not fit (4 metadata groups: larger
+  // records and weight arrays), two workgroups per compute unit
+  static constexpr int NW = lds_bytes(8, 2, 2) <= 160 * 1024 ? 8 : 4;
   static constexpr int NT = 64 * NW;
   // table replicas per pool: the most that fit, the low pool (the larger
   // share of the tokens) first (32: a conflict-free lookup of any entries;
@@ -428,7 +440,6 @@ struct Plan {
   static_assert(RH >= 2 && RL >= 2, "LDS");
   static constexpr int LUTH = Traits<BASE, LH>::LUTDW * RH;  // dwords of the high-pool tables
   static constexpr int LUTL = Traits<BASE, LL>::LUTDW * RL;
-  static_assert(Traits<BASE, LH>::NENT + Traits<BASE, LL>::NENT <= NT, "table spreading");
 };
 
 struct Fin { float m[4], l[4]; float o[4][kD]; };             // one wave's state, merged form
@@ -584,16 +595,21 @@ __device__ void run_pool(const DecodeArgs& a, Shared<PL>& sm, WaveState<PL::NGV>
       zws[i] = z;
     }
   }
-  // value B operand lanes: column n = 4h + gg
+  // value B operand lanes: column n = 4h + gg (gg < NGV: high part of group
+  // gg; then the low parts, or a second pass when NGV = 4)
   const int hv = n >> 2, gg = n & 3;
-  const int vg = gg < Ge::NGV ? gg : (!Ge::LOPASS && gg < 2 * Ge::NGV ? gg - Ge::NGV : -1);
-  const bool vlo = gg >= Ge::NGV;
   _Float16* pvw = sm.pv[wave];
-  constexpr int PLSTRIDE = Ge::PLSTRIDE;
-  const int pvzero = Ge::NPL * PLSTRIDE;
-  // base index (plane 0) of this lane's column, token 0 of its lane group's first symbol
-  const int pvcol = (vg >= 0 ? (((vlo ? 1 : 0) * 4 + hv) * Ge::NGV + vg) * kPvTok : pvzero) + Tr::n * kg;
-  const int pvlo_col = (vg >= 0 ? ((4 + hv) * Ge::NGV + vg) * kPvTok : pvzero) + Tr::n * kg;   // LOPASS
+  const bool vused = Ge::LOPASS || gg < 2 * Ge::NGV;
+  const int pvrd = vused ? kg * Ge::NCOL * 8 + (Ge::LOPASS ? n : hv * 2 * Ge::NGV + gg) * 8 : Ge::NPASS * Ge::PASSB;
+  // softmax lanes: where token 16 blk + n of each block lands (plane 0,
+  // column 0), and this head's first column
+  int pvwr[4];
+#pragma unroll
+  for (int blk = 0; blk < 4; ++blk) {
+    const int t = 16 * blk + n, p = t / Tr::n, d = t - p * Tr::n, k = p >> 2;
+    pvwr[blk] = (k / Tr::SPC) * Ge::CHB + (p & 3) * Ge::NCOL * 8 + (k % Tr::SPC) * Tr::STRIDE + digit_slot<BASE, L>(d);
+  }
+  const int pvhead = (Ge::LOPASS ? 4 : 2 * Ge::NGV) * hs * 8;
   for (int i = lane; i < Ge::PV; i += 64) pvw[i] = _Float16(0.0f);
   const int64_t nrows = a.n_rows[POOL];
 
@@ -684,8 +700,9 @@ __device__ void run_pool(const DecodeArgs& a, Shared<PL>& sm, WaveState<PL::NGV>
           const uint32_t m = vm[blk][i];
           const float x = p * hf(m & 0xFFFFu);
           const _Float16 hi = _Float16(x);
-          pvw[((0 * 4 + hs) * Ge::NGV + i) * kPvTok + t] = hi;
-          pvw[((1 * 4 + hs) * Ge::NGV + i) * kPvTok + t] = _Float16(x - float(hi));
+          _Float16* w = pvw + pvwr[blk] + pvhead;
+          w[i * 8] = hi;
+          w[Ge::LOPASS ? Ge::PASSB + i * 8 : (Ge::NGV + i) * 8] = _Float16(x - float(hi));
           st.z[i] += p * hf(m >> 16);
         }
       } else {
@@ -695,8 +712,9 @@ __device__ void run_pool(const DecodeArgs& a, Shared<PL>& sm, WaveState<PL::NGV>
         for (int pl = 0; pl < Ge::NPL; ++pl) {
           const float x = ps * wP[pl];
           const _Float16 hi = _Float16(x);
-          pvw[pl * PLSTRIDE + (0 * 4 + hs) * kPvTok + t] = hi;
-          pvw[pl * PLSTRIDE + (1 * 4 + hs) * kPvTok + t] = _Float16(x - float(hi));
+          _Float16* w = pvw + pvwr[blk] + pvhead + pl;
+          w[0] = hi;
+          w[8] = _Float16(x - float(hi));
         }
         st.z[0] += p * rho * cZ;
       }
@@ -722,20 +740,8 @@ __device__ void run_pool(const DecodeArgs& a, Shared<PL>& sm, WaveState<PL::NGV>
     half8 Bp[Tr::NCV], Bl[Ge::LOPASS ? Tr::NCV : 1];
 #pragma unroll
     for (int c = 0; c < Tr::NCV; ++c) {
-      _Float16 v[8], w[8];
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        // slot e -> token n*(kg + 4k) + digit; slots past the last token land
-        // in the zero slots 64..79 (pad slots of the chunk are plain zeros)
-        const int k = Tr::SPC * c + e / Tr::STRIDE;
-        const int dig = slot_digit<BASE, L>(e % Tr::STRIDE), pl = slot_plane<BASE, L>(e % Tr::STRIDE);
-        const bool pad = dig < 0;
-        const int toff = Tr::n * 4 * k + (pad ? 0 : dig);
-        v[e] = pad ? _Float16(0.0f) : pvw[pl * PLSTRIDE + pvcol + toff];
-        if constexpr (Ge::LOPASS) w[e] = pad ? _Float16(0.0f) : pvw[pl * PLSTRIDE + pvlo_col + toff];
-      }
-      Bp[c] = half8{v[0], v[1], v[2], v[3], v[4], v[5], v[6], v[7]};
-      if constexpr (Ge::LOPASS) Bl[c] = half8{w[0], w[1], w[2], w[3], w[4], w[5], w[6], w[7]};
+      Bp[c] = *reinterpret_cast<const half8*>(pvw + (vused ? c * Ge::CHB : 0) + pvrd);
+      if constexpr (Ge::LOPASS) Bl[c] = *reinterpret_cast<const half8*>(pvw + Ge::PASSB + c * Ge::CHB + pvrd);
     }
 #pragma unroll
     for (int cb = 0; cb < 8; ++cb) {
