@@ -88,13 +88,22 @@ __host__ __device__ constexpr int slot_digit(int w) {
 }
 template <int BASE, int L>
 __host__ __device__ constexpr int slot_plane(int w) { return (BASE == 1 && L == 4) ? w % 2 : 0; }
-// the slot (within a symbol's STRIDE slots) of code d, plane 0
+// the slot (within a symbol's STRIDE slots) of code d, plane 0: the inverse
+// of slot_digit / slot_plane
 template <int BASE, int L>
 __host__ __device__ constexpr int digit_slot(int d) {
-  for (int w = 0; w < 8; ++w)
-    if (slot_digit<BASE, L>(w) == d && slot_plane<BASE, L>(w) == 0) return w;
-  return -1;
+  return (BASE == 1 && L == 4) ? 2 * d : L == 6 ? (d < 3 ? d : d + 1) : d;
 }
+template <int BASE, int L>
+__host__ __device__ constexpr bool digit_slot_inverts() {
+  for (int d = 0; d < sym_digits(L); ++d) {
+    const int w = digit_slot<BASE, L>(d);
+    if (w < 0 || w >= 8 || slot_digit<BASE, L>(w) != d || slot_plane<BASE, L>(w) != 0) return false;
+  }
+  return true;
+}
+static_assert(digit_slot_inverts<0, 6>() && digit_slot_inverts<0, 5>() && digit_slot_inverts<0, 4>() &&
+              digit_slot_inverts<0, 3>() && digit_slot_inverts<1, 4>() && digit_slot_inverts<1, 3>(), "slots");
 
 // floor(s / L^i) for every symbol s < L^n as (s*2^8 * M) >> 32 with
 // M = ceil(2^24 / L^i): one 24-bit high multiply.
@@ -610,7 +619,8 @@ __device__ void run_pool(const DecodeArgs& a, Shared<PL>& sm, WaveState<PL::NGV>
     pvwr[blk] = (k / Tr::SPC) * Ge::CHB + (p & 3) * Ge::NCOL * 8 + (k % Tr::SPC) * Tr::STRIDE + digit_slot<BASE, L>(d);
   }
   const int pvhead = (Ge::LOPASS ? 4 : 2 * Ge::NGV) * hs * 8;
-  for (int i = lane; i < Ge::PV; i += 64) pvw[i] = _Float16(0.0f);
+  static_assert(Ge::PV % 8 == 0, "weight array pieces");
+  for (int i = lane; i < Ge::PV / 8; i += 64) reinterpret_cast<uint4*>(pvw)[i] = make_uint4(0u, 0u, 0u, 0u);
   const int64_t nrows = a.n_rows[POOL];
 
   for (int it = i0; it < i1; ++it) {
