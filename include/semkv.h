@@ -59,7 +59,8 @@ enum { SEMKV_STATUS_NAN_SCORE = 1, SEMKV_STATUS_NONFINITE_KV = 2, SEMKV_STATUS_B
  *  r_num/r_den: high-precision fraction r (Eq. 4), 0 <= r <= 1.
  *  block:  deferred block size B of Alg. 2; must be 64.
  *  head_dim must be 128, n_q_heads = 4 * n_kv_heads (GQA group of 4).
- *  max_prompt, max_new: capacity in tokens per sequence. */
+ *  max_prompt, max_new: capacity in tokens per sequence (together at most
+ *  2^29). */
 typedef struct semkv_config {
   int32_t n_layers, n_kv_heads, n_q_heads, head_dim, batch;
   int32_t base, L_hi, L_lo, group;

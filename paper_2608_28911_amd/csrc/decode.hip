@@ -182,32 +182,64 @@ __host__ __device__ constexpr uint32_t lut_entry(int e) {
   return w;
 }
 
-// One copy of the table; the workgroup spreads it into interleaved replicas
-// in LDS (entry e of replica r at entry slot e * R + r): the lanes of a wave
-// that LDS serves together read R different banks whatever entries they
-// look up, where a single copy costs ~2.4x in bank conflicts (measured).
-template <int BASE, int L>
-struct LutImage {
-  alignas(16) uint32_t w[Traits<BASE, L>::LUTDW];
-  constexpr LutImage() : w{} {
-    for (int e = 0; e < Traits<BASE, L>::LUTDW; ++e) w[e] = lut_entry<BASE, L>(e);
+// Dword K of table entry E, computed in the kernel (the values lut_entry
+// defines; the division divisors are constants).  The workgroup writes the
+// table into interleaved replicas in LDS (entry e of replica r at entry slot
+// e * R + r): the lanes of a wave that LDS serves together then read R
+// different banks whatever entries they look up, where a single copy costs
+// ~2.4x in bank conflicts (measured).
+template <int BASE, int L, int K>
+__host__ __device__ constexpr uint32_t entry_dword(uint32_t E) {
+  using Tr = Traits<BASE, L>;
+  if constexpr (L == 6) {
+    const bool hi = E >= 216;                       // s div 216 part: 2 codes
+    const uint32_t v = hi ? E - 216 : E, q6 = v / 6, q36 = v / 36;
+    if constexpr (K == 0) return ((v - 6 * q6) << 6) | ((hi ? q6 : q6 - 6 * q36) << 22);
+    else return hi ? 0u : q36 << 6;
+  } else {
+    uint32_t w = 0;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int wsl = 2 * K + h, dg = slot_digit<BASE, L>(wsl);
+      if (dg >= 0) {
+        const uint32_t p = uint32_t(ipow(L, dg)), c = E / p - (E / (p * L)) * L;
+        const uint32_t d = slot_plane<BASE, L>(wsl) ? (c >> 1) : (Tr::P == 2 ? (c & 1u) : c);
+        w |= (d << 6) << (16 * h);
+      }
+    }
+    return w;
   }
-};
+}
 
 template <int BASE, int L>
-__device__ const LutImage<BASE, L> kLutImage = LutImage<BASE, L>();
+__host__ __device__ constexpr bool entries_match_table() {
+  using Tr = Traits<BASE, L>;
+  for (uint32_t E = 0; E < uint32_t(Tr::NENT); ++E) {
+    if (entry_dword<BASE, L, 0>(E) != lut_entry<BASE, L>(E * Tr::TED) ||
+        entry_dword<BASE, L, 1>(E) != lut_entry<BASE, L>(E * Tr::TED + 1))
+      return false;
+    if (Tr::TED == 4 && (entry_dword<BASE, L, 2>(E) != lut_entry<BASE, L>(E * Tr::TED + 2) ||
+                         entry_dword<BASE, L, 3>(E) != lut_entry<BASE, L>(E * Tr::TED + 3)))
+      return false;
+  }
+  return true;
+}
+static_assert(entries_match_table<0, 6>() && entries_match_table<0, 5>() && entries_match_table<0, 4>() &&
+              entries_match_table<0, 3>() && entries_match_table<1, 4>() && entries_match_table<1, 3>(), "tables");
 
 // 16-byte piece q of the replicated LDS table (R >= 2: a piece lies in one
 // entry, repeated when entries are 8 bytes)
 template <int BASE, int L, int R>
-__device__ inline uint4 lut_chunk(int q) {
+__device__ inline uint4 lut_piece(uint32_t q) {
   using Tr = Traits<BASE, L>;
   static_assert(R >= 2 && (R & (R - 1)) == 0, "replicas");
   if constexpr (Tr::TED == 4) {
-    return reinterpret_cast<const uint4*>(kLutImage<BASE, L>.w)[q / R];
+    const uint32_t E = q / R;
+    return make_uint4(entry_dword<BASE, L, 0>(E), entry_dword<BASE, L, 1>(E), entry_dword<BASE, L, 2>(E),
+                      entry_dword<BASE, L, 3>(E));
   } else {
-    const uint2 v = reinterpret_cast<const uint2*>(kLutImage<BASE, L>.w)[(2 * q) / R];
-    return make_uint4(v.x, v.y, v.x, v.y);
+    const uint32_t E = (2 * q) / R, x = entry_dword<BASE, L, 0>(E), y = entry_dword<BASE, L, 1>(E);
+    return make_uint4(x, y, x, y);
   }
 }
 
@@ -1007,7 +1039,8 @@ __global__ __launch_bounds__((Plan<BASE, LH, LL, G>::NT)) void decode_kernel(Dec
   // ---- this workgroup's run of tiles (high pool first), this wave's records
   const int nt0 = int((a.n_rows[0] + kSlots - 1) / kSlots), nt1 = int((a.n_rows[1] + kSlots - 1) / kSlots);
   const int nt = nt0 + nt1;
-  const int f0 = int(int64_t(split) * nt / a.nsplit), f1 = int(int64_t(split + 1) * nt / a.nsplit);
+  const int f0 = int(uint32_t(split) * uint32_t(nt) / uint32_t(a.nsplit));
+  const int f1 = int(uint32_t(split + 1) * uint32_t(nt) / uint32_t(a.nsplit));
   const int first = f0 + wave;
   const int count = first < f1 ? (f1 - first + NW - 1) / NW : 0;
   const int nhi_all = first < nt0 ? (nt0 - first + NW - 1) / NW : 0;
@@ -1022,9 +1055,9 @@ __global__ __launch_bounds__((Plan<BASE, LH, LL, G>::NT)) void decode_kernel(Dec
   constexpr int NTH = (PL::LUTH / 4 + NT - 1) / NT, NTL = (PL::LUTL / 4 + NT - 1) / NT;
   uint4 th[NTH], tl[NTL];
 #pragma unroll
-  for (int k = 0; k < NTH; ++k) th[k] = lut_chunk<BASE, LH, PL::RH>(tid + k * NT < PL::LUTH / 4 ? tid + k * NT : 0);
+  for (int k = 0; k < NTH; ++k) th[k] = lut_piece<BASE, LH, PL::RH>(tid + k * NT < PL::LUTH / 4 ? tid + k * NT : 0);
 #pragma unroll
-  for (int k = 0; k < NTL; ++k) tl[k] = lut_chunk<BASE, LL, PL::RL>(tid + k * NT < PL::LUTL / 4 ? tid + k * NT : 0);
+  for (int k = 0; k < NTL; ++k) tl[k] = lut_piece<BASE, LL, PL::RL>(tid + k * NT < PL::LUTL / 4 ? tid + k * NT : 0);
   // the wave's first record (a wave without records loads tile 0, unused)
   uint4 R[PL::NLD];
   load_tile<BASE, LH, LL, G>(g, unit, count > 0 ? first : 0, nt0, R, lane);
@@ -1059,10 +1092,15 @@ __global__ __launch_bounds__((Plan<BASE, LH, LL, G>::NT)) void decode_kernel(Dec
     // per head: sums of the query over aligned runs of SEG channels (the
     // query threads are whole waves)
     constexpr int SEG = (BASE == 0 && G < 64) ? G : 64;
-    float x = sm.qf[h][c];
-#pragma unroll
-    for (int o = 1; o < SEG; o <<= 1) x += __shfl_xor(x, o);
-    if ((c % SEG) == 0) sm.zpart[h][c / SEG] = x;
+    static_assert(SEG == 32 || SEG == 64, "query runs");
+    const float x = row_sum16(sm.qf[h][c]);
+    const float r0 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), 0));
+    const float r1 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), 16));
+    const float r2 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), 32));
+    const float r3 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), 48));
+    if (SEG == 64 && (c & 63) == 0) sm.zpart[h][c / 64] = (r0 + r1) + (r2 + r3);
+    if (SEG == 32 && (c & 63) == 0) sm.zpart[h][c / 32] = r0 + r1;
+    if (SEG == 32 && (c & 63) == 32) sm.zpart[h][c / 32] = r2 + r3;
   }
   build_aq<BASE, LH, G, 0>(a, sm);
   build_aq<BASE, LL, G, 1>(a, sm);

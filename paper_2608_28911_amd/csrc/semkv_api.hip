@@ -184,7 +184,7 @@ int semkv_cache_sizes(const semkv_config* cfg, semkv_sizes* out) {
   if (k.n_layers < 1 || k.n_kv_heads < 1 || k.batch < 1 || k.n_layers > 128) return SEMKV_EINVAL;
   if (k.r_den <= 0 || k.r_num < 0 || k.r_num > k.r_den || k.max_prompt < 0 || k.max_new < 0)
     return SEMKV_EINVAL;
-  if (k.max_prompt > (int64_t(1) << 30) || k.max_new > (int64_t(1) << 30)) return SEMKV_EINVAL;
+  if (k.max_prompt + k.max_new > (int64_t(1) << 29)) return SEMKV_EINVAL;   // decode splits use 32-bit tile math
   if (k.head_dim != 128 || k.n_q_heads != 4 * k.n_kv_heads || k.block != 64) return SEMKV_EUNSUPPORTED;
   if (k.base != SEMKV_BASE_AFFINE && k.base != SEMKV_BASE_TQ) return SEMKV_EUNSUPPORTED;
   if (!levels_ok(k.base, k.L_hi, k.L_lo)) return SEMKV_EUNSUPPORTED;
