@@ -67,6 +67,8 @@ def parse():
     ap.add_argument("--group", type=int, default=None, help="override the affine metadata group")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="budget of the oracle sample")
+    ap.add_argument("--no-generate", dest="generate", action="store_false",
+                    help="skip the generation leg of workloads with generated tokens")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="run a device fill and copy of this many MiB first (hardware counter calibration)")
     return ap.parse_args()
@@ -129,6 +131,91 @@ def cpu_baseline(cfgw, seconds):
     }
 
 
+def generation(cfgw, cache, gen, dev, outlier_ch):
+    """Generated tokens under block-wise deferred allocation (Alg. 2): per
+    token, every layer appends its fp16 K/V to the tail and attends over the
+    pools and the tail; then the token's score is committed, and every 64th
+    commit closes the block (in-block ranking, quantize + pack of the 64 rows
+    onto the pool ends).  Each block is captured as two HIP graphs -- its 64
+    tokens without the last commit, and that commit with the close -- and
+    both are replayed in order under events, so the close is timed on its own.
+    Returns the timing summary and the close's algorithmic bytes."""
+    import torch
+    B, H, Hq, nL, n = cfgw.batch, cfgw.n_kv_heads, cfgw.n_q_heads, cfgw.n_layers, cfgw.n_gen
+    blk = cfgw.block
+    assert n % blk == 0, "the generation leg closes whole blocks"
+    kn = torch.empty((n, nL, B, H, 128), dtype=torch.float16, device=dev)
+    vn = torch.empty_like(kn)
+    qg = torch.empty((n, nL, B, Hq, 128), dtype=torch.float16, device=dev)
+    for i in range(0, n, blk):
+        k = torch.randn((blk, nL, B, H, 128), generator=gen, device=dev)
+        for l in range(nL):            # the prompt keys' outlier channels
+            for h in range(H):
+                k[:, l, :, h, outlier_ch[l][h]] *= cfgw.outlier_scale
+        kn[i:i + blk] = k.half()
+        vn[i:i + blk] = torch.randn((blk, nL, B, H, 128), generator=gen, device=dev).half()
+        qg[i:i + blk] = torch.randn((blk, nL, B, Hq, 128), generator=gen, device=dev).half()
+        del k
+    from workloads import synth
+    sg = torch.from_numpy(synth.gen_scores(cfgw)).to(dev)
+    out = torch.empty((nL, B, Hq, 128), dtype=torch.float32, device=dev)
+    ws = cache.workspace()
+    rows0 = cache.c.n_hi + cache.c.n_lo
+    graphs = []
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    torch.cuda.synchronize()
+    with torch.cuda.stream(s):
+        for b0 in range(0, n, blk):
+            g_steps, g_close = torch.cuda.CUDAGraph(), torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g_steps, stream=s):
+                for i in range(b0, b0 + blk):
+                    for l in range(nL):
+                        cache.append_kv(l, kn[i, l], vn[i, l])
+                        cache.decode_attn(l, qg[i, l], out=out[l], workspace=ws)
+                    if i + 1 < b0 + blk:
+                        cache.append_commit(sg[i])
+            with torch.cuda.graph(g_close, stream=s):
+                cache.append_commit(sg[b0 + blk - 1])
+            graphs.append((g_steps, g_close))
+    torch.cuda.synchronize()
+    assert cache.c.n_scored == 0 and cache.c.n_hi + cache.c.n_lo == rows0 + n
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True),
+           torch.cuda.Event(enable_timing=True)) for _ in graphs]
+    torch.cuda.synchronize()
+    for (g_steps, g_close), (e0, e1, e2) in zip(graphs, ev):
+        e0.record()
+        g_steps.replay()
+        e1.record()
+        g_close.replay()
+        e2.record()
+    torch.cuda.synchronize()
+    assert cache.status() == 0, "device status word %d" % cache.status()
+    t_steps = sum(e0.elapsed_time(e1) for e0, e1, _ in ev)
+    closes = [e1.elapsed_time(e2) for _, e1, e2 in ev]
+    total_ms = t_steps + sum(closes)
+    close_us = sum(closes) / len(closes) * 1e3
+    # close traffic: the block's fp16 K/V of every layer and kv head read,
+    # its rows written packed (row-exact bits + metadata)
+    from paper_2608_28911_amd.fmt import line_bits
+    from fractions import Fraction
+    kb = round(Fraction(cfgw.r_num * blk, cfgw.r_den))      # round(rB), ties to even
+    meta = (128 // cfgw.group) * 4
+    units = B * nL * H
+    close_in = units * 2 * blk * 128 * 2
+    close_out = units * (kb * (2 * line_bits(cfgw.L_hi, 128) / 8 + 2 * meta) +
+                         (blk - kb) * (2 * line_bits(cfgw.L_lo, 128) / 8 + 2 * meta))
+    del kn, vn, qg
+    return {
+        "tokens": n, "tokens_per_s": round(B * n / (total_ms * 1e-3), 2),
+        "ms_per_token": round(total_ms / n, 4),
+        "close_us": round(close_us, 2), "close_gbps": round((close_in + close_out) / (close_us * 1e-6) / 1e9, 1),
+        "close_bytes": int(close_in + close_out), "blocks": len(graphs),
+        "rows_hi": cache.c.n_hi, "rows_lo": cache.c.n_lo,
+        "note": "per token: append + decode of every layer, then commit; every 64th commit closes the block",
+    }
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -148,7 +235,8 @@ def main():
     B, H, Hq, T, nL = cfgw.batch, cfgw.n_kv_heads, cfgw.n_q_heads, cfgw.prompt_len, cfgw.n_layers
     base = P.BASE_AFFINE if cfgw.base == "affine" else P.BASE_TQ
     cfg = P.make_config(n_layers=nL, n_kv_heads=H, batch=B, base=base, L_hi=cfgw.L_hi, L_lo=cfgw.L_lo,
-                        group=cfgw.group, r_num=cfgw.r_num, r_den=cfgw.r_den, max_prompt=T, max_new=0)
+                        group=cfgw.group, r_num=cfgw.r_num, r_den=cfgw.r_den, max_prompt=T,
+                        max_new=cfgw.n_gen if args.generate else 0)
     signs = synth.all_sign_words(cfgw) if base == P.BASE_TQ else None
     cache = P.SemKVCache(cfg, sign_words=signs)
 
@@ -157,9 +245,11 @@ def main():
     gen.manual_seed(cfgw.seed)
     K = torch.empty((nL, B, H, T, 128), dtype=torch.float16, device=dev)
     V = torch.empty_like(K)
+    outlier_ch = []
     for l in range(nL):
         k = torch.randn((B, H, T, 128), generator=gen, device=dev, dtype=torch.float32)
         ch = torch.randperm(128, generator=gen, device=dev)[:cfgw.outliers * H].view(H, cfgw.outliers)
+        outlier_ch.append(ch)
         for h in range(H):
             k[:, h, :, ch[h]] *= cfgw.outlier_scale
         K[l] = k.half()
@@ -272,6 +362,9 @@ def main():
                      "traffic": measured_traffic() if cfgw.name == "llama8b_kv_b1_t32768_affine" else None,
                      "kernel": "decode_kernel", "bytes_per_launch": int(alg)},
     }
+    if args.generate and cfgw.n_gen > 0:
+        del q
+        line["generation"] = generation(cfgw, cache, gen, dev, outlier_ch)
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(cfgw, args.cpu_seconds)
     print(json.dumps(line), flush=True)
