@@ -1,11 +1,13 @@
 // decode.hip -- split-K GQA decode attention over the mixed-precision cache
 // (the decoding consumer of SemKV, Sec. 3.1 and Alg. 1), for gfx950.
 //
-// Work split: the tiles of one (sequence, kv head) unit -- its high pool, then
-// its low pool -- are cut into nsplit balanced runs, one per workgroup, with
-// nsplit chosen by the host so that the whole grid is resident at once.  A
-// workgroup is NW = 8 waves; wave w takes tiles w, w + NW, ... of its run and keeps its own online-softmax state for the 4 query heads of
-// the kv head.  Records are staged through registers: the next record's
+// Work split: a (sequence, kv head) unit's tiles -- its high pool, then its
+// low pool -- are dealt to nsplit workgroups of NW waves (nsplit chosen by the
+// host so that the whole grid is resident at once): tile u goes to wave slot
+// u mod (nsplit NW), slot v = w nsplit + s being wave w of workgroup s.  Every
+// wave thus gets an even share of the (costlier) high-precision tiles, first
+// in its sequence, and keeps its own online-softmax state for the 4 query
+// heads of the kv head.  Records are staged through registers: the next record's
 // 16-byte pieces are loaded while the current one is computed from the wave's
 // LDS buffer, then written over it.  Per record:
 //   scores  C[16 rows (head, group) x 16 tokens] += A B on MFMA
@@ -582,7 +584,7 @@ __device__ void build_aq(const DecodeArgs& a, Shared<PL>& sm) {
 
 template <int BASE, int LH, int LL, int G, int POOL, class PL>
 __device__ void run_pool(const DecodeArgs& a, Shared<PL>& sm, WaveState<PL::NGV>& st, const uint8_t* unit,
-                         int nt0, int first, int i0, int i1, int count, uint4 (&R)[PL::NLD]) {
+                         int nt0, int first, int stride, int i0, int i1, int count, uint4 (&R)[PL::NLD]) {
   constexpr int L = POOL ? LL : LH;
   using Tr = Traits<BASE, L>;
   using Ge = Geo<BASE, L, G>;
@@ -656,9 +658,9 @@ __device__ void run_pool(const DecodeArgs& a, Shared<PL>& sm, WaveState<PL::NGV>
   const int64_t nrows = a.n_rows[POOL];
 
   for (int it = i0; it < i1; ++it) {
-    const int tile = first + PL::NW * it;
+    const int tile = first + stride * it;
     const bool more = it + 1 < count;
-    if (more) load_tile<BASE, LH, LL, G>(a.g, unit, tile + PL::NW, nt0, R, lane);
+    if (more) load_tile<BASE, LH, LL, G>(a.g, unit, tile + stride, nt0, R, lane);
     const int ptile = POOL ? tile - nt0 : tile;
     const uint8_t* kmeta = rec + 2 * Tr::TB;
     const uint8_t* vmeta = kmeta + Ge::MB;
@@ -1036,15 +1038,12 @@ __global__ __launch_bounds__((Plan<BASE, LH, LL, G>::NT)) void decode_kernel(Dec
   const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
   const PoolGeom& g = a.g;
 
-  // ---- this workgroup's run of tiles (high pool first), this wave's records
+  // ---- this wave's tiles: first, first + stride, ... (high pool first)
   const int nt0 = int((a.n_rows[0] + kSlots - 1) / kSlots), nt1 = int((a.n_rows[1] + kSlots - 1) / kSlots);
-  const int nt = nt0 + nt1;
-  const int f0 = int(uint32_t(split) * uint32_t(nt) / uint32_t(a.nsplit));
-  const int f1 = int(uint32_t(split + 1) * uint32_t(nt) / uint32_t(a.nsplit));
-  const int first = f0 + wave;
-  const int count = first < f1 ? (f1 - first + NW - 1) / NW : 0;
-  const int nhi_all = first < nt0 ? (nt0 - first + NW - 1) / NW : 0;
-  const int nhi = nhi_all < count ? nhi_all : count;
+  const int nt = nt0 + nt1, stride = a.nsplit * NW;
+  const int first = wave * a.nsplit + split;
+  const int count = first < nt ? (nt - first + stride - 1) / stride : 0;
+  const int nhi = first < nt0 ? (nt0 - first + stride - 1) / stride : 0;
   const uint8_t* unit = g.pools + unit_offset(g, b, a.layer, kvh);
 
   // ---- query and decode tables, then the first record in flight; the query
@@ -1115,8 +1114,8 @@ __global__ __launch_bounds__((Plan<BASE, LH, LL, G>::NT)) void decode_kernel(Dec
 #pragma unroll
   for (int cb = 0; cb < 8; ++cb) st.o[cb] = float4v{0, 0, 0, 0};
   if (count > 0) store_pieces(R, sm.stage[wave], lane);
-  if (nhi > 0) run_pool<BASE, LH, LL, G, 0>(a, sm, st, unit, nt0, first, 0, nhi, count, R);
-  if (count > nhi) run_pool<BASE, LH, LL, G, 1>(a, sm, st, unit, nt0, first, nhi, count, count, R);
+  if (nhi > 0) run_pool<BASE, LH, LL, G, 0>(a, sm, st, unit, nt0, first, stride, 0, nhi, count, R);
+  if (count > nhi) run_pool<BASE, LH, LL, G, 1>(a, sm, st, unit, nt0, first, stride, nhi, count, count, R);
   wave_finish<BASE, G>(sm, st);
   __syncthreads();
   const bool tail = split == a.nsplit - 1 && a.n_tail > 0;

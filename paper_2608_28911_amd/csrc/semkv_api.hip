@@ -107,9 +107,10 @@ int64_t decode_slots(const semkv_config& k) {
 }
 
 // Decode split plan: the tiles of each (sequence, kv head) unit, high pool
-// then low pool, are cut into nsplit balanced runs, one workgroup each, so
-// that the whole grid is resident at once and every wave has a record.  The
-// fp16 tail rides with the last run.  0: nothing cached.
+// then low pool, are dealt to nsplit workgroups (tile u to wave slot u mod
+// nsplit * waves), so that the whole grid is resident at once and every wave
+// has a record.  The fp16 tail rides with the last workgroup.  0: nothing
+// cached.
 int plan(const semkv_cache* c, int n_tail) {
   const int64_t nt = (c->n_hi + kSlots - 1) / kSlots + (c->n_lo + kSlots - 1) / kSlots;
   if (nt == 0) return n_tail > 0 ? 1 : 0;
