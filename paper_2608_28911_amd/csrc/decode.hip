@@ -466,8 +466,8 @@ struct Plan {
   }
   // 8 waves: 2 per SIMD, one workgroup per compute unit (12 waves, 3 per SIMD,
   // measured no faster: the record work is bound by the compute unit's issue
-  // rate, not by latency); 4 where 8 do not fit (4 metadata groups: larger
-  // records and weight arrays), two workgroups per compute unit
+  // rate, not by latency).  A level pair whose 8-wave workgroup does not fit
+  // (6 and 3 levels with 32-channel groups) is refused by the host.
   static constexpr int NW = lds_bytes(8, 2, 2) <= 160 * 1024 ? 8 : 4;
   static constexpr int NT = 64 * NW;
   // table replicas per pool: the most that fit, the low pool (the larger
@@ -1034,6 +1034,7 @@ __global__ __launch_bounds__((Plan<BASE, LH, LL, G>::NT)) void decode_kernel(Dec
   constexpr int NW = PL::NW, NT = PL::NT;
   __shared__ Shared<PL> sm;
   static_assert(sizeof(Shared<PL>) <= 160 * 1024, "LDS");
+  static_assert(NT == 4 * kD, "one thread per (head, channel) of the query and the output");
   const int split = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
   const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
   const PoolGeom& g = a.g;
@@ -1168,25 +1169,40 @@ __global__ __launch_bounds__((Plan<BASE, LH, LL, G>::NT)) void decode_kernel(Dec
 template <int BASE, int LH, int LL, int G>
 int waves_of() { return Plan<BASE, LH, LL, G>::NW; }
 
+// the kernel needs 4 x 128 threads (one per query head and channel): level
+// pairs whose 8-wave workgroup does not fit the LDS are not built
+template <int BASE, int LH, int LL, int G>
+constexpr bool fits() { return Plan<BASE, LH, LL, G>::NT == 4 * kD; }
+
 template <int BASE, int LH, int LL, int G>
 int occupancy() {
-  int n = 0;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, decode_kernel<BASE, LH, LL, G>, Plan<BASE, LH, LL, G>::NT, 0) != hipSuccess)
-    return 1;
-  return n > 0 ? n : 1;
+  if constexpr (!fits<BASE, LH, LL, G>()) {
+    return 0;
+  } else {
+    int n = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, decode_kernel<BASE, LH, LL, G>, Plan<BASE, LH, LL, G>::NT, 0) != hipSuccess)
+      return 1;
+    return n > 0 ? n : 1;
+  }
+}
+
+template <int BASE, int LH, int LL, int G>
+int launch_g(const DecodeArgs& a, hipStream_t st) {
+  if constexpr (!fits<BASE, LH, LL, G>()) {
+    return -2;
+  } else {
+    dim3 grid(a.nsplit, a.g.n_kv_heads, a.g.batch);
+    hipLaunchKernelGGL((decode_kernel<BASE, LH, LL, G>), grid, dim3(Plan<BASE, LH, LL, G>::NT), 0, st, a);
+    return hipGetLastError() == hipSuccess ? 0 : -5;
+  }
 }
 
 template <int BASE, int LH, int LL>
 int launch_dec(const DecodeArgs& a, hipStream_t st) {
-  dim3 grid(a.nsplit, a.g.n_kv_heads, a.g.batch);
-  if constexpr (BASE == 1) {
-    hipLaunchKernelGGL((decode_kernel<BASE, LH, LL, 128>), grid, dim3(Plan<BASE, LH, LL, 128>::NT), 0, st, a);
-  } else {
-    if (a.g.G == 128) hipLaunchKernelGGL((decode_kernel<BASE, LH, LL, 128>), grid, dim3(Plan<BASE, LH, LL, 128>::NT), 0, st, a);
-    else if (a.g.G == 64) hipLaunchKernelGGL((decode_kernel<BASE, LH, LL, 64>), grid, dim3(Plan<BASE, LH, LL, 64>::NT), 0, st, a);
-    else hipLaunchKernelGGL((decode_kernel<BASE, LH, LL, 32>), grid, dim3(Plan<BASE, LH, LL, 32>::NT), 0, st, a);
-  }
-  return hipGetLastError() == hipSuccess ? 0 : -5;
+  if constexpr (BASE == 1) return launch_g<BASE, LH, LL, 128>(a, st);
+  if (a.g.G == 128) return launch_g<BASE, LH, LL, 128>(a, st);
+  if (a.g.G == 64) return launch_g<BASE, LH, LL, 64>(a, st);
+  return launch_g<BASE, LH, LL, 32>(a, st);
 }
 
 template <int BASE, int LH, int LL>
