@@ -9,20 +9,24 @@
 // in its sequence, and keeps its own online-softmax state for the 4 query
 // heads of the kv head.  Records are staged through registers: the next record's
 // 16-byte pieces are loaded while the current one is computed from the wave's
-// LDS buffer, then written over it.  Per record:
-//   scores  C[16 rows (head, group) x 16 tokens] += A B on MFMA
-//           (v_mfma_f32_16x16x32_f16): A holds the query restricted to one
-//           metadata group per row, B the base-L digits of 16 tokens, decoded
-//           from the packed K symbols through LDS tables straight into fp16
-//           bit patterns d << 6 (the subnormal d * 2^-18: the matrix core
-//           keeps full fp32 accuracy for subnormal inputs only when their
-//           leading bit is at or above mantissa bit 5, measured on gfx950).
-//           The affine dequantization x = s c + z is folded out:
+// LDS buffer, then written over it.  Products run on the int8 matrix cores
+// (v_mfma_i32_16x16x64_i8), exact in their integer sums.  Per record:
+//   scores  C[16 rows (head, byte) x 16 tokens] += A B: A holds the query of
+//           head h as a fixed-point integer qi = rint(q 2^e) (|qi| < 2^20, e
+//           per head and metadata group) split into three bytes, one per row,
+//           restricted to one metadata group; B the base-L digits of 16
+//           tokens as bytes, decoded from the packed K symbols through LDS
+//           tables (one dword of digit bytes per entry).  The affine
+//           dequantization x = s c + z is folded out:
 //           q.x = s (q.c) + z (sum q) per group.
 //   softmax online, base 2; unnormalized p, rescaled when the maximum moves.
-//   values  C[16 channels x 16 cols] += A[16 x 32 tokens] B[32 tokens x 16]
-//           with A the V digits (V symbols run along tokens) and B = p * s
-//           split into fp16 high and low parts.
+//   values  C[16 rows (head, byte) x 16 channels] += A[16 x 64 tokens]
+//           B[64 tokens x 16 channels] with A the weights p * s as 21-bit
+//           integers (one power-of-2 scale per head, three bytes in three
+//           rows) and B the V digits (V symbols run along tokens).  The
+//           integer sums run across records and are folded into float sums
+//           only when the running maximum moves or a record's weights would
+//           not fit the scale.
 // The last run also takes the fp16 tail of generated tokens.  The waves'
 // states merge in LDS into one partial per workgroup; the last workgroup of a
 // unit to finish merges the partials (log-sum-exp) and, for the TurboQuant-MSE
@@ -34,13 +38,12 @@
 namespace semkv {
 namespace {
 
-typedef _Float16 half8 __attribute__((ext_vector_type(8)));
+typedef int32_t int4v __attribute__((ext_vector_type(4)));
 typedef float float4v __attribute__((ext_vector_type(4)));
 typedef uint32_t uint4v __attribute__((ext_vector_type(4)));
 
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kRsqrtD = 0.08838834764831845f;   // 1 / sqrt(128)
-constexpr float kDigitScale = 262144.0f;          // 2^18: digit d is fed as d * 2^-18
 constexpr int kQPad = 160;                         // query rows, zero past channel 127
 
 // ------------------------------------------------------------ traits ----
@@ -51,16 +54,18 @@ __host__ __device__ constexpr int ipow(int b, int e) {
   return r;
 }
 
-// Chunk layout: 8 MFMA slots per lane group per chunk, filled by SPC symbols
-// of STRIDE slots each; slot_digit / slot_plane give the code a slot holds
-// (-1: a zero pad slot).  4-level codes of the tq base take two slots, their
-// low and high bit (the Lloyd-Max levels are affine in those bits).
+// Chunk layout: an MFMA operand gives each lane 16 byte slots; a chunk fills
+// them with SPC symbols of STRIDE slots each; slot_digit / slot_plane give the
+// code a slot holds (-1: a zero pad slot).  4-level codes of the tq base take
+// two slots, their low and high bit (the Lloyd-Max levels are affine in those
+// bits).
 template <int BASE, int L>
 struct Traits {
   static constexpr int n = sym_digits(L);
   static constexpr int P = (BASE == 1 && L == 4) ? 2 : 1;   // MFMA slots per code
-  static constexpr int SPC = (L == 5 || (L == 4 && BASE == 0)) ? 2 : 1;
-  static constexpr int STRIDE = 8 / SPC;
+  static constexpr int STRIDE = (L == 5 || (L == 4 && BASE == 0)) ? 4 : 8;
+  static constexpr int SPC = 16 / STRIDE;
+  static constexpr int EDW = STRIDE / 4;                     // operand dwords per symbol
   static constexpr int SK = num_syms(L, kD), SV = num_syms(L, kSlots);
   static constexpr int NSK = (SK + 3) / 4, NSV = (SV + 3) / 4;
   static constexpr int NCK = (NSK + SPC - 1) / SPC, NCV = (NSV + SPC - 1) / SPC;
@@ -68,16 +73,11 @@ struct Traits {
   static constexpr int TB = tile_bytes(L);
   static constexpr int KSEGW = (NSK * W + 31) / 32;          // normalized dwords of a K segment
   static constexpr int VSEGW = (NSV * W + 31) / 32;
-  // decode table: symbol -> MFMA operand dwords (codes pre-shifted to d << 6).
-  // L = 6 splits a symbol into s mod 216 (3 codes) and s div 216 (2 codes),
-  // two dwords per entry in both parts.
-  static constexpr int EDW = STRIDE / 2;                     // operand dwords per symbol
-  static constexpr int TED = L == 6 ? 2 : EDW;               // dwords per table entry
+  // decode table: symbol -> operand dwords of digit bytes.  L = 6 splits a
+  // symbol into s mod 216 (3 codes) and s div 216 (2 codes), one dword each.
+  static constexpr int TED = L == 6 ? 1 : EDW;               // dwords per table entry
   static constexpr int NENT = L == 6 ? 216 + 36 : ipow(L, n);   // entries (L = 6: both parts)
   static constexpr int LUTDW = NENT * TED;                   // dwords of one copy
-  // largest query channel an A-operand slot addresses (past 127: a zero pad)
-  static constexpr int MAXCH = n * (3 + 4 * (SPC * NCK - 1)) + n - 1;
-  static_assert(MAXCH < kQPad, "query padding");
 };
 
 template <int BASE, int L>
@@ -154,91 +154,75 @@ __device__ inline uint32_t field(const uint32_t (&seg)[NW]) {
 
 // ------------------------------------------------------ decode tables ----
 
-// Dword e of the decode table: MFMA slots 2k, 2k+1 of symbol value v (codes as
-// d << 6); for L = 6, dwords 0..431 map s mod 216 to slots 0-3 and 432..503
-// map s div 216 to slots 4-7 (6 and 7 are zero pads).
-template <int BASE, int L>
-__host__ __device__ constexpr uint32_t lut_entry(int e) {
-  using Tr = Traits<BASE, L>;
-  if (L == 6) {
-    if (e < 432) {
-      const int v = e / 2;
-      return (e & 1) ? (uint32_t(v / 36) << 6) : (uint32_t(v % 6) << 6) | (uint32_t(v / 6 % 6) << 22);
-    }
-    const int v = (e - 432) / 2;
-    return ((e - 432) & 1) ? 0u : (uint32_t(v % 6) << 6) | (uint32_t(v / 6) << 22);
-  }
-  const int v = e / Tr::EDW, k = e % Tr::EDW;
-  uint32_t w = 0;
-  for (int h = 0; h < 2; ++h) {
-    const int wsl = 2 * k + h, dg = slot_digit<BASE, L>(wsl);
-    uint32_t d = 0;
-    if (dg >= 0) {
-      uint32_t c = uint32_t(v);
-      for (int t = 0; t < dg; ++t) c /= uint32_t(L);
-      c %= uint32_t(L);
-      d = slot_plane<BASE, L>(wsl) ? (c >> 1) : (Tr::P == 2 ? (c & 1u) : c);
-    }
-    w |= (d << 6) << (16 * h);
-  }
-  return w;
-}
-
-// Dword K of table entry E, computed in the kernel (the values lut_entry
-// defines; the division divisors are constants).  The workgroup writes the
-// table into interleaved replicas in LDS (entry e of replica r at entry slot
-// e * R + r): the lanes of a wave that LDS serves together then read R
-// different banks whatever entries they look up, where a single copy costs
-// ~2.4x in bank conflicts (measured).
+// Dword K of table entry E: the digit bytes of operand slots 4K .. 4K+3 of
+// symbol value E (L = 6: entries 0..215 give s mod 216 -> slots 0-3, entries
+// 216..251 give s div 216 -> slots 4-7).
 template <int BASE, int L, int K>
 __host__ __device__ constexpr uint32_t entry_dword(uint32_t E) {
   using Tr = Traits<BASE, L>;
   if constexpr (L == 6) {
-    const bool hi = E >= 216;                       // s div 216 part: 2 codes
-    const uint32_t v = hi ? E - 216 : E, q6 = v / 6, q36 = v / 36;
-    if constexpr (K == 0) return ((v - 6 * q6) << 6) | ((hi ? q6 : q6 - 6 * q36) << 22);
-    else return hi ? 0u : q36 << 6;
+    const bool hi = E >= 216;
+    const uint32_t v = hi ? E - 216 : E;
+    return hi ? (v % 6) | ((v / 6) << 8) : (v % 6) | ((v / 6 % 6) << 8) | ((v / 36) << 16);
   } else {
     uint32_t w = 0;
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      const int wsl = 2 * K + h, dg = slot_digit<BASE, L>(wsl);
+    for (int j = 0; j < 4; ++j) {
+      const int wsl = 4 * K + j, dg = slot_digit<BASE, L>(wsl);
       if (dg >= 0) {
         const uint32_t p = uint32_t(ipow(L, dg)), c = E / p - (E / (p * L)) * L;
         const uint32_t d = slot_plane<BASE, L>(wsl) ? (c >> 1) : (Tr::P == 2 ? (c & 1u) : c);
-        w |= (d << 6) << (16 * h);
+        w |= d << (8 * j);
       }
     }
     return w;
   }
 }
 
+// the digits a table entry gives, checked against plain base-L arithmetic
+// (L = 6: the entries of both parts, which cover every symbol through
+// v mod 216 and v div 216)
 template <int BASE, int L>
-__host__ __device__ constexpr bool entries_match_table() {
+__host__ __device__ constexpr bool entries_match_digits() {
   using Tr = Traits<BASE, L>;
-  for (uint32_t E = 0; E < uint32_t(Tr::NENT); ++E) {
-    if (entry_dword<BASE, L, 0>(E) != lut_entry<BASE, L>(E * Tr::TED) ||
-        entry_dword<BASE, L, 1>(E) != lut_entry<BASE, L>(E * Tr::TED + 1))
-      return false;
-    if (Tr::TED == 4 && (entry_dword<BASE, L, 2>(E) != lut_entry<BASE, L>(E * Tr::TED + 2) ||
-                         entry_dword<BASE, L, 3>(E) != lut_entry<BASE, L>(E * Tr::TED + 3)))
-      return false;
+  const int nent = Tr::NENT;
+  for (int E = 0; E < nent; ++E) {
+    for (int w = 0; w < Tr::STRIDE; ++w) {
+      uint32_t byte = 0, want = 0;
+      if (L == 6) {
+        const bool hi = w >= 4;
+        if (hi != (E >= 216)) continue;
+        byte = (entry_dword<BASE, L, 0>(uint32_t(E)) >> (8 * (w % 4))) & 0xFFu;
+        const int v = hi ? E - 216 : E, dg = slot_digit<BASE, L>(w) - (hi ? 3 : 0);
+        if (slot_digit<BASE, L>(w) >= 0) want = uint32_t(dg == 0 ? v % 6 : dg == 1 ? v / 6 % 6 : v / 36);
+      } else {
+        const uint32_t dw = w < 4 ? entry_dword<BASE, L, 0>(uint32_t(E)) : entry_dword<BASE, L, 1>(uint32_t(E));
+        byte = (dw >> (8 * (w % 4))) & 0xFFu;
+        const int dg = slot_digit<BASE, L>(w);
+        if (dg >= 0) {
+          int c = E;
+          for (int t = 0; t < dg; ++t) c /= L;
+          c %= L;
+          want = slot_plane<BASE, L>(w) ? uint32_t(c >> 1) : (Tr::P == 2 ? uint32_t(c & 1) : uint32_t(c));
+        }
+      }
+      if (byte != want) return false;
+    }
   }
   return true;
 }
-static_assert(entries_match_table<0, 6>() && entries_match_table<0, 5>() && entries_match_table<0, 4>() &&
-              entries_match_table<0, 3>() && entries_match_table<1, 4>() && entries_match_table<1, 3>(), "tables");
+static_assert(entries_match_digits<0, 6>() && entries_match_digits<0, 5>() && entries_match_digits<0, 4>() &&
+              entries_match_digits<0, 3>() && entries_match_digits<1, 4>() && entries_match_digits<1, 3>(), "tables");
 
-// 16-byte piece q of the replicated LDS table (R >= 2: a piece lies in one
-// entry, repeated when entries are 8 bytes)
+// 16-byte piece q of the replicated LDS table (entry e of replica r at entry
+// slot e R + r; R >= 4, so a piece lies in one entry, repeated)
 template <int BASE, int L, int R>
 __device__ inline uint4 lut_piece(uint32_t q) {
   using Tr = Traits<BASE, L>;
-  static_assert(R >= 2 && (R & (R - 1)) == 0, "replicas");
-  if constexpr (Tr::TED == 4) {
-    const uint32_t E = q / R;
-    return make_uint4(entry_dword<BASE, L, 0>(E), entry_dword<BASE, L, 1>(E), entry_dword<BASE, L, 2>(E),
-                      entry_dword<BASE, L, 3>(E));
+  static_assert(R >= 4 && (R & (R - 1)) == 0, "replicas");
+  if constexpr (Tr::TED == 1) {
+    const uint32_t x = entry_dword<BASE, L, 0>((4 * q) / R);
+    return make_uint4(x, x, x, x);
   } else {
     const uint32_t E = (2 * q) / R, x = entry_dword<BASE, L, 0>(E), y = entry_dword<BASE, L, 1>(E);
     return make_uint4(x, y, x, y);
@@ -314,7 +298,7 @@ struct LutRef {
 __host__ __device__ constexpr int ilog2(int x) { return x <= 1 ? 0 : 1 + ilog2(x / 2); }
 
 // floor(v / 216) for v < 6^5 as the high word of x * M with x = (v << S) + b,
-// b < 2^S a multiple of 8 (the lane's replica offset): one multiplier found by
+// b < 2^S a multiple of 4 (the lane's replica offset): one multiplier found by
 // search for S = 7; otherwise b must be 0 and M = ceil(2^(32-S) / 216)
 __host__ __device__ constexpr uint32_t magic216(int S, bool with_base) {
   return with_base ? (S == 7 ? 155345u : 0u) : uint32_t(((uint64_t(1) << (32 - S)) + 215) / 216);
@@ -322,49 +306,58 @@ __host__ __device__ constexpr uint32_t magic216(int S, bool with_base) {
 __host__ __device__ constexpr bool magic216_exact(int S, bool with_base) {
   const uint64_t M = magic216(S, with_base);
   if (M == 0 || M >= (1u << 24) || (7775u << S) + (1u << S) >= (1u << 24)) return false;
-  const uint64_t bmax = with_base ? (1u << S) - 8 : 0;     // x * M is monotonic in b
+  const uint64_t bmax = with_base ? (1u << S) - 4 : 0;     // x * M is monotonic in b
   for (uint64_t v = 0; v < 7776; ++v)
     if (((v << S) * M) >> 32 != v / 216 || (((v << S) + bmax) * M) >> 32 != v / 216) return false;
   return true;
 }
 
+// operand dwords of 6-level symbol K: the s mod 216 and s div 216 entries
+template <int BASE, int S, uint32_t FULL, int K, int NW, int NS>
+__device__ inline uint2 l6_symbol(const uint32_t (&seg)[NW], const uint32_t (&maskS)[NS], const LutRef& lr) {
+  constexpr bool WB = magic216_exact(S, true);
+  static_assert(WB || magic216_exact(S, false), "digit split");
+  uint32_t x;                                                            // (v << S) + lbase
+  if constexpr (WB) x = sym_addr<BASE, 6, S, FULL, K, NW, NS>(seg, maskS, lr.lbase);
+  else x = sym_addr<BASE, 6, S, FULL, K, NW, NS>(seg, maskS, 0u);
+  const uint32_t hi = mulhi24(x, magic216(S, WB));                       // v div 216
+  if constexpr (!WB) x = and_or(x, 0xFFFFFFFFu, lr.lbase);
+  const uint32_t lo = mad_i24(hi, -(216 << S), x);                       // ((v mod 216) << S) + lbase
+  return make_uint2(*reinterpret_cast<const uint32_t*>(lr.t + lo),
+                    *reinterpret_cast<const uint32_t*>(lr.t + ((hi << S) + lr.hbase)));
+}
+
 // MFMA operand of chunk C of a segment (symbols SPC*C ..), read from the tables
 template <int BASE, int L, int S, uint32_t FULL, int C, int NW, int NS>
-__device__ inline half8 chunk_operand(const uint32_t (&seg)[NW], const uint32_t (&maskS)[NS], const LutRef& lr) {
+__device__ inline int4v chunk_operand(const uint32_t (&seg)[NW], const uint32_t (&maskS)[NS], const LutRef& lr) {
   using Tr = Traits<BASE, L>;
   uint4v r;
   if constexpr (L == 6) {
-    constexpr bool WB = magic216_exact(S, true);
-    static_assert(WB || magic216_exact(S, false), "digit split");
-    uint32_t x;                                                          // (v << S) + lbase
-    if constexpr (WB) x = sym_addr<BASE, L, S, FULL, C, NW, NS>(seg, maskS, lr.lbase);
-    else x = sym_addr<BASE, L, S, FULL, C, NW, NS>(seg, maskS, 0u);
-    const uint32_t hi = mulhi24(x, magic216(S, WB));                     // v div 216
-    if constexpr (!WB) x = and_or(x, 0xFFFFFFFFu, lr.lbase);
-    const uint32_t lo = mad_i24(hi, -(216 << S), x);                     // ((v mod 216) << S) + lbase
-    const uint2 a = *reinterpret_cast<const uint2*>(lr.t + lo);
-    const uint2 b = *reinterpret_cast<const uint2*>(lr.t + ((hi << S) + lr.hbase));
-    r = uint4v{a.x, a.y, b.x, b.y};
-  } else if constexpr (Tr::SPC == 2) {
+    const uint2 p0 = l6_symbol<BASE, S, FULL, 2 * C, NW, NS>(seg, maskS, lr);
+    const uint2 p1 = l6_symbol<BASE, S, FULL, 2 * C + 1, NW, NS>(seg, maskS, lr);
+    r = uint4v{p0.x, p0.y, p1.x, p1.y};
+  } else if constexpr (Tr::SPC == 4) {
+    const uint32_t a = *reinterpret_cast<const uint32_t*>(lr.t + sym_addr<BASE, L, S, FULL, 4 * C, NW, NS>(seg, maskS, lr.lbase));
+    const uint32_t b = *reinterpret_cast<const uint32_t*>(lr.t + sym_addr<BASE, L, S, FULL, 4 * C + 1, NW, NS>(seg, maskS, lr.lbase));
+    const uint32_t c = *reinterpret_cast<const uint32_t*>(lr.t + sym_addr<BASE, L, S, FULL, 4 * C + 2, NW, NS>(seg, maskS, lr.lbase));
+    const uint32_t e = *reinterpret_cast<const uint32_t*>(lr.t + sym_addr<BASE, L, S, FULL, 4 * C + 3, NW, NS>(seg, maskS, lr.lbase));
+    r = uint4v{a, b, c, e};
+  } else {
     const uint2 a = *reinterpret_cast<const uint2*>(lr.t + sym_addr<BASE, L, S, FULL, 2 * C, NW, NS>(seg, maskS, lr.lbase));
     const uint2 b = *reinterpret_cast<const uint2*>(lr.t + sym_addr<BASE, L, S, FULL, 2 * C + 1, NW, NS>(seg, maskS, lr.lbase));
     r = uint4v{a.x, a.y, b.x, b.y};
-  } else {
-    const uint4 a = *reinterpret_cast<const uint4*>(lr.t + sym_addr<BASE, L, S, FULL, C, NW, NS>(seg, maskS, lr.lbase));
-    r = uint4v{a.x, a.y, a.z, a.w};
   }
-  return __builtin_bit_cast(half8, r);
+  return __builtin_bit_cast(int4v, r);
 }
 
 // MFMA operands of all NC chunks of a segment: every table read is issued
 // before the first product needs one (LDS returns them in order)
 template <int BASE, int L, int S, uint32_t FULL, int NW, int NS, int NC>
 __device__ inline void chunk_operands(const uint32_t (&seg)[NW], const uint32_t (&maskS)[NS], const LutRef& lr,
-                                      half8 (&A)[NC]) {
-  static_assert(NC <= 11, "chunks");
+                                      int4v (&A)[NC]) {
+  static_assert(NC <= 4, "chunks");
 #define SEMKV_O(C) if constexpr (C < NC) A[C] = chunk_operand<BASE, L, S, FULL, C, NW, NS>(seg, maskS, lr);
-  SEMKV_O(0) SEMKV_O(1) SEMKV_O(2) SEMKV_O(3) SEMKV_O(4) SEMKV_O(5)
-  SEMKV_O(6) SEMKV_O(7) SEMKV_O(8) SEMKV_O(9) SEMKV_O(10)
+  SEMKV_O(0) SEMKV_O(1) SEMKV_O(2) SEMKV_O(3)
 #undef SEMKV_O
 }
 
@@ -399,21 +392,16 @@ struct Geo {
   static constexpr int MB = meta_bytes(BASE, G);
   static constexpr int RB = 2 * Tr::TB + 2 * MB;
   static constexpr int NLD = (RB + 1023) / 1024;            // 1 KB staging pieces per record
-  static constexpr int NG = BASE == 0 ? kD / G : 2;          // score rows per head
+  static constexpr int NG = BASE == 0 ? kD / G : 1;          // score products per chunk (query groups)
   static constexpr int NGV = BASE == 0 ? kD / G : 1;         // value groups
   static constexpr int NPL = Tr::P;                          // value planes (tq, 4 levels: 2)
-  static constexpr bool LOPASS = NGV > 2;                    // low part in a second pass
-  // fp16 weights of one wave, in value B-operand order: [pass][chunk][lane
-  // group][column][8 slots], so a lane reads a chunk's operand at once.  A
-  // pass has the columns (head, high|low, group) in use (8 or 16; with 4
-  // groups the low parts take a second pass); lanes of unused columns read
-  // the zero slot group at the end.  Pad slots and slots past token 63 are
-  // never written and stay zero.
-  static constexpr int NPASS = LOPASS ? 2 : 1;
-  static constexpr int NCOL = LOPASS ? 16 : 8 * NGV;
-  static constexpr int CHB = 4 * NCOL * 8;                   // halves per chunk
-  static constexpr int PASSB = Tr::NCV * CHB;                // halves per pass
-  static constexpr int PV = NPASS * PASSB + 8;
+  // int8 weights of one wave and one value group at a time, in value
+  // A-operand order: [chunk][lane group][row][16 slots], so a lane reads a
+  // chunk's operand at once.  Row 4h + s holds byte s of head h's weights;
+  // rows 4h + 3, pad slots and slots past token 63 are never written and
+  // stay zero.
+  static constexpr int CHB = 4 * 16 * 16;                    // bytes per chunk
+  static constexpr int PV = Tr::NCV * CHB;                   // bytes per wave
   static_assert(RB % 16 == 0, "record pieces");
 };
 
@@ -454,33 +442,32 @@ struct Plan {
   using GH = Geo<BASE, LH, G>;
   using GL = Geo<BASE, LL, G>;
   static constexpr int NLD = GH::NLD > GL::NLD ? GH::NLD : GL::NLD;
-  static constexpr int PV = ((GH::PV > GL::PV ? GH::PV : GL::PV) + 7) / 8 * 8;
+  static constexpr int PV = GH::PV > GL::PV ? GH::PV : GL::PV;
   static constexpr int NGV = GH::NGV;
+  static constexpr int NG = GH::NG;
   static constexpr int NCKH = Traits<BASE, LH>::NCK, NCKL = Traits<BASE, LL>::NCK;
-  static_assert(GH::NGV == GL::NGV && GH::LOPASS == GL::LOPASS, "pools share the value columns");
+  static_assert(GH::NGV == GL::NGV, "pools share the value groups");
   // LDS of a workgroup of nw waves with rh / rl table replicas (the Shared
   // layout below, with margin)
   static constexpr int lds_bytes(int nw, int rh, int rl) {
-    return nw * (NLD * 1024 + PV * 2 + 64) + (Traits<BASE, LH>::LUTDW * rh + Traits<BASE, LL>::LUTDW * rl) * 4 +
-           (NCKH + NCKL) * 64 * 16 + 4 * kQPad * 6 + 4 * kD * 4 + 2080 + 3104 + 256;
+    return nw * (NLD * 1024 + PV + 256) + (Traits<BASE, LH>::LUTDW * rh + Traits<BASE, LL>::LUTDW * rl) * 4 +
+           NG * (NCKH + NCKL) * 64 * 16 + 4 * kQPad * 4 + 4 * kD * 4 + 2080 + 3104 + 512;
   }
-  // 8 waves: 2 per SIMD, one workgroup per compute unit (12 waves, 3 per SIMD,
-  // measured no faster: the record work is bound by the compute unit's issue
-  // rate, not by latency).  A level pair whose 8-wave workgroup does not fit
-  // (6 and 3 levels with 32-channel groups) is refused by the host.
-  static constexpr int NW = lds_bytes(8, 2, 2) <= 160 * 1024 ? 8 : 4;
+  // 8 waves: 2 per SIMD, one workgroup per compute unit.  A level pair whose
+  // 8-wave workgroup does not fit is refused by the host.
+  static constexpr int NW = lds_bytes(8, 4, 4) <= 160 * 1024 ? 8 : 4;
   static constexpr int NT = 64 * NW;
   // table replicas per pool: the most that fit, the low pool (the larger
-  // share of the tokens) first (32: a conflict-free lookup of any entries;
-  // LDS serves a 64-bit read 32 lanes at a time)
+  // share of the tokens) first (32 dword replicas: a conflict-free lookup of
+  // any entries)
   static constexpr int pick_replicas(bool hi) {
-    constexpr int opts[10][2] = {{32, 32}, {16, 32}, {8, 32}, {16, 16}, {8, 16}, {8, 8}, {4, 8}, {4, 4}, {2, 4}, {2, 2}};
+    constexpr int opts[8][2] = {{32, 32}, {16, 32}, {8, 32}, {16, 16}, {8, 16}, {8, 8}, {4, 8}, {4, 4}};
     for (const auto& o : opts)
       if (lds_bytes(NW, o[0], o[1]) <= 160 * 1024) return hi ? o[0] : o[1];
     return 0;
   }
   static constexpr int RH = pick_replicas(true), RL = pick_replicas(false);
-  static_assert(RH >= 2 && RL >= 2, "LDS");
+  static_assert(RH >= 4 && RL >= 4, "LDS");
   static constexpr int LUTH = Traits<BASE, LH>::LUTDW * RH;  // dwords of the high-pool tables
   static constexpr int LUTL = Traits<BASE, LL>::LUTDW * RL;
 };
@@ -494,14 +481,14 @@ struct Shared {
   // immediate offset of an LDS read, so a lookup needs no base add
   alignas(16) uint32_t lut[PL::LUTH + PL::LUTL];
   alignas(16) uint8_t stage[PL::NW][PL::NLD * 1024];         // per wave: one record, later its Fin
-  alignas(16) _Float16 pv[PL::NW][PL::PV];                   // per wave p*s weights, fp16 hi/lo
-  alignas(16) _Float16 qh[4][kQPad];                         // fp16 query (affine base)
+  alignas(16) uint8_t pv[PL::NW][PL::PV];                    // per wave int8 weights
   alignas(16) float qf[4][kQPad];                            // fp32 query, rotated for tq
   float qorig[4][kD];                                        // query as given (fp16 tail)
   Fin tfin;                                                  // the fp16 tail's state
   TailScratch ts;
-  alignas(16) uint4 aq[PL::NCKH + PL::NCKL][64];             // score A operands, per pool and lane
-  float zpart[4][4];                                         // per head: sums of q over 32/64 channels
+  alignas(16) uint4 aq[PL::NG][PL::NCKH + PL::NCKL][64];     // score A operands, per group, pool and lane
+  float zpart[4][4];                                         // per head: sums of q over 32-channel runs
+  float qmax[4][4];                                          // per head: max |q| over 32-channel runs
   float zc[PL::NW][4][4];                                    // per wave, head, group: sum p * zero
   int last;
 };
@@ -512,8 +499,20 @@ __device__ inline Fin* wave_fin(Shared<PL>& sm, int w) { return reinterpret_cast
 template <int NGV>
 struct WaveState {
   float m, l, z[NGV];
-  float4v o[8];
+  float qw, qwi;     // scale of the int8 weights (a power of 2) and its inverse
+  float of[8];       // flushed value sums, channel 16 cb + n of head r
+  int4v cv[8];       // integer value sums since the last flush, rows (head, byte)
 };
+
+// the integer q . codes of one head from its three byte rows
+__device__ inline float comb3(const int4v& c) {
+  return fmaf(float(c[0]), 16384.0f, fmaf(float(c[1]), 128.0f, float(c[2])));
+}
+// the same for one product of a score: |row 0| < 2^16, |row 1| < 2^17, so
+// the integer sum stays below 2^31
+__device__ inline float comb3_score(const int4v& c) {
+  return float((c[0] << 14) + (c[1] << 7) + c[2]);
+}
 
 // ---------------------------------------------------------- staging ----
 
@@ -542,41 +541,84 @@ __device__ inline void store_pieces(const uint4 (&r)[NMAX], uint8_t* lds, int la
   for (int j = 0; j < NMAX; ++j) *reinterpret_cast<uint4*>(lds + j * 1024 + lane * 16) = r[j];
 }
 
+// Per head, of the query x (affine) or the rotated query (tq) held by one
+// thread per (head, channel) -- whole waves, 64 channels of one head each:
+// sums over aligned runs of 32 channels (the zero-point terms) and the
+// largest magnitude of each such run (the fixed-point scale).
+template <class PL>
+__device__ inline void query_runs(float x, int h, int c, Shared<PL>& sm) {
+  const float sx = row_sum16(x), ax = row_max16(fabsf(x));
+  const float s0 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, sx), 0));
+  const float s1 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, sx), 16));
+  const float s2 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, sx), 32));
+  const float s3 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, sx), 48));
+  const float a0 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, ax), 0));
+  const float a1 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, ax), 16));
+  const float a2 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, ax), 32));
+  const float a3 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, ax), 48));
+  if ((c & 31) == 0) {
+    sm.zpart[h][c / 32] = (c & 32) ? s2 + s3 : s0 + s1;
+    sm.qmax[h][c / 32] = (c & 32) ? fmaxf(a2, a3) : fmaxf(a0, a1);
+  }
+}
+
+// sum of head h's query over query group g, and the exponent e of its fixed-
+// point form: the largest magnitude a pool's operands hold (the tq plane
+// weights included), times 2^e, lies in [2^19, 2^20)
+template <int BASE, int G, class PL>
+__device__ inline float query_sum(const Shared<PL>& sm, int h, int g) {
+  constexpr int GQ = BASE == 0 ? G : kD;
+  float z = 0.0f;
+#pragma unroll
+  for (int k = 0; k < GQ / 32; ++k) z += sm.zpart[h][g * GQ / 32 + k];
+  return z;
+}
+template <int BASE, int L, int G, class PL>
+__device__ inline int query_exp(const Shared<PL>& sm, const float* mu, int h, int g) {
+  constexpr int GQ = BASE == 0 ? G : kD;
+  float mx = 0.0f;
+#pragma unroll
+  for (int k = 0; k < GQ / 32; ++k) mx = fmaxf(mx, sm.qmax[h][g * GQ / 32 + k]);
+  mx *= BASE == 0 || L == 3 ? 1.0f : mu[2] + mu[3];        // tq, 4 levels: mu2 + mu3 > mu3 - mu2 > 0
+  const int E = __builtin_amdgcn_frexp_expf(mx);          // mx = f 2^E, f in [0.5, 1)
+  return mx >= 1e-30f ? 20 - E : 0;
+}
+
 // Score A operands of one pool for all 64 lane contexts, by the workgroup:
-// lane (n = 4h + kq, kg) chunk c slot e holds the query of head h at the
-// channel the slot addresses (zero past channel 127), restricted to metadata
-// group kq (affine) or split into an fp16 high (kq = 0) and low (kq = 1) part
-// of the plane-weighted query (tq).
-template <int BASE, int L, int G, int POOL, class PL>
+// for query group g, lane (row m = 4h + s, kg) chunk c slot e holds byte s of
+// qi = rint(x 2^e) at the channel the slot addresses (zero past channel 127,
+// in pad slots, outside group g and in rows 4h + 3), x the query of head h
+// (affine) or its plane-weighted rotated query (tq), |qi| < 2^20.  qi splits
+// as 2^14 b0 + 2^7 b1 + b2 (b0 signed, b1, b2 in [0, 127]), so a product sums
+// the exact integer qi . codes in three rows.
+// Items are dealt to threads from thread OFF on (the low pool's start where
+// the high pool's end), so the two pools' items spread over the workgroup.
+template <int BASE, int L, int G, int POOL, int OFF, class PL>
 __device__ void build_aq(const DecodeArgs& a, Shared<PL>& sm) {
   using Tr = Traits<BASE, L>;
   using Ge = Geo<BASE, L, G>;
   const float* mu = a.mu[POOL];
   const float wP[2] = {BASE == 0 ? 1.0f : (L == 3 ? 1.0f : mu[3] - mu[2]),
                        BASE == 0 ? 1.0f : (L == 3 ? 1.0f : mu[2] + mu[3])};
-  for (int item = threadIdx.x; item < Tr::NCK * 64; item += PL::NT) {
-    const int c = item >> 6, ln = item & 63;
-    const int n = ln & 15, kg = ln >> 4, h = n >> 2, kq = n & 3;
-    const int cb = Tr::n * kg;
-    _Float16 v[8];
+  for (int item = (int(threadIdx.x) + PL::NT - OFF % PL::NT) % PL::NT; item < Ge::NG * Tr::NCK * 64; item += PL::NT) {
+    const int g = item / (Tr::NCK * 64), c = (item >> 6) % Tr::NCK, ln = item & 63;
+    const int m = ln & 15, kg = ln >> 4, h = m >> 2, sp = m & 3;
+    const int e = query_exp<BASE, L, G>(sm, mu, h, g);
+    // branch free: every slot reads at a clamped channel (all reads in
+    // flight together) and keeps the byte only where the slot is real
+    const int shift = sp == 0 ? 14 : sp == 1 ? 7 : 0;
+    const int bmask = sp == 0 ? 0xFF : 0x7F;
+    uint32_t w[4] = {0u, 0u, 0u, 0u};
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const int k = Tr::SPC * c + e / Tr::STRIDE, w = e % Tr::STRIDE;
-      const int dig = slot_digit<BASE, L>(w), pl = slot_plane<BASE, L>(w);
-      v[e] = _Float16(0.0f);
-      if (dig >= 0) {
-        const int ch = cb + Tr::n * 4 * k + dig;         // >= 128: a pad slot, the query reads 0
-        if (BASE == 0) {
-          if (kq < Ge::NG && (ch >> __builtin_ctz(G)) == kq) v[e] = sm.qh[h][ch];
-        } else {
-          const float x = wP[pl] * sm.qf[h][ch];
-          const _Float16 hi = _Float16(x);
-          v[e] = kq == 0 ? hi : (kq == 1 ? _Float16(x - float(hi)) : _Float16(0.0f));
-        }
-      }
+    for (int sl = 0; sl < 16; ++sl) {
+      const int k = Tr::SPC * c + sl / Tr::STRIDE, ws = sl % Tr::STRIDE;
+      const int dig = slot_digit<BASE, L>(ws), pl = slot_plane<BASE, L>(ws);
+      const int ch = kg * Tr::n + Tr::n * 4 * k + (dig < 0 ? 0 : dig);      // >= 128: a pad slot
+      const bool ok = dig >= 0 && sp < 3 && ch < kD && (BASE == 1 || ch / G == g);
+      const int qi = int(rintf(ldexpf(wP[pl] * sm.qf[h][ch < kD ? ch : 0], e)));
+      w[sl >> 2] |= (ok ? uint32_t((qi >> shift) & bmask) : 0u) << (8 * (sl & 3));
     }
-    const uint4v u = __builtin_bit_cast(uint4v, half8{v[0], v[1], v[2], v[3], v[4], v[5], v[6], v[7]});
-    sm.aq[(POOL ? PL::NCKH : 0) + c][ln] = make_uint4(u.x, u.y, u.z, u.w);
+    sm.aq[g][(POOL ? PL::NCKH : 0) + c][ln] = make_uint4(w[0], w[1], w[2], w[3]);
   }
 }
 
@@ -588,6 +630,7 @@ __device__ void run_pool(const DecodeArgs& a, Shared<PL>& sm, WaveState<PL::NGV>
   constexpr int L = POOL ? LL : LH;
   using Tr = Traits<BASE, L>;
   using Ge = Geo<BASE, L, G>;
+  constexpr int NG = Ge::NG, NGV = Ge::NGV;
   const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
   const int n = lane & 15, r = lane >> 4, kg = r;
   uint8_t* rec = sm.stage[wave];
@@ -598,12 +641,15 @@ __device__ void run_pool(const DecodeArgs& a, Shared<PL>& sm, WaveState<PL::NGV>
   const float wP[2] = {BASE == 0 ? 1.0f : (L == 3 ? 1.0f : mu[3] - mu[2]),
                        BASE == 0 ? 1.0f : (L == 3 ? 1.0f : mu[2] + mu[3])};
 
-  // ---- score A operands (built once per workgroup)
-  half8 Aq[Tr::NCK];
+  // ---- score A operands (built once per workgroup): in registers for one
+  // query group, else read per product
+  int4v Aq[NG == 1 ? Tr::NCK : 1];
+  if constexpr (NG == 1) {
 #pragma unroll
-  for (int c = 0; c < Tr::NCK; ++c) {
-    const uint4 v = sm.aq[(POOL ? PL::NCKH : 0) + c][lane];
-    Aq[c] = __builtin_bit_cast(half8, uint4v{v.x, v.y, v.z, v.w});
+    for (int c = 0; c < Tr::NCK; ++c) {
+      const uint4 v = sm.aq[0][(POOL ? PL::NCKH : 0) + c][lane];
+      Aq[c] = __builtin_bit_cast(int4v, uint4v{v.x, v.y, v.z, v.w});
+    }
   }
   // tables: the lane's replica; entries 2^S bytes apart
   constexpr int NR = POOL ? PL::RL : PL::RH;
@@ -622,39 +668,23 @@ __device__ void run_pool(const DecodeArgs& a, Shared<PL>& sm, WaveState<PL::NGV>
   const int koff0 = seg_off<L, kD, kSlots>(kg, n), kstep = 16 * seg_line_bits<L, kD, kSlots>(kg);
   const int voff0 = seg_off<L, kSlots, kD>(kg, n), vstep = 16 * seg_line_bits<L, kSlots, kD>(kg);
   // softmax lanes: token n of each 16-token block, head r
-  const int hs = r;
-  float zws[Ge::NG];                         // sum of q over each metadata group of head hs
-  {
-    constexpr int SEG = (BASE == 0 && G < 64) ? G : 64;
+  float zws[NG], qsc[NG];                    // per query group of head r: sum of q, 2^-e
 #pragma unroll
-    for (int i = 0; i < Ge::NG; ++i) {
-      float z = 0.0f;
-      if (BASE == 0) {
-#pragma unroll
-        for (int p = i * G / SEG; p < (i + 1) * G / SEG; ++p) z += sm.zpart[hs][p];
-      } else if (i == 0) {
-        z = sm.zpart[hs][0] + sm.zpart[hs][1];
-      }
-      zws[i] = z;
-    }
+  for (int i = 0; i < NG; ++i) {
+    zws[i] = query_sum<BASE, G>(sm, r, i);
+    qsc[i] = ldexpf(1.0f, -query_exp<BASE, L, G>(sm, mu, r, i));
   }
-  // value B operand lanes: column n = 4h + gg (gg < NGV: high part of group
-  // gg; then the low parts, or a second pass when NGV = 4)
-  const int hv = n >> 2, gg = n & 3;
-  _Float16* pvw = sm.pv[wave];
-  const bool vused = Ge::LOPASS || gg < 2 * Ge::NGV;
-  const int pvrd = vused ? kg * Ge::NCOL * 8 + (Ge::LOPASS ? n : hv * 2 * Ge::NGV + gg) * 8 : Ge::NPASS * Ge::PASSB;
-  // softmax lanes: where token 16 blk + n of each block lands (plane 0,
-  // column 0), and this head's first column
+  // softmax lanes: where token 16 blk + n of each block lands in the weight
+  // operands (value group 0, plane 0, row 4r)
+  uint8_t* pvw = sm.pv[wave];
   int pvwr[4];
 #pragma unroll
   for (int blk = 0; blk < 4; ++blk) {
     const int t = 16 * blk + n, p = t / Tr::n, d = t - p * Tr::n, k = p >> 2;
-    pvwr[blk] = (k / Tr::SPC) * Ge::CHB + (p & 3) * Ge::NCOL * 8 + (k % Tr::SPC) * Tr::STRIDE + digit_slot<BASE, L>(d);
+    pvwr[blk] = (k / Tr::SPC) * Ge::CHB + (p & 3) * 256 + 64 * r + (k % Tr::SPC) * Tr::STRIDE + digit_slot<BASE, L>(d);
   }
-  const int pvhead = (Ge::LOPASS ? 4 : 2 * Ge::NGV) * hs * 8;
-  static_assert(Ge::PV % 8 == 0, "weight array pieces");
-  for (int i = lane; i < Ge::PV / 8; i += 64) reinterpret_cast<uint4*>(pvw)[i] = make_uint4(0u, 0u, 0u, 0u);
+  static_assert(Ge::PV % 16 == 0, "weight array pieces");
+  for (int i = lane; i < Ge::PV / 16; i += 64) reinterpret_cast<uint4*>(pvw)[i] = make_uint4(0u, 0u, 0u, 0u);
   const int64_t nrows = a.n_rows[POOL];
 
   for (int it = i0; it < i1; ++it) {
@@ -666,13 +696,13 @@ __device__ void run_pool(const DecodeArgs& a, Shared<PL>& sm, WaveState<PL::NGV>
     const uint8_t* vmeta = kmeta + Ge::MB;
     const int nvalid = nrows - int64_t(ptile) * kSlots < kSlots ? int(nrows - int64_t(ptile) * kSlots) : kSlots;
 
-    // ---- scores: C[(h, kq)][token] = q_h,kq . codes; lane holds token n, head r
+    // ---- scores: C[(h, byte)][token] = q_h bytes . codes; lane holds token n, head r
     float lg[4];
     // all four K segments and the lane's metadata words in one round trip
     uint32_t kseg[4][Tr::KSEGW];
 #pragma unroll
     for (int blk = 0; blk < 4; ++blk) lds_segment<Tr::KSEGW>(rec, koff0 + blk * kstep, kseg[blk]);
-    constexpr int NKM = BASE == 0 ? Ge::NG : 1, NVM = BASE == 0 ? Ge::NGV : 1;
+    constexpr int NKM = BASE == 0 ? NG : 1, NVM = BASE == 0 ? NGV : 1;
     uint32_t km[4][NKM], vm[4][NVM];
 #pragma unroll
     for (int blk = 0; blk < 4; ++blk) {
@@ -686,19 +716,51 @@ __device__ void run_pool(const DecodeArgs& a, Shared<PL>& sm, WaveState<PL::NGV>
         vm[blk][i] = BASE == 0 ? *reinterpret_cast<const uint32_t*>(vmeta + (i * kSlots + t) * 4)
                                : uint32_t(*reinterpret_cast<const uint16_t*>(vmeta + t * 2));
     }
+    // the score of token 16 blk + n from its products, one per query group
+    auto score = [&](int blk, const int4v (&acc)[NG]) {
+      float x = 0.0f;
+      if constexpr (BASE == 0) {
+#pragma unroll
+        for (int i = 0; i < NG; ++i)
+          x += comb3_score(acc[i]) * qsc[i] * hf(km[blk][i] & 0xFFFFu) + hf(km[blk][i] >> 16) * zws[i];
+      } else {
+        const float rho = hf(uint16_t(km[blk][0]));
+        x = comb3_score(acc[0]) * qsc[0] * (rho * cS) + rho * cZ * zws[0];
+      }
+      return 16 * blk + n < nvalid ? x * (kLog2e * kRsqrtD) : -INFINITY;
+    };
     // software pipeline: the next block's table reads are in flight during
     // the current block's products
-    half8 Bk[2][Tr::NCK];
+    int4v Bk[2][Tr::NCK];
     chunk_operands<BASE, L, S, KFULL, Tr::KSEGW, Tr::NSK, Tr::NCK>(kseg[0], kmask, lut, Bk[0]);
-    float4v acck[4];
+    constexpr bool DEFER = NG == 1;          // score arithmetic after the value segment reads
+    int4v acck[DEFER ? 4 : 1][NG];
 #pragma unroll
     for (int blk = 0; blk < 4; ++blk) {
       if (blk + 1 < 4) chunk_operands<BASE, L, S, KFULL, Tr::KSEGW, Tr::NSK, Tr::NCK>(kseg[blk + 1], kmask, lut, Bk[(blk + 1) & 1]);
       __builtin_amdgcn_sched_barrier(0);
-      float4v acc = float4v{0, 0, 0, 0};
+      int4v acc[NG];
 #pragma unroll
-      for (int ch = 0; ch < Tr::NCK; ++ch) acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(Aq[ch], Bk[blk & 1][ch], acc, 0, 0, 0);
-      acck[blk] = acc;
+      for (int i = 0; i < NG; ++i) {
+        acc[i] = int4v{0, 0, 0, 0};
+#pragma unroll
+        for (int ch = 0; ch < Tr::NCK; ++ch) {
+          int4v A;
+          if constexpr (NG == 1) {
+            A = Aq[ch];
+          } else {
+            const uint4 v = sm.aq[i][(POOL ? PL::NCKH : 0) + ch][lane];
+            A = __builtin_bit_cast(int4v, uint4v{v.x, v.y, v.z, v.w});
+          }
+          acc[i] = __builtin_amdgcn_mfma_i32_16x16x64_i8(A, Bk[blk & 1][ch], acc[i], 0, 0, 0);
+        }
+      }
+      if constexpr (DEFER) {
+#pragma unroll
+        for (int i = 0; i < NG; ++i) acck[blk][i] = acc[i];
+      } else {
+        lg[blk] = score(blk, acc);
+      }
       __builtin_amdgcn_sched_barrier(0);
     }
     // the value segments and the first value operands do not depend on the
@@ -707,22 +769,11 @@ __device__ void run_pool(const DecodeArgs& a, Shared<PL>& sm, WaveState<PL::NGV>
     uint32_t vseg[8][Tr::VSEGW];
 #pragma unroll
     for (int cb = 0; cb < 8; ++cb) lds_segment<Tr::VSEGW>(vbody, voff0 + cb * vstep, vseg[cb]);
-    half8 Av[2][Tr::NCV];
-    chunk_operands<BASE, L, S, VFULL, Tr::VSEGW, Tr::NSV, Tr::NCV>(vseg[0], vmask, lut, Av[0]);
+    int4v Bv[2][Tr::NCV];
+    chunk_operands<BASE, L, S, VFULL, Tr::VSEGW, Tr::NSV, Tr::NCV>(vseg[0], vmask, lut, Bv[0]);
+    if constexpr (DEFER) {
 #pragma unroll
-    for (int blk = 0; blk < 4; ++blk) {
-      const float4v acc = acck[blk];
-      const int t = 16 * blk + n;
-      float x = 0.0f;
-      if (BASE == 0) {
-#pragma unroll
-        for (int i = 0; i < Ge::NG; ++i)
-          x += acc[i] * hf(km[blk][i] & 0xFFFFu) + hf(km[blk][i] >> 16) * zws[i] * (1.0f / kDigitScale);
-      } else {
-        const float rho = hf(uint16_t(km[blk][0]));
-        x = (acc[0] + acc[1]) * (rho * cS) + rho * cZ * zws[0] * (1.0f / kDigitScale);
-      }
-      lg[blk] = t < nvalid ? x * (kDigitScale * kLog2e * kRsqrtD) : -INFINITY;
+      for (int blk = 0; blk < 4; ++blk) lg[blk] = score(blk, acck[blk]);
     }
     // ---- online softmax (base 2) for head r over this record's 64 tokens
     float mt = fmaxf(fmaxf(lg[0], lg[1]), fmaxf(lg[2], lg[3]));
@@ -730,73 +781,80 @@ __device__ void run_pool(const DecodeArgs& a, Shared<PL>& sm, WaveState<PL::NGV>
     const float m_new = fmaxf(st.m, mt);
     const float alpha = __builtin_amdgcn_exp2f(st.m - m_new);
     st.m = m_new;
-    float lsum = 0.0f;
+    float lsum = 0.0f, wmax = 0.0f;
+    float wv[4][NGV][Ge::NPL];               // value weights of the lane's tokens
 #pragma unroll
-    for (int i = 0; i < Ge::NGV; ++i) st.z[i] *= alpha;
+    for (int i = 0; i < NGV; ++i) st.z[i] *= alpha;
 #pragma unroll
     for (int blk = 0; blk < 4; ++blk) {
-      const int t = 16 * blk + n;
       const float p = __builtin_amdgcn_exp2f(lg[blk] - m_new);   // 0 for masked tokens
       lsum += p;
-      if (BASE == 0) {
+      if constexpr (BASE == 0) {
 #pragma unroll
-        for (int i = 0; i < Ge::NGV; ++i) {
+        for (int i = 0; i < NGV; ++i) {
           const uint32_t m = vm[blk][i];
-          const float x = p * hf(m & 0xFFFFu);
-          const _Float16 hi = _Float16(x);
-          _Float16* w = pvw + pvwr[blk] + pvhead;
-          w[i * 8] = hi;
-          w[Ge::LOPASS ? Ge::PASSB + i * 8 : (Ge::NGV + i) * 8] = _Float16(x - float(hi));
+          wv[blk][i][0] = p * hf(m & 0xFFFFu);
+          wmax = fmaxf(wmax, wv[blk][i][0]);
           st.z[i] += p * hf(m >> 16);
         }
       } else {
         const float rho = hf(uint16_t(vm[blk][0]));
-        const float ps = p * rho * cS;
 #pragma unroll
         for (int pl = 0; pl < Ge::NPL; ++pl) {
-          const float x = ps * wP[pl];
-          const _Float16 hi = _Float16(x);
-          _Float16* w = pvw + pvwr[blk] + pvhead + pl;
-          w[0] = hi;
-          w[8] = _Float16(x - float(hi));
+          wv[blk][0][pl] = p * rho * cS * wP[pl];
+          wmax = fmaxf(wmax, wv[blk][0][pl]);
         }
         st.z[0] += p * rho * cZ;
       }
     }
     st.l = st.l * alpha + lsum;
-    // o columns belong to head n >> 2: fetch that head's alpha
-    {
-      const float al[4] = {__builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, alpha), 0)),
-                           __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, alpha), 16)),
-                           __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, alpha), 32)),
-                           __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, alpha), 48))};
-      if (al[0] != 1.0f || al[1] != 1.0f || al[2] != 1.0f || al[3] != 1.0f) {
-        const float av = al[hv];
+    // ---- the integer value sums hold weights of one scale and one running
+    // maximum: fold them into the float sums when the maximum moves or this
+    // record's weights would not fit 21 bits, and re-pick the scale
+    const bool flush = alpha != 1.0f || wmax * st.qw >= 2097152.0f;
+    if (__builtin_amdgcn_ballot_w64(flush) != 0) {
+      wmax = row_max16(wmax);
 #pragma unroll
-        for (int cb = 0; cb < 8; ++cb) st.o[cb] *= av;
+      for (int cb = 0; cb < 8; ++cb) {
+        st.of[cb] = (st.of[cb] + comb3(st.cv[cb]) * st.qwi) * alpha;
+        st.cv[cb] = int4v{0, 0, 0, 0};
       }
+      const int E = __builtin_amdgcn_frexp_expf(wmax);          // wmax = f 2^E, f in [0.5, 1)
+      const int e = wmax >= 1e-30f ? 19 - E : 100;
+      st.qw = ldexpf(1.0f, e);
+      st.qwi = ldexpf(1.0f, -e);
     }
-    // weights written above by other lanes of this wave are read below
-    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-
-    // ---- values: C[channel][column] += V codes (tokens) x weights
-    half8 Bp[Tr::NCV], Bl[Ge::LOPASS ? Tr::NCV : 1];
-#pragma unroll
-    for (int c = 0; c < Tr::NCV; ++c) {
-      Bp[c] = *reinterpret_cast<const half8*>(pvw + (vused ? c * Ge::CHB : 0) + pvrd);
-      if constexpr (Ge::LOPASS) Bl[c] = *reinterpret_cast<const half8*>(pvw + Ge::PASSB + c * Ge::CHB + pvrd);
-    }
+    // ---- values: C[(h, byte)][channel] += weights (tokens) x V codes, one
+    // value group's int8 weights (byte s of rint(w qw) in row 4r + s) at a time
+    int4v Aw[Tr::NCV];
 #pragma unroll
     for (int cb = 0; cb < 8; ++cb) {
-      if (cb + 1 < 8) chunk_operands<BASE, L, S, VFULL, Tr::VSEGW, Tr::NSV, Tr::NCV>(vseg[cb + 1], vmask, lut, Av[(cb + 1) & 1]);
+      constexpr int CPG = BASE == 0 ? G / 16 : 8;          // channel blocks per value group
+      if (cb % CPG == 0) {
+        const int gv = cb / CPG;
+#pragma unroll
+        for (int blk = 0; blk < 4; ++blk)
+#pragma unroll
+          for (int pl = 0; pl < Ge::NPL; ++pl) {
+            const uint32_t q = uint32_t(rintf(wv[blk][gv][pl] * st.qw));   // < 2^21
+            uint8_t* w = pvw + pvwr[blk] + pl;
+            w[0] = uint8_t(q >> 14);
+            w[16] = uint8_t((q >> 7) & 127u);
+            w[32] = uint8_t(q & 127u);
+          }
+        // weights written above by other lanes of this wave are read below
+        __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+#pragma unroll
+        for (int c = 0; c < Tr::NCV; ++c) {
+          const uint4 v = *reinterpret_cast<const uint4*>(pvw + c * Ge::CHB + kg * 256 + n * 16);
+          Aw[c] = __builtin_bit_cast(int4v, uint4v{v.x, v.y, v.z, v.w});
+        }
+      }
+      if (cb + 1 < 8) chunk_operands<BASE, L, S, VFULL, Tr::VSEGW, Tr::NSV, Tr::NCV>(vseg[cb + 1], vmask, lut, Bv[(cb + 1) & 1]);
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-      for (int ch = 0; ch < Tr::NCV; ++ch) st.o[cb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(Av[cb & 1][ch], Bp[ch], st.o[cb], 0, 0, 0);
-      if constexpr (Ge::LOPASS) {
-#pragma unroll
-        for (int ch = 0; ch < Tr::NCV; ++ch) st.o[cb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(Av[cb & 1][ch], Bl[ch], st.o[cb], 0, 0, 0);
-      }
+      for (int c = 0; c < Tr::NCV; ++c) st.cv[cb] = __builtin_amdgcn_mfma_i32_16x16x64_i8(Aw[c], Bv[cb & 1][c], st.cv[cb], 0, 0, 0);
       __builtin_amdgcn_sched_barrier(0);
     }
     // the next record replaces this one in the wave's buffer (LDS serves a
@@ -805,42 +863,33 @@ __device__ void run_pool(const DecodeArgs& a, Shared<PL>& sm, WaveState<PL::NGV>
   }
 }
 
-// A wave's state in merged form: sums over the tokens of a row, low columns
-// folded into high ones, the zero-point term added.
+// A wave's state in merged form: sums over the tokens of a row, the integer
+// value sums folded in, the zero-point term added.  Lane (n, r) holds head r
+// at channels 16 cb + n.
 template <int BASE, int G, class PL>
 __device__ void wave_finish(Shared<PL>& sm, WaveState<PL::NGV>& st) {
-  using Ge = typename PL::GH;
+  constexpr int NGV = PL::NGV;
   const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
-  const int n = lane & 15, r = lane >> 4, hs = r, hv = n >> 2, gg = n & 3;
+  const int n = lane & 15, r = lane >> 4;
   st.l = row_sum16(st.l);
 #pragma unroll
-  for (int i = 0; i < Ge::NGV; ++i) st.z[i] = row_sum16(st.z[i]);
-  if constexpr (!Ge::LOPASS) {
-#pragma unroll
-    for (int cb = 0; cb < 8; ++cb)
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-        st.o[cb][i] += Ge::NGV == 1 ? dpp<0xB1>(st.o[cb][i]) : dpp<0x4E>(st.o[cb][i]);   // quad xor 1 / xor 2
-  }
+  for (int i = 0; i < NGV; ++i) st.z[i] = row_sum16(st.z[i]);
   if (n == 0) {
 #pragma unroll
-    for (int i = 0; i < Ge::NGV; ++i) sm.zc[wave][hs][i] = st.z[i];
+    for (int i = 0; i < NGV; ++i) sm.zc[wave][r][i] = st.z[i];
   }
   __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
   __builtin_amdgcn_wave_barrier();
   Fin* f = wave_fin(sm, wave);
   if (n == 0) {
-    f->m[hs] = st.m;
-    f->l[hs] = st.l;
+    f->m[r] = st.m;
+    f->l[r] = st.l;
   }
 #pragma unroll
-  for (int cb = 0; cb < 8; ++cb)
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int ch = 16 * cb + 4 * r + i;
-      const bool mine = BASE == 0 ? (ch / G == gg) : (gg == 0);
-      if (mine) f->o[hv][ch] = st.o[cb][i] * kDigitScale + sm.zc[wave][hv][BASE == 0 ? gg : 0];
-    }
+  for (int cb = 0; cb < 8; ++cb) {
+    const int ch = 16 * cb + n;
+    f->o[r][ch] = st.of[cb] + comb3(st.cv[cb]) * st.qwi + sm.zc[wave][r][BASE == 0 ? ch / G : 0];
+  }
 }
 
 // Partials cross workgroups (and XCDs, whose L2 caches are not coherent with
@@ -1079,31 +1128,17 @@ __global__ __launch_bounds__((Plan<BASE, LH, LL, G>::NT)) void decode_kernel(Dec
       xr = ((sw[c >> 5] >> (c & 31)) & 1u) ? -x : x;
     }
     sm.qf[h][c] = xr;
-    sm.qh[h][c] = _Float16(x);
-    if (c < kQPad - kD) {
-      sm.qf[h][kD + c] = 0.0f;
-      sm.qh[h][kD + c] = _Float16(0.0f);
-    }
+    if (c < kQPad - kD) sm.qf[h][kD + c] = 0.0f;
+    if (BASE == 0) query_runs(x, h, c, sm);   // affine: from the query as loaded
   }
   __syncthreads();
-  if (BASE == 1)                            // rotate: H (sign . q)
+  if (BASE == 1) {                          // rotate: H (sign . q), then its runs
     for (int hs = 1; hs < kD; hs <<= 1) fwht_stage(sm.qf, hs);
-  if (qt) {
-    // per head: sums of the query over aligned runs of SEG channels (the
-    // query threads are whole waves)
-    constexpr int SEG = (BASE == 0 && G < 64) ? G : 64;
-    static_assert(SEG == 32 || SEG == 64, "query runs");
-    const float x = row_sum16(sm.qf[h][c]);
-    const float r0 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), 0));
-    const float r1 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), 16));
-    const float r2 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), 32));
-    const float r3 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), 48));
-    if (SEG == 64 && (c & 63) == 0) sm.zpart[h][c / 64] = (r0 + r1) + (r2 + r3);
-    if (SEG == 32 && (c & 63) == 0) sm.zpart[h][c / 32] = r0 + r1;
-    if (SEG == 32 && (c & 63) == 32) sm.zpart[h][c / 32] = r2 + r3;
+    if (qt) query_runs(sm.qf[h][c], h, c, sm);
+    __syncthreads();
   }
-  build_aq<BASE, LH, G, 0>(a, sm);
-  build_aq<BASE, LL, G, 1>(a, sm);
+  build_aq<BASE, LH, G, 0, 0>(a, sm);
+  build_aq<BASE, LL, G, 1, PL::GH::NG * PL::NCKH * 64>(a, sm);
   __syncthreads();
 
   // ---- this wave's records
@@ -1112,8 +1147,12 @@ __global__ __launch_bounds__((Plan<BASE, LH, LL, G>::NT)) void decode_kernel(Dec
   st.l = 0.0f;
 #pragma unroll
   for (int i = 0; i < PL::NGV; ++i) st.z[i] = 0.0f;
+  st.qw = st.qwi = 1.0f;
 #pragma unroll
-  for (int cb = 0; cb < 8; ++cb) st.o[cb] = float4v{0, 0, 0, 0};
+  for (int cb = 0; cb < 8; ++cb) {
+    st.of[cb] = 0.0f;
+    st.cv[cb] = int4v{0, 0, 0, 0};
+  }
   if (count > 0) store_pieces(R, sm.stage[wave], lane);
   if (nhi > 0) run_pool<BASE, LH, LL, G, 0>(a, sm, st, unit, nt0, first, stride, 0, nhi, count, R);
   if (count > nhi) run_pool<BASE, LH, LL, G, 1>(a, sm, st, unit, nt0, first, stride, nhi, count, count, R);
@@ -1199,10 +1238,13 @@ int launch_g(const DecodeArgs& a, hipStream_t st) {
 
 template <int BASE, int LH, int LL>
 int launch_dec(const DecodeArgs& a, hipStream_t st) {
-  if constexpr (BASE == 1) return launch_g<BASE, LH, LL, 128>(a, st);
-  if (a.g.G == 128) return launch_g<BASE, LH, LL, 128>(a, st);
-  if (a.g.G == 64) return launch_g<BASE, LH, LL, 64>(a, st);
-  return launch_g<BASE, LH, LL, 32>(a, st);
+  if constexpr (BASE == 1) {
+    return launch_g<BASE, LH, LL, 128>(a, st);
+  } else {
+    if (a.g.G == 128) return launch_g<BASE, LH, LL, 128>(a, st);
+    if (a.g.G == 64) return launch_g<BASE, LH, LL, 64>(a, st);
+    return launch_g<BASE, LH, LL, 32>(a, st);
+  }
 }
 
 template <int BASE, int LH, int LL>

@@ -62,7 +62,6 @@ def test_sizes_match_the_format(abi):
 @pytest.mark.parametrize("bad,status", [
     (dict(head_dim=64), -2), (dict(n_q_heads=16), -2), (dict(block=32), -2), (dict(L_hi=7), -2),
     (dict(base=1, L_hi=6, L_lo=5), -2), (dict(base=1, L_hi=4, L_lo=3, group=32), -2), (dict(group=16), -2),
-    (dict(L_hi=6, L_lo=3, group=32), -2),   # its 8-wave decode workgroup does not fit the LDS
     (dict(r_num=3, r_den=2), -1), (dict(r_den=0), -1), (dict(batch=0), -1), (dict(max_prompt=-1), -1)])
 def test_config_validation(abi, bad, status):
     s = abi.Sizes()
