@@ -2,82 +2,116 @@
 //
 // One 1024-thread workgroup per sequence.  Scores become order-preserving
 // 32-bit keys (-0 taken as +0); a 4-pass 8-bit radix select finds the K-th
-// largest key and how many of the keys equal to it are taken; equal keys are
-// taken by increasing token index (block-wide prefix counts).  A second scan
-// compacts the flagged and unflagged token indices into ascending slot lists.
+// largest key theta and how many of the keys equal to it are taken (equal
+// keys are taken by increasing token index).  Importance scores are heavily
+// tied (integer Zipf draws, peaked accumulated-attention weights), so the
+// histogram passes put most keys of a wave in one bin: each wave keeps its
+// own histogram and adds its most common bin with a single atomic.  The
+// flag and compaction pass then stages the keys through LDS in segments,
+// loaded coalesced, so that each thread owns a contiguous run of 16 tokens:
+// block-wide prefix counts give every token its tie rank and its slot in the
+// ascending high and low slot lists.
 #include "semkv_internal.h"
 
 namespace semkv {
 namespace {
 
 constexpr int kThreads = 1024;
+constexpr int kWaves = kThreads / 64;
+constexpr int kRun = 16;                     // tokens per thread in a segment
+constexpr int kSeg = kThreads * kRun;        // tokens per LDS segment
+constexpr int kBatch = 8;                    // score loads in flight per thread
 
 __device__ inline uint32_t order_key(float v) {
   uint32_t u = __float_as_uint(v == 0.0f ? 0.0f : v);
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
-// exclusive prefix sum over the workgroup; returns this thread's prefix and
-// writes the total to *total
-__device__ int64_t block_exclusive_scan(int64_t v, int64_t* wsum, int64_t* total) {
-  int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  int64_t x = v;
+// exclusive prefix sum over the workgroup of one value per thread; returns
+// this thread's prefix and the total
+__device__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* wsum, uint32_t* total) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  uint32_t x = v;
 #pragma unroll
   for (int d = 1; d < 64; d <<= 1) {
-    int64_t y = __shfl_up(x, d);
+    const uint32_t y = __shfl_up(x, d);
     if (lane >= d) x += y;
   }
   if (lane == 63) wsum[wave] = x;
   __syncthreads();
-  if (threadIdx.x == 0) {
-    int64_t run = 0;
-    for (int w = 0; w < kThreads / 64; ++w) {
-      int64_t t = wsum[w];
-      wsum[w] = run;
-      run += t;
+  if (wave == 0) {
+    uint32_t w = lane < kWaves ? wsum[lane] : 0u, s = w;
+#pragma unroll
+    for (int d = 1; d < kWaves; d <<= 1) {
+      const uint32_t y = __shfl_up(s, d);
+      if (lane >= d) s += y;
     }
-    wsum[kThreads / 64] = run;
+    if (lane < kWaves) wsum[lane] = s - w;
+    if (lane == kWaves - 1) wsum[kWaves] = s;
   }
   __syncthreads();
-  int64_t r = wsum[wave] + x - v;
-  *total = wsum[kThreads / 64];
+  const uint32_t r = wsum[wave] + x - v;
+  *total = wsum[kWaves];
   __syncthreads();
   return r;
 }
 
 __global__ __launch_bounds__(kThreads) void rank_kernel(RankArgs a) {
-  __shared__ uint32_t hist[256];
+  __shared__ uint32_t hist[kWaves][256];
+  __shared__ alignas(16) uint32_t keys[kSeg];
+  __shared__ uint32_t wsum[kWaves + 1];
   __shared__ uint32_t s_prefix;
   __shared__ int64_t s_krem;
-  __shared__ int64_t wsum[kThreads / 64 + 1];
-  const int b = blockIdx.x, tid = threadIdx.x;
+  const int b = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const float* s = a.scores + int64_t(b) * a.ld_s;
   const int64_t T = a.T, K = a.K;
 
+  // ---- radix select of the K-th largest key, 8 bits per pass
   bool nan_seen = false;
   uint32_t prefix = 0, pmask = 0;
   int64_t krem = K;
   if (K > 0) {
     for (int d = 3; d >= 0; --d) {
-      for (int i = tid; i < 256; i += kThreads) hist[i] = 0;
+      for (int i = tid; i < kWaves * 256; i += kThreads) (&hist[0][0])[i] = 0u;
       __syncthreads();
-      for (int64_t i = tid; i < T; i += kThreads) {
-        float v = s[i];
-        nan_seen |= isnan(v);
-        uint32_t k = order_key(v);
-        if ((k & pmask) == prefix) atomicAdd(&hist[(k >> (8 * d)) & 255u], 1u);
+      for (int64_t i0 = 0; i0 < T; i0 += kBatch * kThreads) {
+        float v[kBatch];                     // all loads of the batch in flight at once
+#pragma unroll
+        for (int j = 0; j < kBatch; ++j) {
+          const int64_t i = i0 + j * kThreads + tid;
+          v[j] = i < T ? s[i] : 0.0f;
+        }
+#pragma unroll
+        for (int j = 0; j < kBatch; ++j) {
+          const int64_t i = i0 + j * kThreads + tid;
+          nan_seen |= i < T && isnan(v[j]);
+          const uint32_t k = order_key(v[j]);
+          const bool in = i < T && (k & pmask) == prefix;
+          const uint32_t bin = (k >> (8 * d)) & 255u;
+          const uint64_t act = __ballot(in);
+          if (act != 0) {
+            // the wave's first counted key's bin in one atomic, the rest singly
+            const int lead = __builtin_ctzll(act);
+            const uint32_t b0 = __shfl(bin, lead);
+            const uint64_t same = __ballot(in && bin == b0);
+            if (lane == lead) atomicAdd(&hist[wave][b0], uint32_t(__popcll(same)));
+            if (in && bin != b0) atomicAdd(&hist[wave][bin], 1u);
+          }
+        }
       }
       __syncthreads();
-      if (tid == 0) {
-        int64_t cum = 0;
-        for (int bin = 255; bin >= 0; --bin) {
-          if (cum + hist[bin] >= krem) {
-            s_prefix = prefix | (uint32_t(bin) << (8 * d));
-            s_krem = krem - cum;
-            break;
-          }
-          cum += hist[bin];
-        }
+      // bin counts over the waves, then the bin holding the krem-th largest
+      // key: thread t < 256 takes bin 255 - t (descending key order)
+      uint32_t cnt = 0;
+      if (tid < 256) {
+#pragma unroll
+        for (int w = 0; w < kWaves; ++w) cnt += hist[w][255 - tid];
+      }
+      uint32_t total;
+      const uint32_t above = block_exclusive_scan(cnt, wsum, &total);   // keys in higher bins
+      if (tid < 256 && int64_t(above) < krem && int64_t(above) + cnt >= krem) {
+        s_prefix = prefix | (uint32_t(255 - tid) << (8 * d));
+        s_krem = krem - above;
       }
       __syncthreads();
       prefix = s_prefix;
@@ -87,44 +121,60 @@ __global__ __launch_bounds__(kThreads) void rank_kernel(RankArgs a) {
     }
   }
   if (nan_seen) atomicOr(a.status, 1);
-  // theta = prefix; keys > theta are taken, and the first krem keys == theta
+  // keys above theta are taken, and the first `ties` keys equal to it
   const uint32_t theta = prefix;
-  const int64_t ties = K > 0 ? krem : 0;
-  auto taken = [&](uint32_t k, int64_t tie_rank) {
-    return K > 0 && (k > theta || (k == theta && tie_rank < ties));
-  };
+  const uint32_t ties = K > 0 ? uint32_t(krem) : 0u;
 
-  // chunks of whole flag words, one per thread, in index order
-  const int64_t chunk = ((T + kThreads - 1) / kThreads + 31) / 32 * 32;
-  const int64_t lo_i = int64_t(tid) * chunk, hi_i = lo_i + chunk < T ? lo_i + chunk : T;
-  int64_t nt = 0;
-  for (int64_t i = lo_i; i < hi_i; ++i) nt += order_key(s[i]) == theta ? 1 : 0;
-  int64_t tot;
-  int64_t tie_base = block_exclusive_scan(nt, wsum, &tot);
-  int64_t nflag = 0, tr = tie_base;
-  for (int64_t w0 = lo_i; w0 < hi_i; w0 += 32) {
-    uint32_t word = 0;
-    for (int e = 0; e < 32 && w0 + e < hi_i; ++e) {
-      uint32_t k = order_key(s[w0 + e]);
-      bool f = taken(k, tr);
-      tr += k == theta ? 1 : 0;
-      word |= f ? (1u << e) : 0u;
-      nflag += f ? 1 : 0;
-    }
-    a.flags[int64_t(b) * a.flag_words + (w0 >> 5)] = word;
-  }
-  int64_t hi_base = block_exclusive_scan(nflag, wsum, &tot);
-  int64_t lo_base = lo_i - hi_base;
-  if (lo_i > T) lo_base = 0;
-  tr = tie_base;
+  // ---- flags and ascending slot lists, one LDS segment of kSeg keys at a time
   int32_t* hi_out = a.hi_idx + int64_t(b) * K;
   int32_t* lo_out = a.lo_idx + int64_t(b) * (T - K);
-  for (int64_t i = lo_i; i < hi_i; ++i) {
-    uint32_t k = order_key(s[i]);
-    bool f = taken(k, tr);
-    tr += k == theta ? 1 : 0;
-    if (f) hi_out[hi_base++] = int32_t(i);
-    else lo_out[lo_base++] = int32_t(i);
+  uint32_t run_tie = 0, run_hi = 0;          // before this segment (T < 2^29)
+  for (int64_t seg0 = 0; seg0 < T; seg0 += kSeg) {
+    const int n = T - seg0 < kSeg ? int(T - seg0) : kSeg;
+#pragma unroll
+    for (int j = 0; j < kRun; ++j) {
+      const int i = j * kThreads + tid;
+      if (i < n) keys[i] = order_key(s[seg0 + i]);
+    }
+    __syncthreads();
+    // this thread's run of 16 keys, in registers (keys past n are not used)
+    const int r0 = tid * kRun, nr = n - r0 < 0 ? 0 : (n - r0 < kRun ? n - r0 : kRun);
+    uint32_t kr[kRun];
+#pragma unroll
+    for (int j = 0; j < kRun / 4; ++j) {
+      const uint4 q = reinterpret_cast<const uint4*>(keys + r0)[j];
+      kr[4 * j] = q.x;
+      kr[4 * j + 1] = q.y;
+      kr[4 * j + 2] = q.z;
+      kr[4 * j + 3] = q.w;
+    }
+    uint32_t nt = 0;
+#pragma unroll
+    for (int j = 0; j < kRun; ++j) nt += (j < nr && kr[j] == theta) ? 1u : 0u;
+    uint32_t tot_tie;
+    uint32_t tr = run_tie + block_exclusive_scan(nt, wsum, &tot_tie);   // tie rank of the run's first tie
+    uint32_t bits = 0, nf = 0;
+#pragma unroll
+    for (int j = 0; j < kRun; ++j) {
+      const uint32_t k = kr[j];
+      const bool f = j < nr && K > 0 && (k > theta || (k == theta && tr < ties));
+      tr += (j < nr && k == theta) ? 1u : 0u;
+      bits |= f ? 1u << j : 0u;
+      nf += f ? 1u : 0u;
+    }
+    // a flag word is the runs of two neighbouring lanes (kRun = 16)
+    const uint32_t other = __shfl_xor(bits, 1);
+    if ((tid & 1) == 0 && nr > 0) a.flags[int64_t(b) * a.flag_words + ((seg0 + r0) >> 5)] = bits | (other << 16);
+    uint32_t tot_hi;
+    uint32_t hb = run_hi + block_exclusive_scan(nf, wsum, &tot_hi);
+    uint32_t lb = uint32_t(seg0 + r0) - hb;
+    for (int j = 0; j < nr; ++j) {
+      if ((bits >> j) & 1u) hi_out[hb++] = int32_t(seg0 + r0 + j);
+      else lo_out[lb++] = int32_t(seg0 + r0 + j);
+    }
+    run_tie += tot_tie;
+    run_hi += tot_hi;
+    __syncthreads();
   }
 }
 
