@@ -58,6 +58,14 @@ __device__ inline void load_quarter(const uint16_t* src, float x[32], bool& nonf
   nonfinite |= big.x >= 0x7C00u || big.y >= 0x7C00u;
 }
 
+// The value of lane (this lane xor 1), xor 2, or of lane 0 of this lane's
+// quad: exact DPP moves within a quad at full VALU rate.
+template <int CTRL>
+__device__ inline float quad_mov(float x) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), CTRL, 0xF, 0xF, false));
+}
+constexpr int kQuadXor1 = 0xB1, kQuadXor2 = 0x4E, kQuadLane0 = 0x00;
+
 // Asymmetric affine quantizer (Sec. 4.1) of one row quarter; the min/max of a
 // group of G channels is combined over the G/32 lanes holding it.  Returns
 // {scale, zero} as fp16 bits (low half = scale).
@@ -70,12 +78,12 @@ __device__ uint32_t affine_quarter(const float x[32], int G, uint32_t code[8]) {
     mx = fmaxf(mx, x[i]);
   }
   if (G >= 64) {
-    mn = fminf(mn, __shfl_xor(mn, 1));
-    mx = fmaxf(mx, __shfl_xor(mx, 1));
+    mn = fminf(mn, quad_mov<kQuadXor1>(mn));
+    mx = fmaxf(mx, quad_mov<kQuadXor1>(mx));
   }
   if (G >= 128) {
-    mn = fminf(mn, __shfl_xor(mn, 2));
-    mx = fmaxf(mx, __shfl_xor(mx, 2));
+    mn = fminf(mn, quad_mov<kQuadXor2>(mn));
+    mx = fmaxf(mx, quad_mov<kQuadXor2>(mx));
   }
   float zero = mn + 0.0f;                               // -0 -> +0
   uint16_t s16 = f2h(__fdiv_rn(mx - mn, float(L - 1)));
@@ -118,28 +126,30 @@ __device__ uint16_t tq_quarter(const float x[32], int q, const uint32_t* sw, con
         u[i] = p + r;
         u[i + h] = p - r;
       }
+  // cross-lane stages: the upper lane of a pair takes o - u = o + (-u), the
+  // lower u + o = o + u (IEEE addition commutes; -u is a sign flip)
+  const uint32_t f1 = (q & 1) ? 0x80000000u : 0u, f2 = (q & 2) ? 0x80000000u : 0u;
 #pragma unroll
   for (int i = 0; i < 32; ++i) {                         // h = 32: partner lane q ^ 1
-    float o = __shfl_xor(u[i], 1);
-    u[i] = (q & 1) ? o - u[i] : u[i] + o;
+    const float o = quad_mov<kQuadXor1>(u[i]);
+    u[i] = o + __uint_as_float(__float_as_uint(u[i]) ^ f1);
   }
 #pragma unroll
   for (int i = 0; i < 32; ++i) {                         // h = 64: partner lane q ^ 2
-    float o = __shfl_xor(u[i], 2);
-    u[i] = (q & 2) ? o - u[i] : u[i] + o;
+    const float o = quad_mov<kQuadXor2>(u[i]);
+    u[i] = o + __uint_as_float(__float_as_uint(u[i]) ^ f2);
   }
 #pragma unroll
-  for (int i = 0; i < 32; ++i) a[i] = a[i] + __shfl_xor(a[i], 2);   // h = 64 (lanes 0,1 keep)
+  for (int i = 0; i < 32; ++i) a[i] = a[i] + quad_mov<kQuadXor2>(a[i]);   // h = 64 (lanes 0,1 keep)
 #pragma unroll
-  for (int i = 0; i < 32; ++i) a[i] = a[i] + __shfl_xor(a[i], 1);   // h = 32 (lane 0 keeps)
+  for (int i = 0; i < 32; ++i) a[i] = a[i] + quad_mov<kQuadXor1>(a[i]);   // h = 32 (lane 0 keeps)
 #pragma unroll
   for (int h = 16; h >= 1; h >>= 1)
 #pragma unroll
     for (int i = 0; i < h; ++i) a[i] = a[i] + a[i + h];
   uint16_t r16 = f2h(sqrt_rn(a[0]));
   if ((r16 & 0x7FFFu) == 0x7C00u) r16 = 0x7BFFu;       // saturate to 65504
-  int lane = __lane_id();
-  r16 = uint16_t(__shfl(int(r16), lane & ~3));
+  r16 = uint16_t(__float_as_uint(quad_mov<kQuadLane0>(__uint_as_float(uint32_t(r16)))));
   float rf = h2f(r16);
   float thr[L - 1];
 #pragma unroll
