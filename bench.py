@@ -134,7 +134,8 @@ def cpu_baseline(cfgw, seconds):
 def generation(cfgw, cache, gen, dev, outlier_ch):
     """Generated tokens under block-wise deferred allocation (Alg. 2): per
     token, every layer appends its fp16 K/V to the tail and attends over the
-    pools and the tail; then the token's score is committed, and every 64th
+    pools and the tail (one fused launch per layer); then the token's score is
+    committed, and every 64th
     commit closes the block (in-block ranking, quantize + pack of the 64 rows
     onto the pool ends).  Each block is captured as two HIP graphs -- its 64
     tokens without the last commit, and that commit with the close -- and
@@ -171,8 +172,7 @@ def generation(cfgw, cache, gen, dev, outlier_ch):
             with torch.cuda.graph(g_steps, stream=s):
                 for i in range(b0, b0 + blk):
                     for l in range(nL):
-                        cache.append_kv(l, kn[i, l], vn[i, l])
-                        cache.decode_attn(l, qg[i, l], out=out[l], workspace=ws)
+                        cache.append_decode_attn(l, kn[i, l], vn[i, l], qg[i, l], out=out[l], workspace=ws)
                     if i + 1 < b0 + blk:
                         cache.append_commit(sg[i])
             with torch.cuda.graph(g_close, stream=s):
@@ -212,7 +212,7 @@ def generation(cfgw, cache, gen, dev, outlier_ch):
         "close_us": round(close_us, 2), "close_gbps": round((close_in + close_out) / (close_us * 1e-6) / 1e9, 1),
         "close_bytes": int(close_in + close_out), "blocks": len(graphs),
         "rows_hi": cache.c.n_hi, "rows_lo": cache.c.n_lo,
-        "note": "per token: append + decode of every layer, then commit; every 64th commit closes the block",
+        "note": "per token: fused append + decode of every layer, then commit; every 64th commit closes the block",
     }
 
 

@@ -186,6 +186,17 @@ int semkv_workspace_bytes(const semkv_cache* c, size_t* bytes);
 int semkv_decode_attn(const semkv_cache* c, int32_t layer, const uint16_t* q, float* out,
                       void* workspace, size_t ws_bytes, hipStream_t stream);
 
+/* Alg. 2, append and attend in one launch: store this layer's K and V of the
+ * current generated token in the fp16 tail (exactly as semkv_append_kv with
+ * this layer) and compute semkv_decode_attn over the cache including it.
+ * k_new, v_new: device fp16 [batch][n_kv_heads][128]; q, out, workspace as
+ * for semkv_decode_attn.  SEMKV_ESTATE if this layer already appended the
+ * current token or a block of 64 scores awaits its close; SEMKV_ECAPACITY
+ * past max_prompt + max_new tokens. */
+int semkv_append_decode(semkv_cache* c, int32_t layer, const uint16_t* k_new, const uint16_t* v_new,
+                        const uint16_t* q, float* out, void* workspace, size_t ws_bytes,
+                        hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

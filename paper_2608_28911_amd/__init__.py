@@ -128,6 +128,19 @@ class SemKVCache:
                                       ws.numel() * ws.element_size(), _stream()), "semkv_decode_attn")
         return out
 
+    def append_decode_attn(self, layer, k, v, q, out=None, workspace=None):
+        """Fused append + decode of one layer: k, v fp16 [B, H_kv, 128] (this
+        layer's new token), q fp16 [B, H_q, 128] -> fp32 [B, H_q, 128]."""
+        import torch
+        q = q.contiguous()
+        if out is None:
+            out = torch.empty(q.shape, dtype=torch.float32, device=q.device)
+        ws = self.workspace() if workspace is None else workspace
+        check(lib().semkv_append_decode(ctypes.byref(self.c), layer, _ptr(k.contiguous()), _ptr(v.contiguous()),
+                                        _ptr(q), _ptr(out), _ptr(ws), ws.numel() * ws.element_size(), _stream()),
+              "semkv_append_decode")
+        return out
+
     # -- state -------------------------------------------------------------
     @property
     def counts(self):

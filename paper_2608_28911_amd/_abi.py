@@ -50,6 +50,7 @@ EXPORTS = {
     "semkv_flush": (ctypes.c_int, [ctypes.POINTER(Cache), vp]),
     "semkv_workspace_bytes": (ctypes.c_int, [ctypes.POINTER(Cache), ctypes.POINTER(sz)]),
     "semkv_decode_attn": (ctypes.c_int, [ctypes.POINTER(Cache), i32, vp, vp, vp, sz, vp]),
+    "semkv_append_decode": (ctypes.c_int, [ctypes.POINTER(Cache), i32, vp, vp, vp, vp, vp, sz, vp]),
 }
 
 _lib = None

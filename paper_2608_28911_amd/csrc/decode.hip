@@ -1096,6 +1096,17 @@ __global__ __launch_bounds__((Plan<BASE, LH, LL, G>::NT)) void decode_kernel(Dec
   const int nhi = first < nt0 ? (nt0 - first + stride - 1) / stride : 0;
   const uint8_t* unit = g.pools + unit_offset(g, b, a.layer, kvh);
 
+  // ---- fused append (Alg. 2): the workgroup that attends over the fp16 tail
+  // first stores this layer's new K/V row in it, as its last row (read back
+  // by the same workgroup after the barriers below)
+  if (a.k_new != nullptr && split == a.nsplit - 1 && tid < 2 * kD / 2) {
+    const int kv = tid >> 6, w = tid & 63;                // 64 dwords each of K and V
+    const uint32_t* src = reinterpret_cast<const uint32_t*>((kv ? a.v_new : a.k_new) + (int64_t(b) * g.n_kv_heads + kvh) * kD);
+    uint32_t* dst = reinterpret_cast<uint32_t*>(
+        a.tail + ((((int64_t(b) * g.n_layers + a.layer) * g.n_kv_heads + kvh) * 2 + kv) * kSlots + (a.n_tail - 1)) * kD);
+    dst[w] = src[w];
+  }
+
   // ---- query and decode tables, then the first record in flight; the query
   // work takes the first 4 x 128 threads, one per (head, channel)
   const bool qt = tid < 4 * kD;

@@ -390,13 +390,12 @@ int semkv_workspace_bytes(const semkv_cache* c, size_t* bytes) {
   return SEMKV_OK;
 }
 
-int semkv_decode_attn(const semkv_cache* c, int32_t layer, const uint16_t* q, float* out,
-                      void* workspace, size_t ws_bytes, hipStream_t stream) {
-  if (!c || !q || !out || !workspace) return SEMKV_EINVAL;
+// Decode launch of one layer; with k_new/v_new, the launch also stores them
+// as the layer's current tail row (the fused append).
+static int decode_launch(const semkv_cache* c, int32_t layer, int n_tail, const uint16_t* k_new,
+                         const uint16_t* v_new, const uint16_t* q, float* out, void* workspace, size_t ws_bytes,
+                         hipStream_t stream) {
   const semkv_config& k = c->cfg;
-  if (layer < 0 || layer >= k.n_layers) return SEMKV_EINVAL;
-  if ((uintptr_t(q) & 3) || (uintptr_t(workspace) & 15)) return SEMKV_EINVAL;
-  int n_tail = c->n_scored + (((c->appended[layer >> 5] >> (layer & 31)) & 1u) ? 1 : 0);
   DecodeArgs a;
   memset(&a, 0, sizeof(a));
   const int nsplit = plan(c, n_tail);
@@ -404,6 +403,8 @@ int semkv_decode_attn(const semkv_cache* c, int32_t layer, const uint16_t* q, fl
   if (ws_bytes < workspace_need(k, nsplit)) return SEMKV_EINVAL;
   a.g = geom(c);
   a.tail = c->tail;
+  a.k_new = k_new;
+  a.v_new = v_new;
   a.q = q;
   a.counters = static_cast<uint32_t*>(workspace);
   a.ws = reinterpret_cast<float*>(static_cast<uint8_t*>(workspace) + counter_bytes(k));
@@ -416,6 +417,31 @@ int semkv_decode_attn(const semkv_cache* c, int32_t layer, const uint16_t* q, fl
   memcpy(a.mu[0], c->mu_hi, sizeof(a.mu[0]));
   memcpy(a.mu[1], c->mu_lo, sizeof(a.mu[1]));
   return launch_decode(a, stream);
+}
+
+int semkv_decode_attn(const semkv_cache* c, int32_t layer, const uint16_t* q, float* out,
+                      void* workspace, size_t ws_bytes, hipStream_t stream) {
+  if (!c || !q || !out || !workspace) return SEMKV_EINVAL;
+  const semkv_config& k = c->cfg;
+  if (layer < 0 || layer >= k.n_layers) return SEMKV_EINVAL;
+  if ((uintptr_t(q) & 3) || (uintptr_t(workspace) & 15)) return SEMKV_EINVAL;
+  const int n_tail = c->n_scored + (((c->appended[layer >> 5] >> (layer & 31)) & 1u) ? 1 : 0);
+  return decode_launch(c, layer, n_tail, nullptr, nullptr, q, out, workspace, ws_bytes, stream);
+}
+
+int semkv_append_decode(semkv_cache* c, int32_t layer, const uint16_t* k_new, const uint16_t* v_new,
+                        const uint16_t* q, float* out, void* workspace, size_t ws_bytes, hipStream_t stream) {
+  if (!c || !k_new || !v_new || !q || !out || !workspace) return SEMKV_EINVAL;
+  const semkv_config& k = c->cfg;
+  if (layer < 0 || layer >= k.n_layers) return SEMKV_EINVAL;
+  if ((uintptr_t(k_new) | uintptr_t(v_new) | uintptr_t(q)) & 3 || (uintptr_t(workspace) & 15)) return SEMKV_EINVAL;
+  if (((c->appended[layer >> 5] >> (layer & 31)) & 1u) != 0) return SEMKV_ESTATE;   // appended already
+  if (c->n_hi + c->n_lo + c->n_scored + 1 > k.max_prompt + k.max_new) return SEMKV_ECAPACITY;
+  if (c->n_scored >= kSlots) return SEMKV_ESTATE;
+  const int st = decode_launch(c, layer, c->n_scored + 1, k_new, v_new, q, out, workspace, ws_bytes, stream);
+  if (st) return st;
+  c->appended[layer >> 5] |= 1u << (layer & 31);
+  return SEMKV_OK;
 }
 
 }  // extern "C"

@@ -62,7 +62,9 @@ struct AppendArgs {
 
 struct DecodeArgs {
   PoolGeom g;
-  const uint16_t* tail;    // fp16 tail base
+  uint16_t* tail;          // fp16 tail base
+  const uint16_t* k_new;   // fused append: this layer's new K/V rows [b][kvh][128], or null
+  const uint16_t* v_new;
   const uint16_t* q;       // [b][Hq][128]
   float* ws;               // partials [b][kvh][nsplit][4][132]
   uint32_t* counters;      // [b][kvh] finished-split counters, zero between calls

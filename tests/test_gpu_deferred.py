@@ -90,3 +90,48 @@ def test_generation_on_the_turboquant_base():
 def test_generation_g32():
     cfgw = get_config(3, n_layers=1, batch=1, n_kv_heads=1, n_q_heads=4, group=32)
     run_generation(cfgw, 64, 64 * 3, check_steps={10, 100, 191})
+
+
+@pytest.mark.parametrize("wl", [3, 4])
+def test_fused_append_decode_matches_separate_calls(wl):
+    """semkv_append_decode (append and attend in one launch) gives the same
+    attention, bit for bit, as semkv_append_kv followed by semkv_decode_attn,
+    and leaves the same tail, pools and flags, across a block close."""
+    import torch
+    from paper_2608_28911_amd import SemKVError
+    cfgw = get_config(wl, n_layers=2, batch=2, n_kv_heads=2, n_q_heads=8)
+    T, n_gen = 150, 64 + 6
+    sep, fus = U.make_cache(cfgw, T, max_new=n_gen), U.make_cache(cfgw, T, max_new=n_gen)
+    for c in (sep, fus):
+        U.prefill(c, cfgw, T)
+    gen = {(b, l, h): synth.unit_gen_kv(cfgw, l, b, h, n_gen)
+           for b in range(cfgw.batch) for l in range(cfgw.n_layers) for h in range(cfgw.n_kv_heads)}
+    gscore = synth.gen_scores(cfgw, n_gen)
+    for i in range(n_gen):
+        for l in range(cfgw.n_layers):
+            k = torch.from_numpy(np.stack([np.stack([gen[(b, l, h)][0][i] for h in range(cfgw.n_kv_heads)])
+                                           for b in range(cfgw.batch)])).cuda()
+            v = torch.from_numpy(np.stack([np.stack([gen[(b, l, h)][1][i] for h in range(cfgw.n_kv_heads)])
+                                           for b in range(cfgw.batch)])).cuda()
+            q = torch.from_numpy(synth.query(cfgw, l, i)).cuda()
+            sep.append_kv(l, k, v)
+            want = sep.decode_attn(l, q)
+            got = fus.append_decode_attn(l, k, v, q)
+            assert torch.equal(got, want), "step %d layer %d" % (i, l)
+            if i == 0 and l == 0:
+                with pytest.raises(SemKVError):          # this layer appended the token already
+                    fus.append_decode_attn(l, k, v, q)
+        s = torch.from_numpy(gscore[i]).cuda()
+        sep.append_commit(s)
+        fus.append_commit(s)
+    torch.cuda.synchronize()
+    assert sep.status() == 0 and fus.status() == 0
+    assert (sep.c.n_hi, sep.c.n_lo, sep.c.n_scored) == (fus.c.n_hi, fus.c.n_lo, fus.c.n_scored)
+    assert torch.equal(sep.flags, fus.flags)
+    for b in range(cfgw.batch):
+        for l in range(cfgw.n_layers):
+            for h in range(cfgw.n_kv_heads):
+                for p, n in ((0, sep.c.n_hi), (1, sep.c.n_lo)):
+                    nt = -(-n // 64)
+                    assert torch.equal(sep.pool_bytes(b, l, h, p, nt), fus.pool_bytes(b, l, h, p, nt))
+    assert torch.equal(sep.tail.view(-1, 2, 64, 128)[:, :, :sep.c.n_scored], fus.tail.view(-1, 2, 64, 128)[:, :, :fus.c.n_scored])
