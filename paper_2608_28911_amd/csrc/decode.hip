@@ -1083,7 +1083,7 @@ __global__ __launch_bounds__((Plan<BASE, LH, LL, G>::NT)) void decode_kernel(Dec
   constexpr int NW = PL::NW, NT = PL::NT;
   __shared__ Shared<PL> sm;
   static_assert(sizeof(Shared<PL>) <= 160 * 1024, "LDS");
-  static_assert(NT == 4 * kD, "one thread per (head, channel) of the query and the output");
+  static_assert(NT >= 4 * kD, "one thread per (head, channel) of the query and the output");
   const int split = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
   const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
   const PoolGeom& g = a.g;
@@ -1222,7 +1222,7 @@ int waves_of() { return Plan<BASE, LH, LL, G>::NW; }
 // the kernel needs 4 x 128 threads (one per query head and channel): level
 // pairs whose 8-wave workgroup does not fit the LDS are not built
 template <int BASE, int LH, int LL, int G>
-constexpr bool fits() { return Plan<BASE, LH, LL, G>::NT == 4 * kD; }
+constexpr bool fits() { return Plan<BASE, LH, LL, G>::NT >= 4 * kD; }
 
 template <int BASE, int LH, int LL, int G>
 int occupancy() {

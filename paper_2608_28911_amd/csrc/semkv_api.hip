@@ -193,7 +193,7 @@ int semkv_cache_sizes(const semkv_config* cfg, semkv_sizes* out) {
   if (k.base == SEMKV_BASE_TQ && k.group != 128) return SEMKV_EUNSUPPORTED;
   // the decode kernel needs one 8-wave workgroup's tables and buffers in a
   // compute unit's LDS (6 and 3 levels with 32-channel groups do not fit)
-  if (decode_waves(k.base, k.L_hi, k.L_lo, k.group) != 8) return SEMKV_EUNSUPPORTED;
+  if (decode_waves(k.base, k.L_hi, k.L_lo, k.group) < 8) return SEMKV_EUNSUPPORTED;
   memset(out, 0, sizeof(*out));
   int64_t khi = top_count(k.max_prompt, k.r_num, k.r_den);
   int64_t hi_rows = khi + k.max_new, lo_rows = k.max_prompt - khi + k.max_new;
