@@ -10,7 +10,8 @@ library and never imports the product package.
 Record format (one 64-slot tile of a pool), bytes in order:
   K body  TB(L)   packed codes, a line = one token row of 128 channels
   V body  TB(L)   packed codes, a line = one channel column over the 64 slots
-  K meta  MB      affine: [128/G groups][64 slots] x (fp16 scale, fp16 zero)
+  K meta  MB      affine and rotated affine:
+                          [128/G groups][64 slots] x (fp16 scale, fp16 zero)
                   tq:     [64 slots] x fp16 rho
   V meta  MB      same
 """
@@ -57,6 +58,7 @@ def lib():
             "oq_affine_row": (i32, [P, i32, i32, P, P]),
             "oq_lloyd_max": (i32, [i32, P, P, P]),
             "oq_tq_row": (i32, [P, P, i32, P, P, P]),
+            "oq_rotaffine_row": (i32, [P, P, i32, i32, P, P]),
             "oq_quantize_rows": (i32, [P, i64, i32, i32, i32, P, P, P, P]),
             "oq_symbol_digits": (i32, [i32]),
             "oq_symbol_bits": (i32, [i32, i32]),
@@ -65,6 +67,7 @@ def lib():
             "oq_pack_tile": (i32, [P, P, i32, P, P]),
             "oq_affine_dequant_rows": (None, [P, P, i64, i32, P]),
             "oq_tq_dequant_rows": (None, [P, P, i64, P, P, P]),
+            "oq_rotaffine_dequant_rows": (None, [P, P, i64, i32, P, P]),
             "oq_attention": (None, [P, i32, P, P, i64, i32, P]),
             "oq_f32_to_f16_n": (None, [P, i64, P]),
             "oq_f16_to_f32_n": (None, [P, i64, P]),
@@ -159,15 +162,19 @@ def codebook32(L):
     return mu.astype(np.float32), tau.astype(np.float32)
 
 
+AFFINE, TQ, ROT_AFFINE = 0, 1, 2
+
+
 def quantize_rows(X, base, L, G=128, sign_words=None):
     """Rows of fp16 [n, 128] -> (codes uint8 [n,128], meta uint16).
-    meta: affine [n, 128/G, 2] (scale, zero bits); tq [n] (rho bits)."""
+    base 0 affine, 1 TurboQuant-MSE, 2 affine of the rotated row.
+    meta: affine / rotated affine [n, 128/G, 2] (scale, zero bits); tq [n] (rho bits)."""
     X = np.ascontiguousarray(X, dtype=np.float16).view(np.uint16)
     n = X.shape[0]
     codes = np.zeros((n, D), np.uint8)
-    if base == 0:
+    if base != TQ:
         meta = np.zeros((n, D // G, 2), np.uint16)
-        sw = np.zeros(4, np.uint32)
+        sw = np.zeros(4, np.uint32) if base == AFFINE else np.ascontiguousarray(sign_words, dtype=np.uint32)
         tau = np.zeros(1, np.float32)
     else:
         meta = np.zeros(n, np.uint16)
@@ -182,12 +189,17 @@ def dequantize_rows(codes, meta, base, L, G=128, sign_words=None) -> np.ndarray:
     """Fake-quantized values (float64 [n,128]); affine values are fp32 exact."""
     codes = np.ascontiguousarray(codes, np.uint8)
     n = codes.shape[0]
-    if base == 0:
+    if base == AFFINE:
         out = np.zeros((n, D), np.float32)
         if n:
             lib().oq_affine_dequant_rows(_p(codes), _p(np.ascontiguousarray(meta, np.uint16)), n, G, _p(out))
         return out.astype(np.float64)
     out = np.zeros((n, D), np.float64)
+    if base == ROT_AFFINE:
+        if n:
+            lib().oq_rotaffine_dequant_rows(_p(codes), _p(np.ascontiguousarray(meta, np.uint16)), n, G,
+                                            _p(np.ascontiguousarray(sign_words, np.uint32)), _p(out))
+        return out
     mu32 = np.ascontiguousarray(codebook32(L)[0])
     if n:
         lib().oq_tq_dequant_rows(_p(codes), _p(np.ascontiguousarray(meta, np.uint16)), n,
@@ -214,7 +226,7 @@ def tile_bytes(L) -> int:
 
 
 def meta_bytes(base, G=128) -> int:
-    return (D // G) * SLOTS * 4 if base == 0 else SLOTS * 2
+    return (D // G) * SLOTS * 4 if base != TQ else SLOTS * 2
 
 
 def record_bytes(base, L, G=128) -> int:
@@ -233,7 +245,7 @@ def pack_tile(kcodes, vcodes, L):
 
 def _meta_tile(meta, base, G, lo, hi):
     """Metadata of slots [lo, hi) in record order; unused slots are zero."""
-    if base == 0:
+    if base != TQ:
         m = np.zeros((D // G, SLOTS, 2), np.uint16)
         m[:, : hi - lo, :] = np.transpose(meta[lo:hi], (1, 0, 2))
     else:
@@ -352,7 +364,7 @@ class UnitCache:
     def pool(self, p):
         d = self.codes[p]
         cat = lambda xs, shape, dt: np.concatenate(xs) if xs else np.zeros(shape, dt)
-        mshape = (0, D // self.G, 2) if self.base == 0 else (0,)
+        mshape = (0, D // self.G, 2) if self.base != TQ else (0,)
         return (cat(d["k"], (0, D), np.uint8), cat(d["km"], mshape, np.uint16),
                 cat(d["v"], (0, D), np.uint8), cat(d["vm"], mshape, np.uint16),
                 cat(d["pos"], (0,), np.int64))
@@ -397,7 +409,7 @@ def effective_bits(n_hi, n_lo, base, L_hi, L_lo, G=128, n_layers=32, n_kv_heads=
     per-token precision flag spread over all layers, heads, K and V."""
     n = n_hi + n_lo
     code = (n_hi * line_bits(L_hi, D) + n_lo * line_bits(L_lo, D)) / (n * D)
-    meta = 32.0 / G if base == 0 else 16.0 / D
+    meta = 32.0 / G if base != TQ else 16.0 / D
     flag = 1.0 / (n_layers * n_kv_heads * 2 * D)
     return code, code + meta + flag
 

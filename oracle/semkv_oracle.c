@@ -6,6 +6,7 @@
  *   Alg. 2       block-exact deferred quantization            (Sec. 3.7)
  *   Sec. 4.1     affine base, two fp16 parameters, mixed-radix packing
  *   Sec. 4.9     TurboQuant-MSE base, one scalar per row, Lloyd-Max codes
+ *   Sec. 4.1/4.9 the affine base under a Hadamard rotation (rotated affine)
  * Build: gcc -O2 -ffp-contract=off -fno-fast-math -fopenmp (IEEE single on SSE).
  */
 #include "semkv_oracle.h"
@@ -219,17 +220,74 @@ int oq_tq_row(const uint16_t* x, const uint32_t* sign_words, int L, const float*
   return status;
 }
 
+/* ------------------------------------------- affine under a rotation -- */
+
+/* The affine quantizer applied to the rotated row y = H diag(sign) x / 16
+ * (Sec. 4.1: integer-level scalar quantization with a Hadamard rotation; Sec.
+ * 4.9: the per-row asymmetric affine quantizer under Hadamard rotation).  H is
+ * the unnormalized Sylvester matrix, so y is the orthonormal rotation of x
+ * scaled by sqrt(128)/16 = 1/sqrt(2): a power of two away from the orthogonal
+ * map, which the affine quantizer does not see apart from fp16 range.  The
+ * rotation is summed in fp32 in the order of oq_tq_row, then divided by 16
+ * (exact).  Per group of G rotated coordinates: zero = fp16(min y) (-0 taken
+ * as +0), scale = fp16(max(0, (max y - zero) / (L-1))), codes as in
+ * oq_affine_row with the stored parameters. */
+int oq_rotaffine_row(const uint16_t* x, const uint32_t* sign_words, int L, int G,
+                     uint8_t* codes, uint16_t* meta) {
+  if (L < 2 || L > 16 || G <= 0 || 128 % G) return OQ_EINVAL;
+  int status = OQ_OK;
+  float y[128];
+  for (int i = 0; i < 128; i++) {
+    float f = oq_f16_to_f32(x[i]);
+    if (!isfinite(f)) status = OQ_ENAN;
+    y[i] = sign_bit(sign_words, i) ? -f : f;
+  }
+  for (int h = 1; h < 128; h <<= 1)
+    for (int i = 0; i < 128; i++)
+      if (!(i & h)) {
+        float p = y[i], q = y[i + h];
+        y[i] = p + q;
+        y[i + h] = p - q;
+      }
+  for (int i = 0; i < 128; i++) y[i] = y[i] / 16.0f;
+  for (int g = 0; g < 128 / G; g++) {
+    float mn = INFINITY, mx = -INFINITY;
+    for (int j = g * G; j < (g + 1) * G; j++) {
+      if (y[j] < mn) mn = y[j];
+      if (y[j] > mx) mx = y[j];
+    }
+    uint16_t z16 = oq_f32_to_f16(mn);
+    if (z16 == 0x8000u) z16 = 0;
+    float zf = oq_f16_to_f32(z16);
+    float s32 = (mx - zf) / (float)(L - 1);
+    if (!(s32 > 0.0f)) s32 = 0.0f;            /* zero rounded above every value */
+    uint16_t s16 = oq_f32_to_f16(s32);
+    float sf = oq_f16_to_f32(s16);
+    float inv = sf == 0.0f ? 0.0f : 1.0f / sf;
+    meta[2 * g] = s16;
+    meta[2 * g + 1] = z16;
+    for (int j = g * G; j < (g + 1) * G; j++) {
+      float c = rintf((y[j] - zf) * inv);
+      if (!(c >= 0.0f)) c = 0.0f;
+      if (c > (float)(L - 1)) c = (float)(L - 1);
+      codes[j] = (uint8_t)c;
+    }
+  }
+  return status;
+}
+
 int oq_quantize_rows(const uint16_t* X, int64_t n, int base, int L, int G,
                      const uint32_t* sign_words, const float* tau32,
                      uint8_t* codes, uint16_t* meta) {
   int status = OQ_OK;
-  int ng = base == 0 ? 128 / G : 1;
-  if (base == 0 && (G <= 0 || 128 % G)) return OQ_EINVAL;
+  if (base < 0 || base > 2) return OQ_EINVAL;
+  int ng = base != 1 ? 128 / G : 1;
+  if (base != 1 && (G <= 0 || 128 % G)) return OQ_EINVAL;
 #pragma omp parallel for schedule(static) reduction(min : status)
   for (int64_t r = 0; r < n; r++) {
-    int st = base == 0
-        ? oq_affine_row(X + r * 128, L, G, codes + r * 128, meta + r * 2 * ng)
-        : oq_tq_row(X + r * 128, sign_words, L, tau32, codes + r * 128, meta + r);
+    int st = base == 0 ? oq_affine_row(X + r * 128, L, G, codes + r * 128, meta + r * 2 * ng)
+           : base == 1 ? oq_tq_row(X + r * 128, sign_words, L, tau32, codes + r * 128, meta + r)
+                       : oq_rotaffine_row(X + r * 128, sign_words, L, G, codes + r * 128, meta + r * 2 * ng);
     if (st < status) status = st;
   }
   return status;
@@ -334,6 +392,28 @@ void oq_tq_dequant_rows(const uint8_t* codes, const uint16_t* rho, int64_t n,
           y[i + h] = p - q;
         }
     for (int i = 0; i < 128; i++) out[r * 128 + i] = (sign_bit(sign_words, i) ? -y[i] : y[i]) / 128.0;
+  }
+}
+
+/* Inverse of the rotation: x = diag(sign) H (16 y) / 128 = diag(sign) H y / 8,
+ * with y = fmaf(c, scale, zero) in fp32 and the transform in double. */
+void oq_rotaffine_dequant_rows(const uint8_t* codes, const uint16_t* meta, int64_t n, int G,
+                               const uint32_t* sign_words, double* out) {
+  int ng = 128 / G;
+  for (int64_t r = 0; r < n; r++) {
+    double y[128];
+    for (int j = 0; j < 128; j++) {
+      const uint16_t* m = meta + (r * ng + j / G) * 2;
+      y[j] = (double)fmaf((float)codes[r * 128 + j], oq_f16_to_f32(m[0]), oq_f16_to_f32(m[1]));
+    }
+    for (int h = 1; h < 128; h <<= 1)
+      for (int i = 0; i < 128; i++)
+        if (!(i & h)) {
+          double p = y[i], q = y[i + h];
+          y[i] = p + q;
+          y[i + h] = p - q;
+        }
+    for (int i = 0; i < 128; i++) out[r * 128 + i] = (sign_bit(sign_words, i) ? -y[i] : y[i]) / 8.0;
   }
 }
 

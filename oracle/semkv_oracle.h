@@ -46,8 +46,15 @@ int oq_lloyd_max(int L, double* mu, double* tau, double* mse);
 int oq_tq_row(const uint16_t* x, const uint32_t* sign_words, int L, const float* tau32,
               uint8_t* codes, uint16_t* rho);
 
-/* Many rows at once (OpenMP across rows).  base 0 affine, 1 tq.
- * meta: affine [n][128/G][2] fp16 bits; tq [n] fp16 bits. */
+/* Affine base under a Hadamard rotation (Sec. 4.1, Sec. 4.9): the affine
+ * quantizer of y = H diag(sign) x / 16 (H the unnormalized Sylvester matrix),
+ * per group of G rotated coordinates; zero = fp16(min y), scale =
+ * fp16(max(0, (max y - zero) / (L-1))).  meta as oq_affine_row. */
+int oq_rotaffine_row(const uint16_t* x, const uint32_t* sign_words, int L, int G,
+                     uint8_t* codes, uint16_t* meta);
+
+/* Many rows at once (OpenMP across rows).  base 0 affine, 1 tq, 2 rotated
+ * affine.  meta: affine [n][128/G][2] fp16 bits; tq [n] fp16 bits. */
 int oq_quantize_rows(const uint16_t* X, int64_t n, int base, int L, int G,
                      const uint32_t* sign_words, const float* tau32,
                      uint8_t* codes, uint16_t* meta);
@@ -67,6 +74,11 @@ int oq_pack_tile(const uint8_t* kcodes, const uint8_t* vcodes, int L,
 void oq_affine_dequant_rows(const uint8_t* codes, const uint16_t* meta, int64_t n, int G, float* out);
 void oq_tq_dequant_rows(const uint8_t* codes, const uint16_t* rho, int64_t n,
                         const uint32_t* sign_words, const float* mu32, double* out);
+
+/* rotated affine: x = diag(sign) H y / 8, y = fmaf(c, scale, zero) in fp32,
+ * the transform in double. */
+void oq_rotaffine_dequant_rows(const uint8_t* codes, const uint16_t* meta, int64_t n, int G,
+                               const uint32_t* sign_words, double* out);
 
 /* Decode attention (the consumer of the cache, Sec. 3.1 / Alg. 1):
  * out[h] = softmax(q_h . k_t / sqrt(D)) . v over all n tokens, in double. */

@@ -154,3 +154,90 @@ def test_tq_norm_is_correctly_rounded_at_fp16_edges():
     sw = np.zeros(4, np.uint32)
     _, rho = O.quantize_rows(X, 1, 4, sign_words=sw)
     assert np.array_equal(np.asarray(rho, np.uint16).reshape(-1), correctly_rounded_norm_f16(X))
+
+
+def sign_vector(sw):
+    return np.array([-1.0 if (int(sw[i // 32]) >> (i % 32)) & 1 else 1.0 for i in range(128)])
+
+
+@pytest.mark.parametrize("L", [3, 5, 6])
+@pytest.mark.parametrize("G", [32, 128])
+def test_rotated_affine_is_affine_of_the_library_rotation(L, G):
+    """On rows whose rotation is exact in fp32 and fp16 (x on a 1/4 grid in
+    [-2, 2], so y = H diag(sign) x / 16 lies on a 1/64 grid within 16), the
+    rotated quantizer equals the pinned affine quantizer applied to y computed
+    with the library's dense Sylvester matrix (Sec. 4.1: affine codes under a
+    Hadamard rotation).  A dropped or misplaced sign, another scaling, another
+    Hadamard ordering or groups over the wrong coordinates all change the
+    codes or the parameters."""
+    rng = np.random.default_rng(100 + L * 10 + G)
+    H = scipy.linalg.hadamard(128).astype(np.float64)
+    n = 400
+    X = rng.integers(-8, 9, (n, 128)).astype(np.float64) / 4
+    X[:, [3, 40, 77, 100]] = rng.choice([-2.0, 2.0], (n, 4))
+    X[0] = 0.25                                                # one non-zero coordinate after H
+    X[1] = 0.0                                                 # all zero: scale 0
+    sw = rng.integers(0, 2**32, 4, dtype=np.uint64).astype(np.uint32)
+    Y = (X * sign_vector(sw)) @ H.T / 16
+    assert np.array_equal(Y.astype(np.float16).astype(np.float64), Y)
+    X16 = X.astype(np.float16)
+    codes, meta = O.quantize_rows(X16, O.ROT_AFFINE, L, G, sw)
+    rcodes, rmeta = O.quantize_rows(Y.astype(np.float16), O.AFFINE, L, G)
+    assert np.array_equal(codes, rcodes)
+    assert np.array_equal(meta, rmeta)
+    assert np.all(codes[1] == 0) and np.all(meta[1] == 0)
+
+
+def test_rotated_affine_dequantization_and_error_bound():
+    """x_hat = diag(sign) H y_hat / 8 with y_hat the affine reconstruction
+    (the pinned base-0 dequantization); by orthogonality of H / sqrt(128),
+    ||x - x_hat|| = sqrt(128)/8 ||y - y_hat||, and every rotated coordinate
+    is within half a step (plus fp16 rounding of the stored zero) of its
+    reconstruction."""
+    rng = np.random.default_rng(7)
+    H = scipy.linalg.hadamard(128).astype(np.float64)
+    X = rng.standard_normal((300, 128)).astype(np.float32)
+    X[:, [3, 40, 77, 100]] *= 10
+    X = X.astype(np.float16)
+    xf = X.astype(np.float64)
+    sw = rng.integers(0, 2**32, 4, dtype=np.uint64).astype(np.uint32)
+    sign = sign_vector(sw)
+    y = (xf * sign) @ H.T / 16
+    for L, G in ((5, 128), (6, 128), (6, 32), (3, 64)):
+        codes, meta = O.quantize_rows(X, O.ROT_AFFINE, L, G, sw)
+        yhat = O.dequantize_rows(codes, meta, O.AFFINE, L, G)
+        xhat = O.dequantize_rows(codes, meta, O.ROT_AFFINE, L, G, sw)
+        assert np.allclose(xhat, sign * (yhat @ H.T) / 8, rtol=0, atol=1e-12)
+        s = np.repeat(meta[:, :, 0].view(np.float16).astype(np.float64), G, axis=1)
+        z = np.repeat(meta[:, :, 1].view(np.float16).astype(np.float64), G, axis=1)
+        # zero is min y rounded to fp16: a value below it may sit up to that
+        # rounding under code 0; the top code may round the step down as well
+        slack = np.abs(z) * 2.0**-11 + s * L * 2.0**-11 + 1e-6 * np.abs(y)
+        assert np.all(np.abs(yhat - y) <= s / 2 + slack + 1e-12)
+        lhs = np.linalg.norm(xhat - xf, axis=1)
+        rhs = np.sqrt(128) / 8 * np.linalg.norm(yhat - y, axis=1)
+        assert np.allclose(lhs, rhs, rtol=1e-9, atol=1e-9)
+        # rotation spreads the outlier channels: far below the unrotated error
+        if G == 128:
+            c0, m0 = O.quantize_rows(X, O.AFFINE, L, G)
+            e0 = np.mean((O.dequantize_rows(c0, m0, O.AFFINE, L, G) - xf) ** 2)
+            assert np.mean((xhat - xf) ** 2) < 0.5 * e0
+
+
+def test_rotated_affine_nonfinite_and_sign_words():
+    X = np.zeros((2, 128), np.float16)
+    X[1, 5] = np.nan
+    with pytest.raises(O.OracleError):
+        O.quantize_rows(X, O.ROT_AFFINE, 6, 128, np.zeros(4, np.uint32))
+    # flipping every sign negates y: zero and scale follow the negated row
+    rng = np.random.default_rng(3)
+    Xr = (rng.integers(-8, 9, (50, 128)) / 4).astype(np.float16)
+    a = O.quantize_rows(Xr, O.ROT_AFFINE, 6, 128, np.zeros(4, np.uint32))
+    b = O.quantize_rows(-Xr, O.ROT_AFFINE, 6, 128, np.full(4, 0xFFFFFFFF, np.uint32))
+    assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1])
+    # the least fp16 subnormal in one channel rotates to +-2^-28 everywhere:
+    # the zero rounds to -0 in fp16 and is stored as +0 (Sec. 4.1 parameters)
+    Xs = np.zeros((4, 128), np.float16)
+    Xs[:, 9] = np.float16(2.0**-24)
+    c, m = O.quantize_rows(Xs, O.ROT_AFFINE, 5, 32, np.zeros(4, np.uint32))
+    assert np.all(m == 0) and np.all(c == 0)
