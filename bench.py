@@ -65,6 +65,9 @@ def parse():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="llama8b_kv_b1_t32768_affine")
     ap.add_argument("--group", type=int, default=None, help="override the affine metadata group")
+    ap.add_argument("--base", default=None, choices=["affine", "rot_affine"],
+                    help="override an affine workload's base (rot_affine: the affine quantizer of the "
+                         "Hadamard-rotated row)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="budget of the oracle sample")
     ap.add_argument("--no-generate", dest="generate", action="store_false",
@@ -79,7 +82,7 @@ def algorithmic_decode_bytes(cfgw, n_hi, n_lo):
     of every cached token (row-exact mixed-radix bits), their metadata, the
     query and the output."""
     from paper_2608_28911_amd.fmt import line_bits
-    meta = (128 // cfgw.group) * 4 if cfgw.base == "affine" else 2
+    meta = (128 // cfgw.group) * 4 if cfgw.base != "tq" else 2
     per_hi = 2 * line_bits(cfgw.L_hi, 128) / 8 + 2 * meta
     per_lo = 2 * line_bits(cfgw.L_lo, 128) / 8 + 2 * meta
     units = cfgw.batch * cfgw.n_kv_heads
@@ -93,7 +96,7 @@ def cpu_baseline(cfgw, seconds):
     from oracle import oracle as O
     from workloads import synth
     T = cfgw.prompt_len
-    base = 0 if cfgw.base == "affine" else 1
+    base = cfgw.base_id
     units, t_attn, t_quant, q_bytes = 0, 0.0, 0.0, 0
     s = synth.scores(cfgw, 0, T)
     flag, _, _ = O.rank(s, cfgw.r_num, cfgw.r_den)
@@ -103,7 +106,7 @@ def cpu_baseline(cfgw, seconds):
         l = units // cfgw.n_kv_heads
         K, V = synth.unit_kv(cfgw, l, 0, h, T)
         u = O.UnitCache(base, cfgw.L_hi, cfgw.L_lo, cfgw.group, cfgw.r_num, cfgw.r_den,
-                        sign_words=synth.sign_words(cfgw, l, h) if base else None)
+                        sign_words=synth.sign_words(cfgw, l, h) if cfgw.rotated else None)
         t0 = time.perf_counter()
         u.prefill(K, V, flag)
         u.records(0)
@@ -227,17 +230,21 @@ def main():
     from workloads import get_config, synth
 
     cfgw = get_config(args.workload)
-    if args.group:
+    if args.group or args.base:
         from dataclasses import replace
-        cfgw = replace(cfgw, group=args.group)
+        if args.base and cfgw.base == "tq":
+            sys.exit("--base applies to the affine workloads")
+        cfgw = replace(cfgw, group=args.group or cfgw.group, base=args.base or cfgw.base)
+        if cfgw.base == "rot_affine":
+            cfgw = replace(cfgw, name=cfgw.name.replace("_affine", "_rot_affine"))
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     B, H, Hq, T, nL = cfgw.batch, cfgw.n_kv_heads, cfgw.n_q_heads, cfgw.prompt_len, cfgw.n_layers
-    base = P.BASE_AFFINE if cfgw.base == "affine" else P.BASE_TQ
+    base = cfgw.base_id
     cfg = P.make_config(n_layers=nL, n_kv_heads=H, batch=B, base=base, L_hi=cfgw.L_hi, L_lo=cfgw.L_lo,
                         group=cfgw.group, r_num=cfgw.r_num, r_den=cfgw.r_den, max_prompt=T,
                         max_new=cfgw.n_gen if args.generate else 0)
-    signs = synth.all_sign_words(cfgw) if base == P.BASE_TQ else None
+    signs = synth.all_sign_words(cfgw) if cfgw.rotated else None
     cache = P.SemKVCache(cfg, sign_words=signs)
 
     # ---- synthetic inputs, resident in HBM

@@ -45,7 +45,7 @@ enum {
   SEMKV_ESTATE = -6        /* call out of order (e.g. commit before append)   */
 };
 
-enum { SEMKV_BASE_AFFINE = 0, SEMKV_BASE_TQ = 1 };
+enum { SEMKV_BASE_AFFINE = 0, SEMKV_BASE_TQ = 1, SEMKV_BASE_ROT_AFFINE = 2 };
 enum { SEMKV_STATUS_NAN_SCORE = 1, SEMKV_STATUS_NONFINITE_KV = 2, SEMKV_STATUS_BAD_INDEX = 4 };
 
 /* Configuration of one cache.
@@ -55,6 +55,13 @@ enum { SEMKV_STATUS_NAN_SCORE = 1, SEMKV_STATUS_NONFINITE_KV = 2, SEMKV_STATUS_B
  *          SEMKV_BASE_TQ -- TurboQuant-MSE: random-sign Hadamard rotation and a
  *          Lloyd-Max codebook of the unit Gaussian, one fp16 scalar (the row
  *          norm) per row (Sec. 4.9); L_hi, L_lo in {4, 3} (2.0/1.585 bits).
+ *          SEMKV_BASE_ROT_AFFINE -- the affine quantizer of the rotated row
+ *          y = H diag(sign) x / 16 (H the unnormalized 128-point Sylvester
+ *          Hadamard matrix), the integer-level quantization with a Hadamard
+ *          rotation of Sec. 4.1 and Sec. 4.9: per group of `group` rotated
+ *          coordinates zero = fp16(min y), scale = fp16((max y - zero)/(L-1))
+ *          (at least 0); x is reconstructed as diag(sign) H y_hat / 8.
+ *          L_hi, L_lo in {6, 5} or {5, 4}.
  *  group:  affine metadata group in {32, 64, 128}; must be 128 for tq.
  *  r_num/r_den: high-precision fraction r (Eq. 4), 0 <= r <= 1.
  *  block:  deferred block size B of Alg. 2; must be 64.
@@ -80,8 +87,9 @@ typedef struct semkv_config {
  *          row (128 channels), a V line one channel column over the 64 slots;
  *          segment j of a line is its symbols p = j, j+4, j+8, ...; a body is
  *          segment 0 of every line, then segments 1, 2, 3, LSB-first, zero
- *          padded to a multiple of 16 bytes.  Meta: affine, per group g and
- *          slot s, fp16 {scale, zero} at [g][s]; tq, fp16 rho at [s].
+ *          padded to a multiple of 16 bytes.  Meta: affine and rotated
+ *          affine, per group g and slot s, fp16 {scale, zero} at [g][s]; tq,
+ *          fp16 rho at [s].
  *          Slots of a pool are in increasing token position, prompt tokens
  *          first, then each closed generation block.
  *  tail:   fp16 [batch][n_layers][n_kv_heads][2 (K,V)][64][128], the
@@ -105,7 +113,7 @@ typedef struct semkv_cache {
   uint16_t* tail;             /* device, fp16 */
   float* tail_scores;         /* device */
   uint32_t* flags;            /* device */
-  const uint32_t* tq_signs;   /* device [n_layers][n_kv_heads][4] (tq) or NULL */
+  const uint32_t* signs;      /* device [n_layers][n_kv_heads][4] (bases 1, 2) or NULL */
   int32_t* status;            /* device status word */
   float mu_hi[16], tau_hi[16], mu_lo[16], tau_lo[16];  /* tq codebooks */
   int64_t n_prompt;           /* prompt tokens quantized (same for every sequence) */
@@ -127,10 +135,11 @@ int semkv_tq_codebook(int L, float* mu, float* tau);
 
 /* Initialize `c` over caller buffers sized by semkv_cache_sizes.  The buffers
  * need no clearing except `flags` and `status`, which must be zero.
- * tq_signs: device uint32 [n_layers][n_kv_heads][4]; bit i set = channel i of
- * that head is negated before the Hadamard transform (tq only, else NULL). */
+ * signs: device uint32 [n_layers][n_kv_heads][4]; bit i set = channel i of
+ * that head is negated before the Hadamard transform (the rotated bases, tq
+ * and rotated affine; NULL for the affine base). */
 int semkv_cache_init(semkv_cache* c, const semkv_config* cfg, void* pools, void* tail,
-                     float* tail_scores, uint32_t* flags, const uint32_t* tq_signs,
+                     float* tail_scores, uint32_t* flags, const uint32_t* signs,
                      int32_t* status);
 
 /* Eq. (4)-(5) for every sequence: K = floor(r T); the K tokens with the

@@ -9,9 +9,9 @@ import ctypes
 import numpy as np
 
 from . import _abi
-from ._abi import BASE_AFFINE, BASE_TQ, SemKVError, check, lib
+from ._abi import BASE_AFFINE, BASE_ROT_AFFINE, BASE_TQ, SemKVError, check, lib
 
-__all__ = ["SemKVCache", "SemKVError", "BASE_AFFINE", "BASE_TQ", "tq_codebook", "cache_sizes"]
+__all__ = ["SemKVCache", "SemKVError", "BASE_AFFINE", "BASE_TQ", "BASE_ROT_AFFINE", "tq_codebook", "cache_sizes"]
 
 
 def _stream():
@@ -58,7 +58,7 @@ class SemKVCache:
         self.flags = torch.zeros(self.sz.flag_bytes // 4, dtype=torch.int32, device=dev)
         self.status_word = torch.zeros(4, dtype=torch.int32, device=dev)
         self.signs = None
-        if cfg.base == BASE_TQ:
+        if cfg.base != BASE_AFFINE:
             sw = np.ascontiguousarray(sign_words, dtype=np.uint32).reshape(cfg.n_layers, cfg.n_kv_heads, 4)
             self.signs = torch.from_numpy(sw.view(np.int32)).to(dev)
         self.c = _abi.Cache()

@@ -10,7 +10,7 @@ vp = ctypes.c_void_p
 
 SEMKV_OK, SEMKV_EINVAL, SEMKV_EUNSUPPORTED, SEMKV_ECAPACITY, SEMKV_ENAN, SEMKV_EHIP, SEMKV_ESTATE = \
     0, -1, -2, -3, -4, -5, -6
-BASE_AFFINE, BASE_TQ = 0, 1
+BASE_AFFINE, BASE_TQ, BASE_ROT_AFFINE = 0, 1, 2
 STATUS_NAN_SCORE, STATUS_NONFINITE_KV = 1, 2
 
 
@@ -30,7 +30,7 @@ class Sizes(ctypes.Structure):
 
 class Cache(ctypes.Structure):
     _fields_ = [("cfg", Config), ("sz", Sizes),
-                ("pools", vp), ("tail", vp), ("tail_scores", vp), ("flags", vp), ("tq_signs", vp),
+                ("pools", vp), ("tail", vp), ("tail_scores", vp), ("flags", vp), ("signs", vp),
                 ("status", vp),
                 ("mu_hi", f32 * 16), ("tau_hi", f32 * 16), ("mu_lo", f32 * 16), ("tau_lo", f32 * 16),
                 ("n_prompt", i64), ("n_hi", i64), ("n_lo", i64), ("n_scored", i32), ("appended", u32 * 4)]

@@ -29,8 +29,12 @@
 //           not fit the scale.
 // The last run also takes the fp16 tail of generated tokens.  The waves'
 // states merge in LDS into one partial per workgroup; the last workgroup of a
-// unit to finish merges the partials (log-sum-exp) and, for the TurboQuant-MSE
-// base, applies the inverse random-sign Hadamard rotation.
+// unit to finish merges the partials (log-sum-exp) and, for the rotated bases
+// (TurboQuant-MSE, and the affine base under its Hadamard rotation), applies
+// the inverse random-sign Hadamard rotation.
+// Bases: 0 affine, 1 TurboQuant-MSE, 2 affine of the rotated row.  Bases 0
+// and 2 share the affine levels and metadata; bases 1 and 2 score against the
+// rotated query H diag(sign) q and accumulate values in the rotated domain.
 #include <hip/hip_fp16.h>
 
 #include "semkv_internal.h"
@@ -63,7 +67,7 @@ template <int BASE, int L>
 struct Traits {
   static constexpr int n = sym_digits(L);
   static constexpr int P = (BASE == 1 && L == 4) ? 2 : 1;   // MFMA slots per code
-  static constexpr int STRIDE = (L == 5 || (L == 4 && BASE == 0)) ? 4 : 8;
+  static constexpr int STRIDE = (L == 5 || (L == 4 && BASE != 1)) ? 4 : 8;
   static constexpr int SPC = 16 / STRIDE;
   static constexpr int EDW = STRIDE / 4;                     // operand dwords per symbol
   static constexpr int SK = num_syms(L, kD), SV = num_syms(L, kSlots);
@@ -392,8 +396,8 @@ struct Geo {
   static constexpr int MB = meta_bytes(BASE, G);
   static constexpr int RB = 2 * Tr::TB + 2 * MB;
   static constexpr int NLD = (RB + 1023) / 1024;            // 1 KB staging pieces per record
-  static constexpr int NG = BASE == 0 ? kD / G : 1;          // score products per chunk (query groups)
-  static constexpr int NGV = BASE == 0 ? kD / G : 1;         // value groups
+  static constexpr int NG = BASE != 1 ? kD / G : 1;          // score products per chunk (query groups)
+  static constexpr int NGV = BASE != 1 ? kD / G : 1;         // value groups
   static constexpr int NPL = Tr::P;                          // value planes (tq, 4 levels: 2)
   // int8 weights of one wave and one value group at a time, in value
   // A-operand order: [chunk][lane group][row][16 slots], so a lane reads a
@@ -482,7 +486,7 @@ struct Shared {
   alignas(16) uint32_t lut[PL::LUTH + PL::LUTL];
   alignas(16) uint8_t stage[PL::NW][PL::NLD * 1024];         // per wave: one record, later its Fin
   alignas(16) uint8_t pv[PL::NW][PL::PV];                    // per wave int8 weights
-  alignas(16) float qf[4][kQPad];                            // fp32 query, rotated for tq
+  alignas(16) float qf[4][kQPad];                            // fp32 query, rotated for bases 1, 2
   float qorig[4][kD];                                        // query as given (fp16 tail)
   Fin tfin;                                                  // the fp16 tail's state
   TailScratch ts;
@@ -541,7 +545,7 @@ __device__ inline void store_pieces(const uint4 (&r)[NMAX], uint8_t* lds, int la
   for (int j = 0; j < NMAX; ++j) *reinterpret_cast<uint4*>(lds + j * 1024 + lane * 16) = r[j];
 }
 
-// Per head, of the query x (affine) or the rotated query (tq) held by one
+// Per head, of the query x (affine) or the rotated query (bases 1, 2) held by one
 // thread per (head, channel) -- whole waves, 64 channels of one head each:
 // sums over aligned runs of 32 channels (the zero-point terms) and the
 // largest magnitude of each such run (the fixed-point scale).
@@ -567,7 +571,7 @@ __device__ inline void query_runs(float x, int h, int c, Shared<PL>& sm) {
 // weights included), times 2^e, lies in [2^19, 2^20)
 template <int BASE, int G, class PL>
 __device__ inline float query_sum(const Shared<PL>& sm, int h, int g) {
-  constexpr int GQ = BASE == 0 ? G : kD;
+  constexpr int GQ = BASE != 1 ? G : kD;
   float z = 0.0f;
 #pragma unroll
   for (int k = 0; k < GQ / 32; ++k) z += sm.zpart[h][g * GQ / 32 + k];
@@ -575,11 +579,11 @@ __device__ inline float query_sum(const Shared<PL>& sm, int h, int g) {
 }
 template <int BASE, int L, int G, class PL>
 __device__ inline int query_exp(const Shared<PL>& sm, const float* mu, int h, int g) {
-  constexpr int GQ = BASE == 0 ? G : kD;
+  constexpr int GQ = BASE != 1 ? G : kD;
   float mx = 0.0f;
 #pragma unroll
   for (int k = 0; k < GQ / 32; ++k) mx = fmaxf(mx, sm.qmax[h][g * GQ / 32 + k]);
-  mx *= BASE == 0 || L == 3 ? 1.0f : mu[2] + mu[3];        // tq, 4 levels: mu2 + mu3 > mu3 - mu2 > 0
+  mx *= BASE != 1 || L == 3 ? 1.0f : mu[2] + mu[3];        // tq, 4 levels: mu2 + mu3 > mu3 - mu2 > 0
   const int E = __builtin_amdgcn_frexp_expf(mx);          // mx = f 2^E, f in [0.5, 1)
   return mx >= 1e-30f ? 20 - E : 0;
 }
@@ -588,7 +592,8 @@ __device__ inline int query_exp(const Shared<PL>& sm, const float* mu, int h, in
 // for query group g, lane (row m = 4h + s, kg) chunk c slot e holds byte s of
 // qi = rint(x 2^e) at the channel the slot addresses (zero past channel 127,
 // in pad slots, outside group g and in rows 4h + 3), x the query of head h
-// (affine) or its plane-weighted rotated query (tq), |qi| < 2^20.  qi splits
+// (affine), its rotated query (rotated affine) or its plane-weighted rotated
+// query (tq), |qi| < 2^20.  qi splits
 // as 2^14 b0 + 2^7 b1 + b2 (b0 signed, b1, b2 in [0, 127]), so a product sums
 // the exact integer qi . codes in three rows.
 // Items are dealt to threads from thread OFF on (the low pool's start where
@@ -598,8 +603,8 @@ __device__ void build_aq(const DecodeArgs& a, Shared<PL>& sm) {
   using Tr = Traits<BASE, L>;
   using Ge = Geo<BASE, L, G>;
   const float* mu = a.mu[POOL];
-  const float wP[2] = {BASE == 0 ? 1.0f : (L == 3 ? 1.0f : mu[3] - mu[2]),
-                       BASE == 0 ? 1.0f : (L == 3 ? 1.0f : mu[2] + mu[3])};
+  const float wP[2] = {BASE != 1 ? 1.0f : (L == 3 ? 1.0f : mu[3] - mu[2]),
+                       BASE != 1 ? 1.0f : (L == 3 ? 1.0f : mu[2] + mu[3])};
   for (int item = (int(threadIdx.x) + PL::NT - OFF % PL::NT) % PL::NT; item < Ge::NG * Tr::NCK * 64; item += PL::NT) {
     const int g = item / (Tr::NCK * 64), c = (item >> 6) % Tr::NCK, ln = item & 63;
     const int m = ln & 15, kg = ln >> 4, h = m >> 2, sp = m & 3;
@@ -636,10 +641,15 @@ __device__ void run_pool(const DecodeArgs& a, Shared<PL>& sm, WaveState<PL::NGV>
   uint8_t* rec = sm.stage[wave];
   // tq: mu = -m, 0, m (L = 3) or -b, -a, a, b (L = 4)
   const float* mu = a.mu[POOL];
-  const float cS = BASE == 0 ? 1.0f : (L == 3 ? mu[2] / 128.0f : 1.0f / 128.0f);
-  const float cZ = BASE == 0 ? 0.0f : (L == 3 ? -mu[2] / 128.0f : -mu[3] / 128.0f);
-  const float wP[2] = {BASE == 0 ? 1.0f : (L == 3 ? 1.0f : mu[3] - mu[2]),
-                       BASE == 0 ? 1.0f : (L == 3 ? 1.0f : mu[2] + mu[3])};
+  const float cS = BASE != 1 ? 1.0f : (L == 3 ? mu[2] / 128.0f : 1.0f / 128.0f);
+  const float cZ = BASE != 1 ? 0.0f : (L == 3 ? -mu[2] / 128.0f : -mu[3] / 128.0f);
+  const float wP[2] = {BASE != 1 ? 1.0f : (L == 3 ? 1.0f : mu[3] - mu[2]),
+                       BASE != 1 ? 1.0f : (L == 3 ? 1.0f : mu[2] + mu[3])};
+  // rotated affine: k = sign . H y / 8 with y = s c + z the affine value of
+  // the rotated coordinates, so q . k = (H sign . q) . y / 8, and the values
+  // are summed as y / 8 in the rotated domain (powers of 2: exact)
+  constexpr float kR = BASE == 2 ? 0.125f : 1.0f;
+  constexpr float kScore = kLog2e * kRsqrtD * kR;
 
   // ---- score A operands (built once per workgroup): in registers for one
   // query group, else read per product
@@ -702,24 +712,24 @@ __device__ void run_pool(const DecodeArgs& a, Shared<PL>& sm, WaveState<PL::NGV>
     uint32_t kseg[4][Tr::KSEGW];
 #pragma unroll
     for (int blk = 0; blk < 4; ++blk) lds_segment<Tr::KSEGW>(rec, koff0 + blk * kstep, kseg[blk]);
-    constexpr int NKM = BASE == 0 ? NG : 1, NVM = BASE == 0 ? NGV : 1;
+    constexpr int NKM = BASE != 1 ? NG : 1, NVM = BASE != 1 ? NGV : 1;
     uint32_t km[4][NKM], vm[4][NVM];
 #pragma unroll
     for (int blk = 0; blk < 4; ++blk) {
       const int t = 16 * blk + n;
 #pragma unroll
       for (int i = 0; i < NKM; ++i)
-        km[blk][i] = BASE == 0 ? *reinterpret_cast<const uint32_t*>(kmeta + (i * kSlots + t) * 4)
+        km[blk][i] = BASE != 1 ? *reinterpret_cast<const uint32_t*>(kmeta + (i * kSlots + t) * 4)
                                : uint32_t(*reinterpret_cast<const uint16_t*>(kmeta + t * 2));
 #pragma unroll
       for (int i = 0; i < NVM; ++i)
-        vm[blk][i] = BASE == 0 ? *reinterpret_cast<const uint32_t*>(vmeta + (i * kSlots + t) * 4)
+        vm[blk][i] = BASE != 1 ? *reinterpret_cast<const uint32_t*>(vmeta + (i * kSlots + t) * 4)
                                : uint32_t(*reinterpret_cast<const uint16_t*>(vmeta + t * 2));
     }
     // the score of token 16 blk + n from its products, one per query group
     auto score = [&](int blk, const int4v (&acc)[NG]) {
       float x = 0.0f;
-      if constexpr (BASE == 0) {
+      if constexpr (BASE != 1) {
 #pragma unroll
         for (int i = 0; i < NG; ++i)
           x += comb3_score(acc[i]) * qsc[i] * hf(km[blk][i] & 0xFFFFu) + hf(km[blk][i] >> 16) * zws[i];
@@ -727,7 +737,7 @@ __device__ void run_pool(const DecodeArgs& a, Shared<PL>& sm, WaveState<PL::NGV>
         const float rho = hf(uint16_t(km[blk][0]));
         x = comb3_score(acc[0]) * qsc[0] * (rho * cS) + rho * cZ * zws[0];
       }
-      return 16 * blk + n < nvalid ? x * (kLog2e * kRsqrtD) : -INFINITY;
+      return 16 * blk + n < nvalid ? x * kScore : -INFINITY;
     };
     // software pipeline: the next block's table reads are in flight during
     // the current block's products
@@ -789,13 +799,14 @@ __device__ void run_pool(const DecodeArgs& a, Shared<PL>& sm, WaveState<PL::NGV>
     for (int blk = 0; blk < 4; ++blk) {
       const float p = __builtin_amdgcn_exp2f(lg[blk] - m_new);   // 0 for masked tokens
       lsum += p;
-      if constexpr (BASE == 0) {
+      if constexpr (BASE != 1) {
+        const float pr = p * kR;
 #pragma unroll
         for (int i = 0; i < NGV; ++i) {
           const uint32_t m = vm[blk][i];
-          wv[blk][i][0] = p * hf(m & 0xFFFFu);
+          wv[blk][i][0] = pr * hf(m & 0xFFFFu);
           wmax = fmaxf(wmax, wv[blk][i][0]);
-          st.z[i] += p * hf(m >> 16);
+          st.z[i] += pr * hf(m >> 16);
         }
       } else {
         const float rho = hf(uint16_t(vm[blk][0]));
@@ -829,7 +840,7 @@ __device__ void run_pool(const DecodeArgs& a, Shared<PL>& sm, WaveState<PL::NGV>
     int4v Aw[Tr::NCV];
 #pragma unroll
     for (int cb = 0; cb < 8; ++cb) {
-      constexpr int CPG = BASE == 0 ? G / 16 : 8;          // channel blocks per value group
+      constexpr int CPG = BASE != 1 ? G / 16 : 8;          // channel blocks per value group
       if (cb % CPG == 0) {
         const int gv = cb / CPG;
 #pragma unroll
@@ -888,7 +899,7 @@ __device__ void wave_finish(Shared<PL>& sm, WaveState<PL::NGV>& st) {
 #pragma unroll
   for (int cb = 0; cb < 8; ++cb) {
     const int ch = 16 * cb + n;
-    f->o[r][ch] = st.of[cb] + comb3(st.cv[cb]) * st.qwi + sm.zc[wave][r][BASE == 0 ? ch / G : 0];
+    f->o[r][ch] = st.of[cb] + comb3(st.cv[cb]) * st.qwi + sm.zc[wave][r][BASE != 1 ? ch / G : 0];
   }
 }
 
@@ -901,41 +912,33 @@ __device__ inline void st_agent(float* p, float v) {
 }
 
 
-// one radix-2 stage of the unnormalized Walsh-Hadamard transform of the 4
-// rows of x (128 entries each), by the first 256 threads
-__device__ inline void fwht_stage(float (*x)[kQPad], int hs) {
-  const int tid = threadIdx.x, hh = tid >> 6, i = tid & 63;
-  float a = 0.0f, b = 0.0f;
-  int lo = 0, hi = 0;
-  if (hh < 4) {
-    lo = (i / hs) * 2 * hs + (i % hs);
-    hi = lo + hs;
-    a = x[hh][lo];
-    b = x[hh][hi];
+// The unnormalized Walsh-Hadamard transform H x of the 4 rows of 128 values
+// held one per thread by threads 0..511 (thread t: row t >> 7, entry t & 127).
+// Stages 1..32 pair lanes of one wave (DPP quad permutes for 1 and 2, lane
+// exchanges for the rest); stage 64 pairs the two waves of a row through the
+// LDS buffer xch.  Each stage computes the lower entry as lower + upper and the
+// upper as lower - upper, the radix-2 butterflies in the usual order.  Every
+// thread of the workgroup calls it; xch is free again when it returns.
+__device__ inline float fwht_rows(float x, float (*xch)[kD]) {
+  const int tid = threadIdx.x, lane = tid & 63;
+  float p = dpp<0xB1>(x);                                  // lane ^ 1
+  x = (lane & 1) ? p - x : x + p;
+  p = dpp<0x4E>(x);                                        // lane ^ 2
+  x = (lane & 2) ? p - x : x + p;
+#pragma unroll
+  for (int hs = 4; hs < 64; hs <<= 1) {
+    p = __shfl_xor(x, hs);
+    x = (lane & hs) ? p - x : x + p;
+  }
+  const bool mine = tid < 4 * kD;
+  if (mine) xch[tid >> 7][tid & 127] = x;
+  __syncthreads();
+  if (mine) {
+    p = xch[tid >> 7][(tid & 127) ^ 64];
+    x = (tid & 64) ? p - x : x + p;
   }
   __syncthreads();
-  if (hh < 4) {
-    x[hh][lo] = a + b;
-    x[hh][hi] = a - b;
-  }
-  __syncthreads();
-}
-__device__ inline void fwht_stage(float (*x)[kD], int hs) {
-  const int tid = threadIdx.x, hh = tid >> 6, i = tid & 63;
-  float a = 0.0f, b = 0.0f;
-  int lo = 0, hi = 0;
-  if (hh < 4) {
-    lo = (i / hs) * 2 * hs + (i % hs);
-    hi = lo + hs;
-    a = x[hh][lo];
-    b = x[hh][hi];
-  }
-  __syncthreads();
-  if (hh < 4) {
-    x[hh][lo] = a + b;
-    x[hh][hi] = a - b;
-  }
-  __syncthreads();
+  return x;
 }
 
 // fp16 tail of generated tokens (at most 64 rows), plain vector arithmetic;
@@ -969,20 +972,17 @@ __device__ void tail_split(const DecodeArgs& a, Shared<PL>& sm, int b, int kvh) 
   }
   __syncthreads();
   const int h = tid >> 7, c = tid & 127;
+  float o = 0.0f;
   if (tid < 4 * kD) {
-    float o = 0.0f;
     for (int t = 0; t < nt; ++t) o += ts.lg[h][t] * hf(vt[t * kD + c]);
-    if (BASE == 1) {                       // into the rotated domain: H (sign . o) / 128
+    if (BASE != 0) {                       // into the rotated domain: H (sign . o) / 128
       const uint32_t* sw = g.signs + (int64_t(a.layer) * g.n_kv_heads + kvh) * 4;
       o = ((sw[c >> 5] >> (c & 31)) & 1u) ? -o : o;
     }
-    ts.o[h][c] = o;
   }
-  __syncthreads();
-  if (BASE == 1)
-    for (int hs = 1; hs < kD; hs <<= 1) fwht_stage(ts.o, hs);
+  if (BASE != 0) o = fwht_rows(o, ts.o) * (1.0f / 128.0f);
   if (tid < 4 * kD) {
-    sm.tfin.o[h][c] = ts.o[h][c] * (BASE == 1 ? 1.0f / 128.0f : 1.0f);
+    sm.tfin.o[h][c] = o;
     if (c == 0) {
       sm.tfin.m[h] = ts.mx[h];
       sm.tfin.l[h] = ts.sum[h];
@@ -991,8 +991,8 @@ __device__ void tail_split(const DecodeArgs& a, Shared<PL>& sm, int b, int kvh) 
 }
 
 // Merge of the partials of one (sequence, kv head), run by the last workgroup
-// to finish: log-sum-exp over the partials, then for the tq base the inverse
-// rotation o = sign . H o_rot.
+// to finish: log-sum-exp over the partials, then for the rotated bases the
+// inverse rotation o = sign . H o_rot.
 template <int BASE, class PL>
 __device__ void merge_splits(const DecodeArgs& a, Shared<PL>& sm, int b, int kvh) {
   const int tid = threadIdx.x;
@@ -1003,6 +1003,8 @@ __device__ void merge_splits(const DecodeArgs& a, Shared<PL>& sm, int b, int kvh
   // agent-scope loads), then the four quarters merge in LDS
   const bool mine = tid < 4 * kD;
   const int h = (tid >> 7) & 3, q = (tid >> 5) & 3, cq = tid & 31;
+  // the sign of this thread's output channel (rotated bases), loaded first
+  const uint32_t sbits = BASE != 0 && mine ? a.g.signs[(int64_t(a.layer) * a.g.n_kv_heads + kvh) * 4 + ((tid & 127) >> 5)] : 0u;
   const __amdgpu_buffer_rsrc_t rs =
       __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(unit), 0, ns * 4 * kPartial * 4, kBufferWord3);
   constexpr int kCoherent = 16;              // sc1
@@ -1066,13 +1068,9 @@ __device__ void merge_splits(const DecodeArgs& a, Shared<PL>& sm, int b, int kvh
     }
     r = O / L;
   }
-  if (BASE == 1) {
-    __syncthreads();
-    if (mine) sm.qf[hc][c] = r;
-    __syncthreads();
-    for (int hs = 1; hs < kD; hs <<= 1) fwht_stage(sm.qf, hs);
-    const uint32_t* sw = a.g.signs + (int64_t(a.layer) * a.g.n_kv_heads + kvh) * 4;
-    if (mine) r = ((sw[c >> 5] >> (c & 31)) & 1u) ? -sm.qf[hc][c] : sm.qf[hc][c];
+  if (BASE != 0) {
+    r = fwht_rows(r, sm.ts.o);
+    r = ((sbits >> (c & 31)) & 1u) ? -r : r;
   }
   if (mine) a.out[((int64_t(b) * a.g.n_kv_heads + kvh) * 4 + hc) * kD + c] = r;
 }
@@ -1112,6 +1110,8 @@ __global__ __launch_bounds__((Plan<BASE, LH, LL, G>::NT)) void decode_kernel(Dec
   const bool qt = tid < 4 * kD;
   const int h = qt ? tid >> 7 : 0, c = tid & 127;
   const uint16_t qbits = qt ? a.q[((int64_t(b) * g.n_kv_heads * 4) + kvh * 4 + h) * kD + c] : uint16_t(0);
+  // rotated bases: the sign word of this thread's channel, in flight with the query
+  const uint32_t qsign = BASE != 0 && qt ? g.signs[(int64_t(a.layer) * g.n_kv_heads + kvh) * 4 + (c >> 5)] : 0u;
   constexpr int NTH = (PL::LUTH / 4 + NT - 1) / NT, NTL = (PL::LUTL / 4 + NT - 1) / NT;
   uint4 th[NTH], tl[NTL];
 #pragma unroll
@@ -1130,24 +1130,19 @@ __global__ __launch_bounds__((Plan<BASE, LH, LL, G>::NT)) void decode_kernel(Dec
     for (int k = 0; k < NTL; ++k)
       if (tid + k * NT < PL::LUTL / 4) d[PL::LUTH / 4 + tid + k * NT] = tl[k];
   }
+  float xq = 0.0f;
   if (qt) {
-    const float x = hf(qbits);
-    sm.qorig[h][c] = x;
-    float xr = x;
-    if (BASE == 1) {
-      const uint32_t* sw = g.signs + (int64_t(a.layer) * g.n_kv_heads + kvh) * 4;
-      xr = ((sw[c >> 5] >> (c & 31)) & 1u) ? -x : x;
-    }
-    sm.qf[h][c] = xr;
+    xq = hf(qbits);
+    sm.qorig[h][c] = xq;
+    if (BASE != 0) xq = ((qsign >> (c & 31)) & 1u) ? -xq : xq;
+  }
+  if (BASE != 0) xq = fwht_rows(xq, sm.ts.o);    // rotate: H (sign . q)
+  if (qt) {
+    sm.qf[h][c] = xq;
     if (c < kQPad - kD) sm.qf[h][kD + c] = 0.0f;
-    if (BASE == 0) query_runs(x, h, c, sm);   // affine: from the query as loaded
+    query_runs(xq, h, c, sm);                   // the query the scores use: its runs
   }
   __syncthreads();
-  if (BASE == 1) {                          // rotate: H (sign . q), then its runs
-    for (int hs = 1; hs < kD; hs <<= 1) fwht_stage(sm.qf, hs);
-    if (qt) query_runs(sm.qf[h][c], h, c, sm);
-    __syncthreads();
-  }
   build_aq<BASE, LH, G, 0, 0>(a, sm);
   build_aq<BASE, LL, G, 1, PL::GH::NG * PL::NCKH * 64>(a, sm);
   __syncthreads();
@@ -1280,6 +1275,8 @@ int launch_decode(const DecodeArgs& a, hipStream_t s) {
   if (B == 0 && LH == 5 && LL == 3) return launch_dec<0, 5, 3>(a, s);
   if (B == 0 && LH == 6 && LL == 3) return launch_dec<0, 6, 3>(a, s);
   if (B == 1 && LH == 4 && LL == 3) return launch_dec<1, 4, 3>(a, s);
+  if (B == 2 && LH == 6 && LL == 5) return launch_dec<2, 6, 5>(a, s);
+  if (B == 2 && LH == 5 && LL == 4) return launch_dec<2, 5, 4>(a, s);
   return -2;
 }
 
@@ -1291,6 +1288,8 @@ static int decode_query(int base, int LH, int LL, int G, bool waves) {
   if (base == 0 && LH == 5 && LL == 3) return occ_dec<0, 5, 3>(G, waves);
   if (base == 0 && LH == 6 && LL == 3) return occ_dec<0, 6, 3>(G, waves);
   if (base == 1 && LH == 4 && LL == 3) return occ_dec<1, 4, 3>(G, waves);
+  if (base == 2 && LH == 6 && LL == 5) return occ_dec<2, 6, 5>(G, waves);
+  if (base == 2 && LH == 5 && LL == 4) return occ_dec<2, 5, 4>(G, waves);
   return waves ? 8 : 1;
 }
 

@@ -104,19 +104,13 @@ __device__ uint32_t affine_quarter(const float x[32], int G, uint32_t code[8]) {
   return uint32_t(s16) | (uint32_t(f2h(zero)) << 16);
 }
 
-// TurboQuant-MSE base (Sec. 4.9) of one row quarter: sign flip, unnormalized
-// Walsh-Hadamard transform (stages 1..64), the row norm by a fixed pairwise
-// tree, one fp16 scalar, and Lloyd-Max threshold codes.  Returns rho bits.
-template <int L>
-__device__ uint16_t tq_quarter(const float x[32], int q, const uint32_t* sw, const float* tau,
-                               uint32_t code[8]) {
-  float u[32], a[32];
-  uint32_t sbits = sw[q];
+// H diag(sign) x of one row quarter: sign flip, then the unnormalized
+// Walsh-Hadamard transform, stages 1..16 inside the lane and 32, 64 across
+// the lanes of the row's quad.
+__device__ inline void rotate_quarter(const float x[32], int q, const uint32_t* sw, float u[32]) {
+  const uint32_t sbits = sw[q];
 #pragma unroll
-  for (int i = 0; i < 32; ++i) {
-    u[i] = ((sbits >> i) & 1u) ? -x[i] : x[i];
-    a[i] = x[i] * x[i];
-  }
+  for (int i = 0; i < 32; ++i) u[i] = ((sbits >> i) & 1u) ? -x[i] : x[i];
 #pragma unroll
   for (int h = 1; h < 32; h <<= 1)
 #pragma unroll
@@ -139,6 +133,18 @@ __device__ uint16_t tq_quarter(const float x[32], int q, const uint32_t* sw, con
     const float o = quad_mov<kQuadXor2>(u[i]);
     u[i] = o + __uint_as_float(__float_as_uint(u[i]) ^ f2);
   }
+}
+
+// TurboQuant-MSE base (Sec. 4.9) of one row quarter: the rotation, the row
+// norm by a fixed pairwise tree, one fp16 scalar, and Lloyd-Max threshold
+// codes.  Returns rho bits.
+template <int L>
+__device__ uint16_t tq_quarter(const float x[32], int q, const uint32_t* sw, const float* tau,
+                               uint32_t code[8]) {
+  float u[32], a[32];
+  rotate_quarter(x, q, sw, u);
+#pragma unroll
+  for (int i = 0; i < 32; ++i) a[i] = x[i] * x[i];
 #pragma unroll
   for (int i = 0; i < 32; ++i) a[i] = a[i] + quad_mov<kQuadXor2>(a[i]);   // h = 64 (lanes 0,1 keep)
 #pragma unroll
@@ -169,13 +175,60 @@ __device__ uint16_t tq_quarter(const float x[32], int q, const uint32_t* sw, con
   return r16;
 }
 
+// Affine quantizer of the rotated row (Sec. 4.1 with its Hadamard rotation):
+// y = H diag(sign) x / 16 (the division is exact), then per group of G
+// rotated coordinates zero = fp16(min y) (-0 stored as +0) and scale =
+// fp16(max(0, (max y - zero) / (L-1))), codes against the stored pair.
+// Returns {scale, zero} as fp16 bits (low half = scale).
+template <int L>
+__device__ uint32_t rot_affine_quarter(const float x[32], int q, const uint32_t* sw, int G, uint32_t code[8]) {
+  float y[32];
+  rotate_quarter(x, q, sw, y);
+  float mn = INFINITY, mx = -INFINITY;
+#pragma unroll
+  for (int i = 0; i < 32; ++i) {
+    y[i] *= 0.0625f;
+    mn = fminf(mn, y[i]);
+    mx = fmaxf(mx, y[i]);
+  }
+  if (G >= 64) {
+    mn = fminf(mn, quad_mov<kQuadXor1>(mn));
+    mx = fmaxf(mx, quad_mov<kQuadXor1>(mx));
+  }
+  if (G >= 128) {
+    mn = fminf(mn, quad_mov<kQuadXor2>(mn));
+    mx = fmaxf(mx, quad_mov<kQuadXor2>(mx));
+  }
+  uint16_t z16 = f2h(mn);
+  z16 = z16 == 0x8000u ? uint16_t(0) : z16;
+  const float zero = h2f(z16);
+  const float s32 = __fdiv_rn(mx - zero, float(L - 1));
+  const uint16_t s16 = f2h(s32 > 0.0f ? s32 : 0.0f);
+  const float sf = h2f(s16);
+  const float inv = sf == 0.0f ? 0.0f : __fdiv_rn(1.0f, sf);
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    uint32_t w = 0;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      float c = rintf((y[4 * k + e] - zero) * inv);
+      c = fminf(fmaxf(c, 0.0f), float(L - 1));
+      w = __builtin_amdgcn_cvt_pk_u8_f32(c, e, w);
+    }
+    code[k] = w;
+  }
+  return uint32_t(s16) | (uint32_t(z16) << 16);
+}
+
 // Quantize the quarter row held by this lane and write its metadata.
 template <int BASE, int L>
 __device__ void quantize_quarter(const PoolGeom& g, const float x[32], int q, int layer, int kvh,
                                  const float* tau, uint32_t code[8], uint8_t* meta_dst, int slot,
                                  bool valid) {
-  if (BASE == 0) {
-    uint32_t m = affine_quarter<L>(x, g.G, code);
+  if (BASE != 1) {
+    const uint32_t m = BASE == 0 ? affine_quarter<L>(x, g.G, code)
+                                 : rot_affine_quarter<L>(x, q, g.signs + (int64_t(layer) * g.n_kv_heads + kvh) * 4,
+                                                         g.G, code);
     int per = g.G / 32;
     if (q % per == 0)
       reinterpret_cast<uint32_t*>(meta_dst)[(q / per) * kSlots + slot] = valid ? m : 0u;
@@ -481,6 +534,8 @@ int launch_cl(const CloseArgs& a, hipStream_t st) {
   if (BASE == 0 && LH == 5 && LL == 3) return FN<0, 5, 3>(__VA_ARGS__);              \
   if (BASE == 0 && LH == 6 && LL == 3) return FN<0, 6, 3>(__VA_ARGS__);              \
   if (BASE == 1 && LH == 4 && LL == 3) return FN<1, 4, 3>(__VA_ARGS__);              \
+  if (BASE == 2 && LH == 6 && LL == 5) return FN<2, 6, 5>(__VA_ARGS__);              \
+  if (BASE == 2 && LH == 5 && LL == 4) return FN<2, 5, 4>(__VA_ARGS__);              \
   return -2;
 
 int launch_quantize(const QuantArgs& a, hipStream_t s) {

@@ -17,6 +17,7 @@ namespace {
 
 bool levels_ok(int base, int lh, int ll) {
   if (base == SEMKV_BASE_TQ) return lh == 4 && ll == 3;
+  if (base == SEMKV_BASE_ROT_AFFINE) return (lh == 6 && ll == 5) || (lh == 5 && ll == 4);
   static const int pairs[][2] = {{6, 5}, {5, 4}, {6, 4}, {4, 3}, {5, 3}, {6, 3}};
   for (auto& p : pairs)
     if (p[0] == lh && p[1] == ll) return true;
@@ -52,7 +53,7 @@ PoolGeom geom(const semkv_cache* c) {
   g.batch = k.batch;
   memcpy(g.tau[0], c->tau_hi, sizeof(g.tau[0]));
   memcpy(g.tau[1], c->tau_lo, sizeof(g.tau[1]));
-  g.signs = c->tq_signs;
+  g.signs = c->signs;
   g.status = c->status;
   return g;
 }
@@ -187,9 +188,10 @@ int semkv_cache_sizes(const semkv_config* cfg, semkv_sizes* out) {
     return SEMKV_EINVAL;
   if (k.max_prompt + k.max_new > (int64_t(1) << 29)) return SEMKV_EINVAL;   // decode splits use 32-bit tile math
   if (k.head_dim != 128 || k.n_q_heads != 4 * k.n_kv_heads || k.block != 64) return SEMKV_EUNSUPPORTED;
-  if (k.base != SEMKV_BASE_AFFINE && k.base != SEMKV_BASE_TQ) return SEMKV_EUNSUPPORTED;
+  if (k.base != SEMKV_BASE_AFFINE && k.base != SEMKV_BASE_TQ && k.base != SEMKV_BASE_ROT_AFFINE)
+    return SEMKV_EUNSUPPORTED;
   if (!levels_ok(k.base, k.L_hi, k.L_lo)) return SEMKV_EUNSUPPORTED;
-  if (k.base == SEMKV_BASE_AFFINE && k.group != 32 && k.group != 64 && k.group != 128) return SEMKV_EUNSUPPORTED;
+  if (k.base != SEMKV_BASE_TQ && k.group != 32 && k.group != 64 && k.group != 128) return SEMKV_EUNSUPPORTED;
   if (k.base == SEMKV_BASE_TQ && k.group != 128) return SEMKV_EUNSUPPORTED;
   // the decode kernel needs one 8-wave workgroup's tables and buffers in a
   // compute unit's LDS (6 and 3 levels with 32-channel groups do not fit)
@@ -257,13 +259,13 @@ int semkv_tq_codebook(int L, float* mu, float* tau) {
 }
 
 int semkv_cache_init(semkv_cache* c, const semkv_config* cfg, void* pools, void* tail,
-                     float* tail_scores, uint32_t* flags, const uint32_t* tq_signs, int32_t* status) {
+                     float* tail_scores, uint32_t* flags, const uint32_t* signs, int32_t* status) {
   if (!c || !cfg) return SEMKV_EINVAL;
   semkv_sizes sz;
   int st = semkv_cache_sizes(cfg, &sz);
   if (st) return st;
   if (!pools || !tail || !tail_scores || !flags || !status) return SEMKV_EINVAL;
-  if (cfg->base == SEMKV_BASE_TQ && !tq_signs) return SEMKV_EINVAL;
+  if (cfg->base != SEMKV_BASE_AFFINE && !signs) return SEMKV_EINVAL;
   if ((uintptr_t(pools) | uintptr_t(tail)) & 15) return SEMKV_EINVAL;
   memset(c, 0, sizeof(*c));
   c->cfg = *cfg;
@@ -272,7 +274,7 @@ int semkv_cache_init(semkv_cache* c, const semkv_config* cfg, void* pools, void*
   c->tail = static_cast<uint16_t*>(tail);
   c->tail_scores = tail_scores;
   c->flags = flags;
-  c->tq_signs = tq_signs;
+  c->signs = signs;
   c->status = status;
   if (cfg->base == SEMKV_BASE_TQ) {
     semkv_tq_codebook(cfg->L_hi, c->mu_hi, c->tau_hi);

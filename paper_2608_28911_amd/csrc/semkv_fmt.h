@@ -74,9 +74,11 @@ __host__ __device__ constexpr int tile_bytes(int L) {
   return ((bits + 7) / 8 + 15) / 16 * 16;
 }
 
-// bytes of one slot-major metadata block (K or V) of a tile
+// bytes of one slot-major metadata block (K or V) of a tile: fp16 {scale,
+// zero} per group for the affine bases (0, and 2 under a rotation), one fp16
+// rho for TurboQuant-MSE (1)
 __host__ __device__ constexpr int meta_bytes(int base, int G) {
-  return base == 0 ? (kD / G) * kSlots * 4 : kSlots * 2;
+  return base != 1 ? (kD / G) * kSlots * 4 : kSlots * 2;
 }
 
 __host__ __device__ constexpr int record_bytes(int base, int L, int G) {

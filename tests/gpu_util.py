@@ -9,7 +9,7 @@ TOL = 2e-3            # max-abs attention tolerance against the oracle
 
 
 def base_id(cfgw):
-    return 0 if cfgw.base == "affine" else 1
+    return cfgw.base_id
 
 
 def make_cache(cfgw, T, n_layers=None, max_new=None):
@@ -18,7 +18,7 @@ def make_cache(cfgw, T, n_layers=None, max_new=None):
     cfg = P.make_config(n_layers=nl, n_kv_heads=cfgw.n_kv_heads, batch=cfgw.batch, base=base_id(cfgw),
                         L_hi=cfgw.L_hi, L_lo=cfgw.L_lo, group=cfgw.group, r_num=cfgw.r_num,
                         r_den=cfgw.r_den, max_prompt=T, max_new=cfgw.n_gen if max_new is None else max_new)
-    signs = synth.all_sign_words(cfgw)[:nl] if cfgw.base == "tq" else None
+    signs = synth.all_sign_words(cfgw)[:nl] if cfgw.rotated else None
     return P.SemKVCache(cfg, sign_words=signs)
 
 
@@ -38,7 +38,7 @@ def prefill(cache, cfgw, T, scores=None, kv=None):
 
 def oracle_unit(cfgw, l, b, h, flag, T, kv=None):
     u = O.UnitCache(base_id(cfgw), cfgw.L_hi, cfgw.L_lo, cfgw.group, cfgw.r_num, cfgw.r_den,
-                    sign_words=synth.sign_words(cfgw, l, h) if cfgw.base == "tq" else None)
+                    sign_words=synth.sign_words(cfgw, l, h) if cfgw.rotated else None)
     if kv is None:
         K, V = synth.unit_kv(cfgw, l, b, h, T)
     else:

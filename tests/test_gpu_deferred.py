@@ -87,19 +87,26 @@ def test_generation_on_the_turboquant_base():
     run_generation(cfgw, 200, 64 + 5, check_steps={0, 63, 64, 68})
 
 
+def test_generation_on_the_rotated_affine_base():
+    cfgw = get_config(3, base="rot_affine", n_layers=1, batch=1, n_kv_heads=2, n_q_heads=8)
+    run_generation(cfgw, 200, 64 + 5, check_steps={0, 63, 64, 68})
+
+
 def test_generation_g32():
     cfgw = get_config(3, n_layers=1, batch=1, n_kv_heads=1, n_q_heads=4, group=32)
     run_generation(cfgw, 64, 64 * 3, check_steps={10, 100, 191})
 
 
-@pytest.mark.parametrize("wl", [3, 4])
-def test_fused_append_decode_matches_separate_calls(wl):
+@pytest.mark.parametrize("wl,base", [(3, None), (4, None), (3, "rot_affine")])
+def test_fused_append_decode_matches_separate_calls(wl, base):
     """semkv_append_decode (append and attend in one launch) gives the same
     attention, bit for bit, as semkv_append_kv followed by semkv_decode_attn,
     and leaves the same tail, pools and flags, across a block close."""
     import torch
     from paper_2608_28911_amd import SemKVError
     cfgw = get_config(wl, n_layers=2, batch=2, n_kv_heads=2, n_q_heads=8)
+    if base:
+        cfgw = get_config(wl, n_layers=2, batch=2, n_kv_heads=2, n_q_heads=8, base=base)
     T, n_gen = 150, 64 + 6
     sep, fus = U.make_cache(cfgw, T, max_new=n_gen), U.make_cache(cfgw, T, max_new=n_gen)
     for c in (sep, fus):

@@ -87,6 +87,13 @@ def test_llama8b_b1_t32768_affine_full_size():
     _check_decode(cache, cfgw, oracle)
 
 
+def test_llama8b_b1_t32768_rot_affine_full_size():
+    """The headline shape under the affine base of Hadamard-rotated rows."""
+    cfgw = get_config("llama8b_kv_b1_t32768_affine", base="rot_affine")
+    cache, oracle = _prefill_and_check(cfgw, 1, [(0, 0, 3)])
+    _check_decode(cache, cfgw, oracle)
+
+
 def test_batched_b16_t16384_dirichlet_full_size():
     cfgw = get_config("llama8b_kv_b16_t16384_affine_dirichlet")
     cache, oracle = _prefill_and_check(cfgw, 1, [(0, 0, 2), (15, 0, 7), (9, 0, 0)])

@@ -103,6 +103,24 @@ def test_turboquant_base_small():
     _check_decode(cache, cfgw, 1500, flags, [0, 1])
 
 
+@pytest.mark.parametrize("G", [32, 128])
+@pytest.mark.parametrize("levels", [(6, 5), (5, 4)])
+def test_rotated_affine_base(levels, G):
+    """The affine quantizer of the Hadamard-rotated rows (Sec. 4.1): records
+    bit-exact, attention over two layers (two sign masks) within tolerance."""
+    cfgw = get_config(0, base="rot_affine", L_hi=levels[0], L_lo=levels[1], group=G, n_layers=2, batch=2,
+                      n_kv_heads=2, n_q_heads=8)
+    cache, flags = _check_prefill(cfgw, 1000, n_layers=2)
+    _check_decode(cache, cfgw, 1000, flags, [0, 1])
+
+
+@pytest.mark.parametrize("T", [1, 65])
+def test_rotated_affine_ragged(T):
+    cfgw = get_config(0, base="rot_affine", group=64, n_kv_heads=2, n_q_heads=8)
+    cache, flags = _check_prefill(cfgw, T)
+    _check_decode(cache, cfgw, T, flags, [0])
+
+
 def test_constant_rows_quantize_exactly():
     import torch
     cfgw = get_config(0, n_kv_heads=1, n_q_heads=4, group=32)

@@ -20,7 +20,7 @@ class WorkloadConfig:
     prompt_len: int          # T, tokens quantized at prefill (Alg. 1)
     n_gen: int               # generated tokens under deferred blocks (Alg. 2)
     decode_steps: int        # decode steps measured
-    base: str                # "affine" | "tq"
+    base: str                # "affine" | "tq" | "rot_affine"
     L_hi: int                # levels of the high precision (6 -> 2.585 b)
     L_lo: int                # levels of the low precision  (5 -> 2.322 b)
     group: int               # affine metadata group (channels); 128 for tq
@@ -35,6 +35,19 @@ class WorkloadConfig:
     @property
     def gqa(self) -> int:
         return self.n_q_heads // self.n_kv_heads
+
+    @property
+    def base_id(self) -> int:
+        """0 affine, 1 TurboQuant-MSE, 2 affine of the Hadamard-rotated row."""
+        return BASES[self.base]
+
+    @property
+    def rotated(self) -> bool:
+        """The base rotates rows by a random-sign Hadamard transform."""
+        return self.base != "affine"
+
+
+BASES = {"affine": 0, "tq": 1, "rot_affine": 2}
 
 
 CONFIGS = [
