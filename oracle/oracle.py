@@ -69,6 +69,9 @@ def lib():
             "oq_tq_dequant_rows": (None, [P, P, i64, P, P, P]),
             "oq_rotaffine_dequant_rows": (None, [P, P, i64, i32, P, P]),
             "oq_attention": (None, [P, i32, P, P, i64, i32, P]),
+            "oq_score_hidden": (i32, [i32, P, i32, i64, i32, P]),
+            "oq_score_kv_norm": (i32, [P, i32, i64, P]),
+            "oq_bf16_to_f32_n": (None, [P, i64, P]),
             "oq_f32_to_f16_n": (None, [P, i64, P]),
             "oq_f16_to_f32_n": (None, [P, i64, P]),
         }
@@ -291,6 +294,39 @@ def attention(q, khat, vhat) -> np.ndarray:
     assert k.shape[0] >= 1
     lib().oq_attention(_p(q), q.shape[0], _p(k), _p(v), k.shape[0], q.shape[1], _p(out))
     return out
+
+
+# ---------------------------------------------------------- indicators ----
+
+DELTA_NORM, NORM, VARIANCE, COSINE_DELTA = 0, 1, 2, 3
+
+
+def bf16_bits_to_f32(h) -> np.ndarray:
+    h = np.ascontiguousarray(h, dtype=np.uint16)
+    out = np.empty(h.shape, np.float32)
+    lib().oq_bf16_to_f32_n(_p(h), h.size, _p(out))
+    return out
+
+
+def score_hidden(indicator, H, bf16=False) -> np.ndarray:
+    """Sec. 3.3 hidden-state indicators of one sequence.  H: [m+1, T, d] fp16
+    values (or bf16 bits as uint16 with bf16=True), state k = layer L-m+k.
+    Returns float64 [T]."""
+    Hf = bf16_bits_to_f32(H) if bf16 else np.ascontiguousarray(H, np.float16).astype(np.float32)
+    n, T, d = Hf.shape
+    s = np.zeros(T, np.float64)
+    _check(lib().oq_score_hidden(indicator, _p(Hf), n - 1, T, d, _p(s)))
+    return s
+
+
+def score_kv_norm(X) -> np.ndarray:
+    """KV-norm indicator of one sequence: X fp16 [R rows (layer x kv head), T, 128]
+    -> sqrt of the sum of squares over every row of each token, float64 [T]."""
+    Xf = np.ascontiguousarray(X, np.float16).astype(np.float32)
+    R, T, _ = Xf.shape
+    s = np.zeros(T, np.float64)
+    _check(lib().oq_score_kv_norm(_p(Xf), R, T, _p(s)))
+    return s
 
 
 # ------------------------------------------------ one unit of the cache ----

@@ -7,6 +7,7 @@
  *   Sec. 4.1     affine base, two fp16 parameters, mixed-radix packing
  *   Sec. 4.9     TurboQuant-MSE base, one scalar per row, Lloyd-Max codes
  *   Sec. 4.1/4.9 the affine base under a Hadamard rotation (rotated affine)
+ *   Sec. 3.3     token-importance indicators (Eq. 3 and its families)
  * Build: gcc -O2 -ffp-contract=off -fno-fast-math -fopenmp (IEEE single on SSE).
  */
 #include "semkv_oracle.h"
@@ -414,6 +415,71 @@ void oq_rotaffine_dequant_rows(const uint8_t* codes, const uint16_t* meta, int64
           y[i + h] = p - q;
         }
     for (int i = 0; i < 128; i++) out[r * 128 + i] = (sign_bit(sign_words, i) ? -y[i] : y[i]) / 8.0;
+  }
+}
+
+/* ----------------------------------------------------------- indicators -- */
+
+static double dot_d(const float* a, const float* b, int d) {
+  double s = 0.0;
+  for (int j = 0; j < d; j++) s += (double)a[j] * (double)b[j];
+  return s;
+}
+
+int oq_score_hidden(int indicator, const float* h, int m, int64_t T, int d, double* s) {
+  if (indicator < 0 || indicator > 3 || m < 0 || d <= 0 || T < 0) return OQ_EINVAL;
+  if ((indicator == 0 || indicator == 3) && m < 1) return OQ_EINVAL;
+  int status = OQ_OK;
+  for (int64_t t = 0; t < T; t++) {
+    const float* last = h + ((int64_t)m * T + t) * d;
+    double v = 0.0;
+    if (indicator == 0 || indicator == 3) {
+      for (int k = 1; k <= m; k++) {
+        const float* a = h + ((int64_t)k * T + t) * d;
+        const float* b = h + ((int64_t)(k - 1) * T + t) * d;
+        if (indicator == 0) {                 /* ||h^(l) - h^(l-1)||_2 */
+          double q = 0.0;
+          for (int j = 0; j < d; j++) {
+            double e = (double)a[j] - (double)b[j];
+            q += e * e;
+          }
+          v += sqrt(q);
+        } else {                              /* 1 - cos(h^(l), h^(l-1)) */
+          double na = sqrt(dot_d(a, a, d)), nb = sqrt(dot_d(b, b, d));
+          double c = (na > 0.0 && nb > 0.0) ? dot_d(a, b, d) / (na * nb) : 0.0;
+          v += 1.0 - c;
+        }
+      }
+      v /= m;
+    } else if (indicator == 1) {
+      v = sqrt(dot_d(last, last, d));
+    } else {
+      double mean = 0.0;
+      for (int j = 0; j < d; j++) mean += last[j];
+      mean /= d;
+      for (int j = 0; j < d; j++) v += ((double)last[j] - mean) * ((double)last[j] - mean);
+      v /= d;
+    }
+    if (!isfinite(v)) status = OQ_ENAN;
+    s[t] = v;
+  }
+  return status;
+}
+
+int oq_score_kv_norm(const float* X, int R, int64_t T, double* s) {
+  if (R <= 0 || T < 0) return OQ_EINVAL;
+  for (int64_t t = 0; t < T; t++) {
+    double q = 0.0;
+    for (int r = 0; r < R; r++) q += dot_d(X + ((int64_t)r * T + t) * 128, X + ((int64_t)r * T + t) * 128, 128);
+    s[t] = sqrt(q);
+  }
+  return OQ_OK;
+}
+
+void oq_bf16_to_f32_n(const uint16_t* h, int64_t n, float* out) {
+  for (int64_t i = 0; i < n; i++) {
+    uint32_t u = (uint32_t)h[i] << 16;
+    memcpy(&out[i], &u, 4);
   }
 }
 

@@ -80,6 +80,19 @@ void oq_tq_dequant_rows(const uint8_t* codes, const uint16_t* rho, int64_t n,
 void oq_rotaffine_dequant_rows(const uint8_t* codes, const uint16_t* meta, int64_t n, int G,
                                const uint32_t* sign_words, double* out);
 
+/* Token-importance indicators (Sec. 3.3), in double.  Hidden-state family
+ * over the states h[k][t][j] of the last m+1 layers (k = 0..m, layer L-m+k;
+ * d channels): 0 delta-norm, Eq. (3): (1/m) sum_{k=1..m} ||h_k - h_{k-1}||_2;
+ * 1 norm ||h_m||_2; 2 variance (1/d) sum_j (h_m[j] - mean)^2 (population);
+ * 3 cosine-delta (1/m) sum_k (1 - cos(h_k, h_{k-1})), cos taken as 0 when a
+ * norm is 0.  m >= 1 for 0 and 3, m >= 0 otherwise.  s[T]. */
+int oq_score_hidden(int indicator, const float* h, int m, int64_t T, int d, double* s);
+/* KV-norm family: s[t] = sqrt(sum_r sum_j X[r][t][j]^2) over R rows of 128
+ * channels per token (every layer and kv head of the key or value cache). */
+int oq_score_kv_norm(const float* X, int R, int64_t T, double* s);
+/* bfloat16 bits -> binary32 (exact) */
+void oq_bf16_to_f32_n(const uint16_t* h, int64_t n, float* out);
+
 /* Decode attention (the consumer of the cache, Sec. 3.1 / Alg. 1):
  * out[h] = softmax(q_h . k_t / sqrt(D)) . v over all n tokens, in double. */
 void oq_attention(const double* q, int nq, const double* k, const double* v,
