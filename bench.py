@@ -69,6 +69,8 @@ def parse():
                     help="override an affine workload's base (rot_affine: the affine quantizer of the "
                          "Hadamard-rotated row)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-indicators", dest="indicators", action="store_false",
+                    help="skip timing the token-importance indicators")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="budget of the oracle sample")
     ap.add_argument("--no-generate", dest="generate", action="store_false",
                     help="skip the generation leg of workloads with generated tokens")
@@ -88,6 +90,39 @@ def algorithmic_decode_bytes(cfgw, n_hi, n_lo):
     units = cfgw.batch * cfgw.n_kv_heads
     qo = cfgw.batch * cfgw.n_q_heads * 128 * (2 + 4)
     return units * (n_hi * per_hi + n_lo * per_lo) + qo
+
+
+HIDDEN_DIM, LAST_M = 4096, 4      # hidden size of Llama-3.1-8B / Mistral-7B; Eq. (3) over the last 4 layers
+
+
+def indicators(cache, K, gen, dev, reps=3):
+    """Time the Sec. 3.3 indicators that produce the prompt's scores: delta-norm
+    (Eq. 3) over synthetic hidden states of the last m+1 layers, and key-norm
+    over the prompt's K of every layer.  Both read their input once (HBM)."""
+    import torch
+    import paper_2608_28911_amd as P
+    _, B, _, T, _ = K.shape
+    Hs = torch.randn((LAST_M + 1, B, T, HIDDEN_DIM), generator=gen, device=dev, dtype=torch.float32).half()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+    sc = P.score_hidden("delta_norm", Hs)
+    ev[0].record()
+    for _ in range(reps):
+        P.score_hidden("delta_norm", Hs, scores=sc)
+    ev[1].record()
+    cache.score_kv_norm(K, scores=sc)
+    ev[2].record()
+    for _ in range(reps):
+        cache.score_kv_norm(K, scores=sc)
+    ev[3].record()
+    torch.cuda.synchronize()
+    dn_us = ev[0].elapsed_time(ev[1]) / reps * 1e3
+    kn_us = ev[2].elapsed_time(ev[3]) / reps * 1e3
+    dn_bytes = Hs.numel() * 2 + B * T * 4
+    kn_bytes = K.numel() * 2 + B * T * 4
+    del Hs
+    return {"delta_norm_us": round(dn_us, 1), "delta_norm_gbps": round(dn_bytes / (dn_us * 1e-6) / 1e9, 1),
+            "key_norm_us": round(kn_us, 1), "key_norm_gbps": round(kn_bytes / (kn_us * 1e-6) / 1e9, 1),
+            "hidden_dim": HIDDEN_DIM, "m": LAST_M}
 
 
 def cpu_baseline(cfgw, seconds):
@@ -289,6 +324,7 @@ def main():
     n_hi, n_lo = cache.c.n_hi, cache.c.n_lo
     t_hi, t_lo = -(-n_hi // 64), -(-n_lo // 64)
     quant_bytes = 2 * K.numel() * 2 + nL * B * H * (t_hi * cache.sz.record_bytes_hi + t_lo * cache.sz.record_bytes_lo)
+    ind = indicators(cache, K, gen, dev) if args.indicators else None
     del K, V
     torch.cuda.empty_cache()
 
@@ -369,6 +405,8 @@ def main():
                      "traffic": measured_traffic() if cfgw.name == "llama8b_kv_b1_t32768_affine" else None,
                      "kernel": "decode_kernel", "bytes_per_launch": int(alg)},
     }
+    if ind is not None:
+        line["indicators"] = ind
     if args.generate and cfgw.n_gen > 0:
         del q
         line["generation"] = generation(cfgw, cache, gen, dev, outlier_ch)

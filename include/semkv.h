@@ -206,6 +206,35 @@ int semkv_append_decode(semkv_cache* c, int32_t layer, const uint16_t* k_new, co
                         const uint16_t* q, float* out, void* workspace, size_t ws_bytes,
                         hipStream_t stream);
 
+/* Token-importance indicators (Sec. 3.3): device fp32 scores [batch][T] for
+ * semkv_rank (which uses only their order), from tensors the model already
+ * computes.  Hidden-state family, over the hidden states of the last m+1
+ * layers (state k = layer L-m+k, k = 0..m):
+ *   SEMKV_IND_DELTA_NORM    Eq. (3): (1/m) sum_{k=1..m} ||h_k - h_{k-1}||_2 (m >= 1)
+ *   SEMKV_IND_NORM          ||h_m||_2
+ *   SEMKV_IND_VARIANCE      (1/d) sum_j (h_m[j] - mean)^2 (population variance)
+ *   SEMKV_IND_COSINE_DELTA  (1/m) sum_k (1 - cos(h_k, h_{k-1})), cos = 0 when a
+ *                           state is all zero (m >= 1)
+ * hidden: device, fp16 (SEMKV_DTYPE_F16) or bfloat16 (SEMKV_DTYPE_BF16);
+ * element (k, b, t, j) at k*s_state + b*s_batch + t*s_token + j (elements;
+ * the norm and variance read state m only, m may be 0).  d_model: a multiple
+ * of 8, at most 8192; strides multiples of 8; hidden 16-byte aligned.
+ * Sums run in fp32 (the score's relative error is below 1e-5 for d <= 8192).
+ * A non-finite state gives a non-finite score, which semkv_rank reports. */
+enum { SEMKV_IND_DELTA_NORM = 0, SEMKV_IND_NORM = 1, SEMKV_IND_VARIANCE = 2, SEMKV_IND_COSINE_DELTA = 3 };
+enum { SEMKV_DTYPE_F16 = 0, SEMKV_DTYPE_BF16 = 1 };
+int semkv_score_hidden(int32_t indicator, const void* hidden, int32_t dtype, int32_t m, int32_t batch,
+                       int64_t T, int32_t d_model, int64_t s_state, int64_t s_batch, int64_t s_token,
+                       float* scores, hipStream_t stream);
+
+/* KV-norm family (Sec. 3.3: key-norm ||K_t||_2, value-norm ||V_t||_2): the
+ * norm of token t's rows over every layer and kv head of `c`, from the fp16 K
+ * (or V) tensors laid out as for semkv_quantize_pack with layer == -1:
+ * element (l, b, h, t, j) at l*sL + b*sB + h*sH + t*sT + j.  scores: device
+ * fp32 [batch][T]. */
+int semkv_score_kv_norm(const semkv_cache* c, const uint16_t* X, int64_t sL, int64_t sB, int64_t sH,
+                        int64_t sT, int64_t T, float* scores, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

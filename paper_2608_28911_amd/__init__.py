@@ -11,7 +11,11 @@ import numpy as np
 from . import _abi
 from ._abi import BASE_AFFINE, BASE_ROT_AFFINE, BASE_TQ, SemKVError, check, lib
 
-__all__ = ["SemKVCache", "SemKVError", "BASE_AFFINE", "BASE_TQ", "BASE_ROT_AFFINE", "tq_codebook", "cache_sizes"]
+__all__ = ["SemKVCache", "SemKVError", "BASE_AFFINE", "BASE_TQ", "BASE_ROT_AFFINE", "tq_codebook", "cache_sizes",
+           "score_hidden", "INDICATORS"]
+
+INDICATORS = {"delta_norm": _abi.IND_DELTA_NORM, "norm": _abi.IND_NORM, "variance": _abi.IND_VARIANCE,
+              "cosine_delta": _abi.IND_COSINE_DELTA}
 
 
 def _stream():
@@ -42,6 +46,23 @@ def tq_codebook(L):
     tau = np.zeros(16, np.float32)
     check(lib().semkv_tq_codebook(L, mu.ctypes.data, tau.ctypes.data), "semkv_tq_codebook")
     return mu[:L].copy(), tau[:L - 1].copy()
+
+
+def score_hidden(indicator, hidden, scores=None):
+    """Sec. 3.3 hidden-state indicator on the device.  hidden: fp16 or bf16
+    [m+1, B, T, d] (any strides with a unit channel stride), state k = layer
+    L-m+k; indicator: a name of INDICATORS or its code.  Returns fp32 [B, T]."""
+    import torch
+    code = INDICATORS[indicator] if isinstance(indicator, str) else int(indicator)
+    assert hidden.dim() == 4 and hidden.stride(3) == 1
+    dt = {torch.float16: _abi.DTYPE_F16, torch.bfloat16: _abi.DTYPE_BF16}[hidden.dtype]
+    n, B, T, d = hidden.shape
+    if scores is None:
+        scores = torch.empty((B, T), dtype=torch.float32, device=hidden.device)
+    st = hidden.stride()
+    check(lib().semkv_score_hidden(code, _ptr(hidden), dt, n - 1, B, T, d, st[0], st[1], st[2], _ptr(scores),
+                                   _stream()), "semkv_score_hidden")
+    return scores
 
 
 class SemKVCache:
@@ -92,6 +113,19 @@ class SemKVCache:
         T = K.shape[-2]
         check(lib().semkv_quantize_pack(ctypes.byref(self.c), layer, _ptr(K), _ptr(V), sL, sB, sH, sT, T,
                                         _ptr(hi_idx), _ptr(lo_idx), _stream()), "semkv_quantize_pack")
+
+    def score_kv_norm(self, X, scores=None):
+        """Key-norm (X = K) or value-norm (X = V) of every token: X fp16
+        [n_layers, B, H_kv, T, 128] -> fp32 [B, T] (Sec. 3.3)."""
+        import torch
+        assert X.dtype == torch.float16 and X.dim() == 5 and X.stride(4) == 1
+        T = X.shape[3]
+        if scores is None:
+            scores = torch.empty((self.cfg.batch, T), dtype=torch.float32, device=X.device)
+        st = X.stride()
+        check(lib().semkv_score_kv_norm(ctypes.byref(self.c), _ptr(X), st[0], st[1], st[2], st[3], T,
+                                        _ptr(scores), _stream()), "semkv_score_kv_norm")
+        return scores
 
     def append_kv(self, layer, k, v):
         check(lib().semkv_append_kv(ctypes.byref(self.c), layer, _ptr(k.contiguous()), _ptr(v.contiguous()),

@@ -12,6 +12,8 @@ SEMKV_OK, SEMKV_EINVAL, SEMKV_EUNSUPPORTED, SEMKV_ECAPACITY, SEMKV_ENAN, SEMKV_E
     0, -1, -2, -3, -4, -5, -6
 BASE_AFFINE, BASE_TQ, BASE_ROT_AFFINE = 0, 1, 2
 STATUS_NAN_SCORE, STATUS_NONFINITE_KV = 1, 2
+IND_DELTA_NORM, IND_NORM, IND_VARIANCE, IND_COSINE_DELTA = 0, 1, 2, 3
+DTYPE_F16, DTYPE_BF16 = 0, 1
 
 
 class Config(ctypes.Structure):
@@ -51,6 +53,8 @@ EXPORTS = {
     "semkv_workspace_bytes": (ctypes.c_int, [ctypes.POINTER(Cache), ctypes.POINTER(sz)]),
     "semkv_decode_attn": (ctypes.c_int, [ctypes.POINTER(Cache), i32, vp, vp, vp, sz, vp]),
     "semkv_append_decode": (ctypes.c_int, [ctypes.POINTER(Cache), i32, vp, vp, vp, vp, vp, sz, vp]),
+    "semkv_score_hidden": (ctypes.c_int, [i32, vp, i32, i32, i32, i64, i32, i64, i64, i64, vp, vp]),
+    "semkv_score_kv_norm": (ctypes.c_int, [ctypes.POINTER(Cache), vp, i64, i64, i64, i64, i64, vp, vp]),
 }
 
 _lib = None

@@ -25,6 +25,7 @@ SOURCES = {
     "rank.hip": ["-ffp-contract=off"],
     "quant.hip": ["-ffp-contract=off"],
     "decode.hip": [],
+    "score.hip": ["-ffp-contract=off"],
 }
 
 

@@ -446,4 +446,47 @@ int semkv_append_decode(semkv_cache* c, int32_t layer, const uint16_t* k_new, co
   return SEMKV_OK;
 }
 
+int semkv_score_hidden(int32_t indicator, const void* hidden, int32_t dtype, int32_t m, int32_t batch,
+                       int64_t T, int32_t d_model, int64_t s_state, int64_t s_batch, int64_t s_token,
+                       float* scores, hipStream_t stream) {
+  if (!hidden || !scores || batch < 1 || T < 1 || m < 0) return SEMKV_EINVAL;
+  if (indicator < SEMKV_IND_DELTA_NORM || indicator > SEMKV_IND_COSINE_DELTA) return SEMKV_EINVAL;
+  if (dtype != SEMKV_DTYPE_F16 && dtype != SEMKV_DTYPE_BF16) return SEMKV_EINVAL;
+  if ((indicator == SEMKV_IND_DELTA_NORM || indicator == SEMKV_IND_COSINE_DELTA) && m < 1) return SEMKV_EINVAL;
+  if (d_model < 8 || d_model % 8) return SEMKV_EINVAL;
+  if (d_model > 8192) return SEMKV_EUNSUPPORTED;
+  if ((uintptr_t(hidden) & 15) || (uintptr_t(scores) & 3) || ((s_state | s_batch | s_token) & 7)) return SEMKV_EINVAL;
+  HiddenArgs a;
+  a.h = static_cast<const uint16_t*>(hidden);
+  a.s_state = s_state;
+  a.s_batch = s_batch;
+  a.s_token = s_token;
+  a.indicator = indicator;
+  a.dtype = dtype;
+  a.m = m;
+  a.batch = batch;
+  a.d = d_model;
+  a.T = T;
+  a.scores = scores;
+  return launch_score_hidden(a, stream);
+}
+
+int semkv_score_kv_norm(const semkv_cache* c, const uint16_t* X, int64_t sL, int64_t sB, int64_t sH,
+                        int64_t sT, int64_t T, float* scores, hipStream_t stream) {
+  if (!c || !X || !scores || T < 1) return SEMKV_EINVAL;
+  if ((uintptr_t(X) & 15) || (uintptr_t(scores) & 3) || ((sL | sB | sH | sT) & 7) || sT < 128) return SEMKV_EINVAL;
+  KvNormArgs a;
+  a.X = X;
+  a.sL = sL;
+  a.sB = sB;
+  a.sH = sH;
+  a.sT = sT;
+  a.n_layers = c->cfg.n_layers;
+  a.n_kv_heads = c->cfg.n_kv_heads;
+  a.batch = c->cfg.batch;
+  a.T = T;
+  a.scores = scores;
+  return launch_kv_norm(a, stream);
+}
+
 }  // extern "C"

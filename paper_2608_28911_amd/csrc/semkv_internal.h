@@ -76,6 +76,22 @@ struct DecodeArgs {
   float mu[2][16];         // tq codebooks
 };
 
+struct HiddenArgs {
+  const uint16_t* h;       // state k, sequence b, token t at k*s_state + b*s_batch + t*s_token
+  int64_t s_state, s_batch, s_token;
+  int32_t indicator, dtype, m, batch, d;
+  int64_t T;
+  float* scores;           // [batch][T]
+};
+
+struct KvNormArgs {
+  const uint16_t* X;       // (l, b, h, t, :) at l*sL + b*sB + h*sH + t*sT
+  int64_t sL, sB, sH, sT;
+  int32_t n_layers, n_kv_heads, batch;
+  int64_t T;
+  float* scores;           // [batch][T]
+};
+
 constexpr int kPartial = 132;  // m, l, 2 pad, o[128]
 constexpr int kMaxSplits = 256;   // splits per (sequence, kv head)
 
@@ -84,6 +100,8 @@ int launch_quantize(const QuantArgs& a, hipStream_t s);
 int launch_append(const AppendArgs& a, hipStream_t s);
 int launch_close(const CloseArgs& a, hipStream_t s);
 int launch_decode(const DecodeArgs& a, hipStream_t s);
+int launch_score_hidden(const HiddenArgs& a, hipStream_t s);
+int launch_kv_norm(const KvNormArgs& a, hipStream_t s);
 // decode workgroups one compute unit holds at once for this cache's kernel,
 // and the waves of one such workgroup (a wave takes every NW-th tile of a run)
 int decode_blocks_per_cu(int base, int L_hi, int L_lo, int G);
