@@ -254,6 +254,120 @@ def generation(cfgw, cache, gen, dev, outlier_ch):
     }
 
 
+def multiturn(args, cfgw):
+    """A dialogue at the multi-turn operating point (Sec. 3.7, Sec. 4.6): each
+    turn resets the cache, ranks and quantizes the accumulated conversation
+    (rank + quantize/pack of every layer), then generates its answer (per
+    token: fused append + decode of every layer, commit; block closes) and
+    flushes the residual block.  The whole dialogue is captured as HIP graphs
+    (per turn: the prefill, each 64-token block, the residual + flush) and
+    replayed in order under events.  One JSON line: generated tokens/s over
+    the dialogue, with each turn's prefill and generation times."""
+    import torch
+    import paper_2608_28911_amd as P
+    from workloads import synth
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    B, H, Hq, nL, blk = cfgw.batch, cfgw.n_kv_heads, cfgw.n_q_heads, cfgw.n_layers, cfgw.block
+    plan = cfgw.turn_plan()
+    n_all, n_gen = cfgw.conversation_len, sum(g for _, g in plan)
+    cfg = P.make_config(n_layers=nL, n_kv_heads=H, batch=B, base=cfgw.base_id, L_hi=cfgw.L_hi, L_lo=cfgw.L_lo,
+                        group=cfgw.group, r_num=cfgw.r_num, r_den=cfgw.r_den,
+                        max_prompt=max(p for p, _ in plan), max_new=max(g for _, g in plan))
+    cache = P.SemKVCache(cfg, sign_words=synth.all_sign_words(cfgw) if cfgw.rotated else None)
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(cfgw.seed)
+    K = torch.randn((nL, B, H, n_all, 128), generator=gen, device=dev).half()
+    V = torch.randn((nL, B, H, n_all, 128), generator=gen, device=dev).half()
+    kn = K.permute(3, 0, 1, 2, 4).contiguous()      # [token][layer][b][kvh][128]: one step's rows together
+    vn = V.permute(3, 0, 1, 2, 4).contiguous()
+    qg = torch.randn((n_gen, nL, B, Hq, 128), generator=gen, device=dev).half()
+    out = torch.empty((nL, B, Hq, 128), dtype=torch.float32, device=dev)
+    ws = cache.workspace()
+    scores = [torch.from_numpy(synth.turn_scores(cfgw, t, p)).to(dev) for t, (p, _) in enumerate(plan)]
+    gsc = [torch.from_numpy(synth.turn_gen_scores(cfgw, t, g)).to(dev) for t, (_, g) in enumerate(plan)]
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    torch.cuda.synchronize()
+    turns, step = [], 0
+    with torch.cuda.stream(s):
+        for t, (p, g) in enumerate(plan):
+            gp = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(gp, stream=s):
+                cache.reset()
+                hi, lo = cache.rank(scores[t])
+                cache.quantize_pack(-1, K[:, :, :, :p], V[:, :, :, :p], hi, lo)
+            gens = []
+            for b0 in range(0, g, blk):
+                gg = torch.cuda.CUDAGraph()
+                with torch.cuda.graph(gg, stream=s):
+                    for i in range(b0, min(g, b0 + blk)):
+                        for l in range(nL):
+                            cache.append_decode_attn(l, kn[p + i, l], vn[p + i, l], qg[step, l], out=out[l],
+                                                     workspace=ws)
+                        cache.append_commit(gsc[t][i])
+                        step += 1
+                    if b0 + blk >= g:
+                        cache.flush()
+                gens.append(gg)
+            turns.append((p, g, gp, gens, hi, lo))
+    torch.cuda.synchronize()
+    for _ in range(args.warmup and 1):          # one untimed pass of the whole dialogue
+        for _, _, gp, gens, _, _ in turns:
+            gp.replay()
+            for gg in gens:
+                gg.replay()
+    torch.cuda.synchronize()
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in turns]
+    for (_, _, gp, gens, _, _), (e0, e1, e2) in zip(turns, ev):
+        e0.record()
+        gp.replay()
+        e1.record()
+        for gg in gens:
+            gg.replay()
+        e2.record()
+    torch.cuda.synchronize()
+    assert cache.status() == 0, "device status word %d" % cache.status()
+    per = [{"prompt": p, "generated": g, "prefill_ms": round(e0.elapsed_time(e1), 3),
+            "gen_ms_per_token": round(e1.elapsed_time(e2) / g, 4)}
+           for (p, g, *_), (e0, e1, e2) in zip(turns, ev)]
+    total_ms = sum(e0.elapsed_time(e2) for e0, _, e2 in ev)
+    gen_ms = sum(e1.elapsed_time(e2) for _, e1, e2 in ev)
+    # decode traffic of the dialogue: every generated token reads, per layer,
+    # the turn's quantized rows (packed) and its fp16 tail
+    from paper_2608_28911_amd.fmt import line_bits
+    meta = (128 // cfgw.group) * 4 if cfgw.base != "tq" else 2
+    per_hi = 2 * line_bits(cfgw.L_hi, 128) / 8 + 2 * meta
+    per_lo = 2 * line_bits(cfgw.L_lo, 128) / 8 + 2 * meta
+    dec_bytes = 0.0
+    from fractions import Fraction
+    for p, g in plan:
+        kh = p * cfgw.r_num // cfgw.r_den
+        n_hi, n_lo = kh, p - kh
+        for i in range(g):
+            if i and i % blk == 0:
+                kb = round(Fraction(cfgw.r_num * blk, cfgw.r_den))
+                n_hi, n_lo = n_hi + kb, n_lo + blk - kb
+            dec_bytes += nL * B * H * (n_hi * per_hi + n_lo * per_lo + (i % blk + 1) * 512)
+    achieved = dec_bytes / (gen_ms * 1e-3) / 1e9
+    tokens_per_s = B * n_gen / (total_ms * 1e-3)
+    line = {
+        "metric": "multi-turn dialogue: generated tokens/s incl. each turn's re-prefill (rank + quantize/pack)",
+        "value": round(tokens_per_s, 2), "unit": "tokens/s", "n_gpus": 1, "steps": n_gen, "warmup": 1,
+        "ms_per_step": round(total_ms / n_gen, 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f16", "data": "synthetic",
+        "config": {"workload": cfgw.name, "layers": nL, "batch": B, "kv_heads": H, "q_heads": Hq,
+                   "head_dim": 128, "base": cfgw.base, "levels": [cfgw.L_hi, cfgw.L_lo],
+                   "r": cfgw.r_num / cfgw.r_den, "group": cfgw.group, "turns": [list(x) for x in cfgw.turns]},
+        "turns": per, "dialogue_ms": round(total_ms, 3),
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None, "kernel": "decode_kernel",
+                     "note": "decode bytes of every generated token over the generation replays (commits and "
+                             "closes included in the time)"},
+    }
+    print(json.dumps(line), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -265,6 +379,8 @@ def main():
     from workloads import get_config, synth
 
     cfgw = get_config(args.workload)
+    if cfgw.turns:
+        return multiturn(args, cfgw)
     if args.group or args.base:
         from dataclasses import replace
         if args.base and cfgw.base == "tq":

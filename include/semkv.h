@@ -179,6 +179,15 @@ int semkv_append_commit(semkv_cache* c, const float* score_new, hipStream_t stre
  * round(r*n) high-precision tokens (nearest integer, ties to even). */
 int semkv_flush(semkv_cache* c, hipStream_t stream);
 
+/* Empty the cache for a new prompt: clear the flag bitmap (a kernel on
+ * `stream`) and every host-side count; pools, tail and status word are left
+ * as they are (their contents are rewritten before they are read again).
+ * Multi-turn dialogue (Sec. 3.7, Sec. 4.6): each turn resets the cache and
+ * applies the prompt procedure to the accumulated conversation (semkv_rank +
+ * semkv_quantize_pack), then block-exact generation and semkv_flush at the
+ * turn's end. */
+int semkv_cache_reset(semkv_cache* c, hipStream_t stream);
+
 /* Bytes of workspace semkv_decode_attn needs for this cache's current counts
  * (semkv_sizes.workspace_bytes bounds it for every count). */
 int semkv_workspace_bytes(const semkv_cache* c, size_t* bytes);

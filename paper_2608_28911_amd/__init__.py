@@ -138,6 +138,10 @@ class SemKVCache:
     def flush(self):
         check(lib().semkv_flush(ctypes.byref(self.c), _stream()), "semkv_flush")
 
+    def reset(self):
+        """Empty the cache for a new prompt (a multi-turn dialogue's next turn)."""
+        check(lib().semkv_cache_reset(ctypes.byref(self.c), _stream()), "semkv_cache_reset")
+
     def workspace_bytes(self):
         n = ctypes.c_size_t()
         check(lib().semkv_workspace_bytes(ctypes.byref(self.c), ctypes.byref(n)), "semkv_workspace_bytes")

@@ -50,6 +50,7 @@ EXPORTS = {
     "semkv_append_kv": (ctypes.c_int, [ctypes.POINTER(Cache), i32, vp, vp, vp]),
     "semkv_append_commit": (ctypes.c_int, [ctypes.POINTER(Cache), vp, vp]),
     "semkv_flush": (ctypes.c_int, [ctypes.POINTER(Cache), vp]),
+    "semkv_cache_reset": (ctypes.c_int, [ctypes.POINTER(Cache), vp]),
     "semkv_workspace_bytes": (ctypes.c_int, [ctypes.POINTER(Cache), ctypes.POINTER(sz)]),
     "semkv_decode_attn": (ctypes.c_int, [ctypes.POINTER(Cache), i32, vp, vp, vp, sz, vp]),
     "semkv_append_decode": (ctypes.c_int, [ctypes.POINTER(Cache), i32, vp, vp, vp, vp, vp, sz, vp]),

@@ -163,6 +163,12 @@ __global__ void store_score_kernel(float* dst, const float* src, int slot, int b
   if (b < batch) dst[b * kSlots + slot] = src[b];
 }
 
+// zero n words (a kernel, not a memset node, so that a captured graph replays it)
+__global__ void zero_words_kernel(uint32_t* p, int64_t n) {
+  for (int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < n; i += int64_t(gridDim.x) * blockDim.x)
+    p[i] = 0u;
+}
+
 }  // namespace
 
 extern "C" {
@@ -376,6 +382,20 @@ int semkv_append_commit(semkv_cache* c, const float* score_new, hipStream_t stre
   c->n_scored += 1;
   memset(c->appended, 0, sizeof(c->appended));
   if (c->n_scored == kSlots) return close_block(c, kSlots, stream);
+  return SEMKV_OK;
+}
+
+int semkv_cache_reset(semkv_cache* c, hipStream_t stream) {
+  if (!c || !c->flags) return SEMKV_EINVAL;
+  const int64_t n = int64_t(c->cfg.batch) * c->sz.flag_words;
+  const int64_t blocks = (n + 255) / 256 < 1024 ? (n + 255) / 256 : 1024;
+  hipLaunchKernelGGL(zero_words_kernel, dim3(unsigned(blocks)), dim3(256), 0, stream, c->flags, n);
+  if (hipGetLastError() != hipSuccess) return SEMKV_EHIP;
+  c->n_prompt = 0;
+  c->n_hi = 0;
+  c->n_lo = 0;
+  c->n_scored = 0;
+  memset(c->appended, 0, sizeof(c->appended));
   return SEMKV_OK;
 }
 

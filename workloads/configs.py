@@ -30,11 +30,27 @@ class WorkloadConfig:
     score_dist: str = "zipf" # "zipf" | "dirichlet"
     outliers: int = 4        # key channels scaled x10 per (layer, kv head)
     outlier_scale: float = 10.0
+    turns: tuple = ()        # multi-turn dialogue: ((user tokens, generated tokens), ...)
     note: str = ""
 
     @property
     def gqa(self) -> int:
         return self.n_q_heads // self.n_kv_heads
+
+    def turn_plan(self):
+        """Per turn of a dialogue: (accumulated prompt length P_k, generated
+        tokens g_k).  Turn k's prompt is the conversation so far plus the new
+        user tokens; its answer follows it."""
+        plan, n = [], 0
+        for user, gen in self.turns:
+            n += user
+            plan.append((n, gen))
+            n += gen
+        return plan
+
+    @property
+    def conversation_len(self) -> int:
+        return sum(u + g for u, g in self.turns)
 
     @property
     def base_id(self) -> int:
@@ -77,6 +93,13 @@ CONFIGS = [
         n_q_heads=32, head_dim=128, batch=1, prompt_len=131072, n_gen=0,
         decode_steps=64, base="tq", L_hi=4, L_lo=3, group=128, r_num=40,
         r_den=100, note="TurboQuant-MSE base, 4/3 Lloyd-Max levels"),
+    WorkloadConfig(
+        name="llama8b_kv_b4_multiturn4_r35", seed=5, n_layers=32, n_kv_heads=8,
+        n_q_heads=32, head_dim=128, batch=4, prompt_len=4352, n_gen=256,
+        decode_steps=1024, base="affine", L_hi=6, L_lo=5, group=128, r_num=35,
+        r_den=100, turns=((2048, 256), (512, 256), (512, 256), (512, 256)),
+        note="multi-turn operating point (2.41 code bits): each turn re-ranks and quantizes the "
+             "accumulated conversation, generates block-exactly and flushes its residual block"),
 ]
 
 

@@ -11,7 +11,7 @@ import numpy as np
 from .configs import WorkloadConfig
 
 # stream identifiers (part of the seed key)
-S_K, S_V, S_OUTLIER, S_SCORE, S_Q, S_SIGN, S_GEN_K, S_GEN_V, S_GEN_SCORE = range(1, 10)
+S_K, S_V, S_OUTLIER, S_SCORE, S_Q, S_SIGN, S_GEN_K, S_GEN_V, S_GEN_SCORE, S_TURN_SCORE, S_TURN_GEN = range(1, 12)
 
 
 def _rng(*key):
@@ -112,3 +112,25 @@ def gen_scores(cfg: WorkloadConfig, n: int | None = None) -> np.ndarray:
         else:
             out[:, b] = rng.random(n, dtype=np.float32)
     return out
+
+
+# -------------------------------------------------------- multi-turn dialogue
+
+def conversation_kv(cfg: WorkloadConfig, layer: int, b: int, kvh: int):
+    """K and V rows of a whole dialogue (every turn's user tokens and answers,
+    in order) of one unit: two fp16 [conversation_len, D]; a turn's prompt is
+    a prefix, its answer the rows after it."""
+    return unit_kv(cfg, layer, b, kvh, cfg.conversation_len)
+
+
+def turn_scores(cfg: WorkloadConfig, turn: int, T: int) -> np.ndarray:
+    """Scores of the accumulated prompt of a turn (re-scored every turn, as a
+    fresh prefill would): float32 [B, T], integer Zipf(1.1) draws."""
+    return np.stack([_rng(cfg.seed, S_TURN_SCORE, turn, b).zipf(1.1, T).astype(np.float32)
+                     for b in range(cfg.batch)])
+
+
+def turn_gen_scores(cfg: WorkloadConfig, turn: int, n: int) -> np.ndarray:
+    """Scores of a turn's generated tokens: float32 [n, B]."""
+    return np.stack([_rng(cfg.seed, S_TURN_GEN, turn, b).zipf(1.1, n).astype(np.float32)
+                     for b in range(cfg.batch)], axis=1)
