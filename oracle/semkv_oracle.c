@@ -114,7 +114,7 @@ int oq_rank_k(const float* s, int64_t T, int64_t k, uint8_t* flag) {
 /* ------------------------------------------------------ affine quantizer -- */
 
 int oq_affine_row(const uint16_t* x, int L, int G, uint8_t* codes, uint16_t* meta) {
-  if (L < 3 || L > 16 || G <= 0 || 128 % G) return OQ_EINVAL;
+  if (L < 2 || L > 16 || G <= 0 || 128 % G) return OQ_EINVAL;
   int status = OQ_OK;
   for (int g = 0; g < 128 / G; g++) {
     float mn = INFINITY, mx = -INFINITY;
@@ -303,7 +303,8 @@ int oq_symbol_digits(int L) {
     case 5: return 3;   /* 5^3 = 125 <= 2^7   : 2.333 b/value */
     case 6: return 5;   /* 6^5 = 7776 <= 2^13 : 2.600 b/value */
     case 2: return 8;   /* 2^8 = 256          : 1.000 b/value */
-    case 8: return 1;   /* 8 <= 2^3           : 3.000 b/value */
+    case 7: return 7;   /* 7^7 = 823543 <= 2^20 : 2.857 b/value (the paper gives no 7-level packing) */
+    case 8: return 2;   /* 8^2 = 64 = 2^6     : 3.000 b/value */
     case 16: return 2;  /* 16^2 = 256 = 2^8   : 4.000 b/value */
     default: return 0;
   }

@@ -9,7 +9,7 @@ kernels).  Format (mixed-radix packing, Sec. 4.1):
   the 64 slots of a tile; segment j of a line is its symbols p = j, j+4, ...;
 * a body is segment 0 of every line, then segment 1, 2, 3, bits LSB-first.
 """
-DIGITS = {2: 8, 3: 5, 4: 4, 5: 3, 6: 5, 8: 1, 16: 2}
+DIGITS = {2: 8, 3: 5, 4: 4, 5: 3, 6: 5, 7: 7, 8: 2, 16: 2}
 
 
 def sym_bits(L, n):

@@ -11,7 +11,7 @@ from tests import formatref as F
 GOLD = os.path.join(os.path.dirname(__file__), "golden")
 
 
-@pytest.mark.parametrize("L", [2, 3, 4, 5, 6, 8, 16])
+@pytest.mark.parametrize("L", [2, 3, 4, 5, 6, 7, 8, 16])
 def test_symbol_rates_and_bounds(L):
     n = O.symbol_digits(L)
     assert n == F.DIGITS[L]
@@ -20,7 +20,7 @@ def test_symbol_rates_and_bounds(L):
     assert {5: (3, 7), 6: (5, 13)}.get(L, (n, w)) == (n, w)   # 3 in 7 bits, 5 in 13 bits
 
 
-@pytest.mark.parametrize("L", [2, 3, 4, 5, 6, 8, 16])
+@pytest.mark.parametrize("L", [2, 3, 4, 5, 6, 7, 8, 16])
 @pytest.mark.parametrize("seed", [0, 1])
 def test_pack_roundtrip_bigint(L, seed):
     rng = np.random.default_rng(seed * 100 + L)
@@ -37,6 +37,12 @@ def test_pack_roundtrip_bigint(L, seed):
 
 def test_tile_sizes():
     assert [O.tile_bytes(L) for L in (3, 4, 5, 6)] == [1648, 2048, 2400, 2672]
+    # the uniform-grid levels: 8 codes per byte (1 bit), two 8-level codes in
+    # 6 bits (3 bits), seven 7-level codes in 20 bits (2.857 bits, 1.8 % over log2 7)
+    assert O.line_bits(2, 128) == 128 and O.line_bits(8, 128) == 384
+    assert O.line_bits(7, 128) == 18 * 20 + 6 and O.line_bits(7, 64) == 9 * 20 + 3
+    assert [O.tile_bytes(L) for L in (2, 7, 8)] == [1024, 2928, 3072]
+    assert abs(20 / 7 / np.log2(7) - 1 - 0.0177) < 1e-3
     assert O.line_bits(6, 128) == 25 * 13 + 8 and O.line_bits(5, 128) == 42 * 7 + 5
     assert O.line_bits(4, 128) == 256 and O.line_bits(3, 128) == 25 * 8 + 5
 

@@ -23,7 +23,7 @@ def nearest_grid(x, z, s, L):
     return k.astype(np.int64), frac
 
 
-@pytest.mark.parametrize("L", [3, 5, 6, 16])
+@pytest.mark.parametrize("L", [2, 3, 5, 6, 7, 8, 16])
 @pytest.mark.parametrize("G", [32, 128])
 def test_affine_matches_nearest_grid_point(L, G):
     rng = np.random.default_rng(L * 1000 + G)
@@ -56,7 +56,7 @@ def test_affine_matches_nearest_grid_point(L, G):
     assert np.all(codes[0] == 0) and np.all(meta[0, :, 0] == 0)
 
 
-@pytest.mark.parametrize("L", [3, 5, 6])
+@pytest.mark.parametrize("L", [2, 3, 5, 6, 7, 8])
 def test_affine_exhaustive_fp16_in_range(L):
     h = np.arange(0, 65536, dtype=np.uint32).astype(np.uint16)
     v = h.view(np.float16)
