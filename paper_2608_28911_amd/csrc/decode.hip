@@ -67,7 +67,7 @@ template <int BASE, int L>
 struct Traits {
   static constexpr int n = sym_digits(L);
   static constexpr int P = (BASE == 1 && L == 4) ? 2 : 1;   // MFMA slots per code
-  static constexpr int STRIDE = (L == 5 || (L == 4 && BASE != 1)) ? 4 : 8;
+  static constexpr int STRIDE = (L == 5 || L == 8 || (L == 4 && BASE != 1)) ? 4 : 8;
   static constexpr int SPC = 16 / STRIDE;
   static constexpr int EDW = STRIDE / 4;                     // operand dwords per symbol
   static constexpr int SK = num_syms(L, kD), SV = num_syms(L, kSlots);
@@ -78,9 +78,12 @@ struct Traits {
   static constexpr int KSEGW = (NSK * W + 31) / 32;          // normalized dwords of a K segment
   static constexpr int VSEGW = (NSV * W + 31) / 32;
   // decode table: symbol -> operand dwords of digit bytes.  L = 6 splits a
-  // symbol into s mod 216 (3 codes) and s div 216 (2 codes), one dword each.
-  static constexpr int TED = L == 6 ? 1 : EDW;               // dwords per table entry
-  static constexpr int NENT = L == 6 ? 216 + 36 : ipow(L, n);   // entries (L = 6: both parts)
+  // symbol into s mod 216 (3 codes) and s div 216 (2 codes), L = 7 into
+  // s mod 2401 (4 codes) and s div 2401 (3 codes), one dword each.
+  static constexpr bool SPLIT = L == 6 || L == 7;
+  static constexpr int DIV = L == 6 ? 216 : L == 7 ? 2401 : 1;  // the split's divisor
+  static constexpr int TED = SPLIT ? 1 : EDW;                // dwords per table entry
+  static constexpr int NENT = SPLIT ? DIV + ipow(L, n) / DIV : ipow(L, n);   // entries (split: both parts)
   static constexpr int LUTDW = NENT * TED;                   // dwords of one copy
 };
 
@@ -90,7 +93,9 @@ __host__ __device__ constexpr int slot_digit(int w) {
        : L == 6 ? (w < 3 ? w : (w == 4 || w == 5) ? w - 1 : -1)
        : L == 5 ? (w < 3 ? w : -1)
        : L == 3 ? (w < 5 ? w : -1)
-       : w;                                                  // affine L = 4
+       : L == 7 ? (w < 7 ? w : -1)
+       : L == 8 ? (w < 2 ? w : -1)
+       : w;                                                  // affine L = 4, L = 2
 }
 template <int BASE, int L>
 __host__ __device__ constexpr int slot_plane(int w) { return (BASE == 1 && L == 4) ? w % 2 : 0; }
@@ -109,7 +114,8 @@ __host__ __device__ constexpr bool digit_slot_inverts() {
   return true;
 }
 static_assert(digit_slot_inverts<0, 6>() && digit_slot_inverts<0, 5>() && digit_slot_inverts<0, 4>() &&
-              digit_slot_inverts<0, 3>() && digit_slot_inverts<1, 4>() && digit_slot_inverts<1, 3>(), "slots");
+              digit_slot_inverts<0, 3>() && digit_slot_inverts<1, 4>() && digit_slot_inverts<1, 3>() &&
+              digit_slot_inverts<0, 2>() && digit_slot_inverts<0, 7>() && digit_slot_inverts<0, 8>(), "slots");
 
 // floor(s / L^i) for every symbol s < L^n as (s*2^8 * M) >> 32 with
 // M = ceil(2^24 / L^i): one 24-bit high multiply.
@@ -168,6 +174,10 @@ __host__ __device__ constexpr uint32_t entry_dword(uint32_t E) {
     const bool hi = E >= 216;
     const uint32_t v = hi ? E - 216 : E;
     return hi ? (v % 6) | ((v / 6) << 8) : (v % 6) | ((v / 6 % 6) << 8) | ((v / 36) << 16);
+  } else if constexpr (L == 7) {                             // s mod 2401: 4 codes; s div 2401: 3 codes
+    const bool hi = E >= 2401;
+    const uint32_t v = hi ? E - 2401 : E;
+    return (v % 7) | ((v / 7 % 7) << 8) | ((v / 49 % 7) << 16) | (hi ? 0u : (v / 343) << 24);
   } else {
     uint32_t w = 0;
 #pragma unroll
@@ -193,12 +203,19 @@ __host__ __device__ constexpr bool entries_match_digits() {
   for (int E = 0; E < nent; ++E) {
     for (int w = 0; w < Tr::STRIDE; ++w) {
       uint32_t byte = 0, want = 0;
-      if (L == 6) {
+      if (Tr::SPLIT) {
+        // the low part's entry gives the first digits (3 of base 6, 4 of
+        // base 7) in slots 0-3, the high part's the rest from slot 4 on
         const bool hi = w >= 4;
-        if (hi != (E >= 216)) continue;
+        if (hi != (E >= Tr::DIV)) continue;
         byte = (entry_dword<BASE, L, 0>(uint32_t(E)) >> (8 * (w % 4))) & 0xFFu;
-        const int v = hi ? E - 216 : E, dg = slot_digit<BASE, L>(w) - (hi ? 3 : 0);
-        if (slot_digit<BASE, L>(w) >= 0) want = uint32_t(dg == 0 ? v % 6 : dg == 1 ? v / 6 % 6 : v / 36);
+        const int v = hi ? E - Tr::DIV : E, first = L == 6 ? 3 : 4;
+        const int dg = slot_digit<BASE, L>(w) - (hi ? first : 0);
+        if (slot_digit<BASE, L>(w) >= 0) {
+          int c = v;
+          for (int t = 0; t < dg; ++t) c /= L;
+          want = uint32_t(c % L);
+        }
       } else {
         const uint32_t dw = w < 4 ? entry_dword<BASE, L, 0>(uint32_t(E)) : entry_dword<BASE, L, 1>(uint32_t(E));
         byte = (dw >> (8 * (w % 4))) & 0xFFu;
@@ -216,7 +233,8 @@ __host__ __device__ constexpr bool entries_match_digits() {
   return true;
 }
 static_assert(entries_match_digits<0, 6>() && entries_match_digits<0, 5>() && entries_match_digits<0, 4>() &&
-              entries_match_digits<0, 3>() && entries_match_digits<1, 4>() && entries_match_digits<1, 3>(), "tables");
+              entries_match_digits<0, 3>() && entries_match_digits<1, 4>() && entries_match_digits<1, 3>() &&
+              entries_match_digits<0, 2>() && entries_match_digits<0, 7>() && entries_match_digits<0, 8>(), "tables");
 
 // 16-byte piece q of the replicated LDS table (entry e of replica r at entry
 // slot e R + r; R >= 4, so a piece lies in one entry, repeated)
@@ -316,6 +334,31 @@ __host__ __device__ constexpr bool magic216_exact(int S, bool with_base) {
   return true;
 }
 
+// floor(v / 2401) for v < 7^7 as the high word of v * 1788825 (v and the
+// multiplier fit 24 bits).  floor(v M / 2^32) does not decrease with v, so it
+// is exact everywhere when it is exact on both sides of every multiple of 2401.
+constexpr uint32_t kMagic2401 = 1788825u;
+__host__ __device__ constexpr bool magic2401_exact() {
+  if (kMagic2401 >= (1u << 24) || 823542u >= (1u << 24)) return false;
+  for (uint64_t k = 1; k <= 343; ++k) {
+    const uint64_t below = 2401 * k - 1, at = 2401 * k;
+    if ((below * kMagic2401) >> 32 != k - 1) return false;
+    if (at < 823543 && (at * kMagic2401) >> 32 != k) return false;
+  }
+  return true;
+}
+static_assert(magic2401_exact(), "7-level digit split");
+
+// operand dwords of 7-level symbol K: the s mod 2401 and s div 2401 entries
+template <int BASE, int S, uint32_t FULL, int K, int NW, int NS>
+__device__ inline uint2 l7_symbol(const uint32_t (&seg)[NW], const uint32_t (&maskS)[NS], const LutRef& lr) {
+  const uint32_t x = sym_addr<BASE, 7, S, FULL, K, NW, NS>(seg, maskS, 0u);   // v << S
+  const uint32_t hi = mulhi24(x >> S, kMagic2401);                           // v div 2401
+  const uint32_t lo = mad_i24(hi, -(2401 << S), x) + lr.lbase;                // ((v mod 2401) << S) + lbase
+  return make_uint2(*reinterpret_cast<const uint32_t*>(lr.t + lo),
+                    *reinterpret_cast<const uint32_t*>(lr.t + ((hi << S) + lr.hbase)));
+}
+
 // operand dwords of 6-level symbol K: the s mod 216 and s div 216 entries
 template <int BASE, int S, uint32_t FULL, int K, int NW, int NS>
 __device__ inline uint2 l6_symbol(const uint32_t (&seg)[NW], const uint32_t (&maskS)[NS], const LutRef& lr) {
@@ -339,6 +382,10 @@ __device__ inline int4v chunk_operand(const uint32_t (&seg)[NW], const uint32_t 
   if constexpr (L == 6) {
     const uint2 p0 = l6_symbol<BASE, S, FULL, 2 * C, NW, NS>(seg, maskS, lr);
     const uint2 p1 = l6_symbol<BASE, S, FULL, 2 * C + 1, NW, NS>(seg, maskS, lr);
+    r = uint4v{p0.x, p0.y, p1.x, p1.y};
+  } else if constexpr (L == 7) {
+    const uint2 p0 = l7_symbol<BASE, S, FULL, 2 * C, NW, NS>(seg, maskS, lr);
+    const uint2 p1 = l7_symbol<BASE, S, FULL, 2 * C + 1, NW, NS>(seg, maskS, lr);
     r = uint4v{p0.x, p0.y, p1.x, p1.y};
   } else if constexpr (Tr::SPC == 4) {
     const uint32_t a = *reinterpret_cast<const uint32_t*>(lr.t + sym_addr<BASE, L, S, FULL, 4 * C, NW, NS>(seg, maskS, lr.lbase));
@@ -464,10 +511,14 @@ struct Plan {
   // table replicas per pool: the most that fit, the low pool (the larger
   // share of the tokens) first (32 dword replicas: a conflict-free lookup of
   // any entries)
+  // (the 7-level tables, 2744 entries, keep 4 replicas: 44 KB)
+  static constexpr int cap(int L) { return L == 7 ? 4 : 32; }
   static constexpr int pick_replicas(bool hi) {
     constexpr int opts[8][2] = {{32, 32}, {16, 32}, {8, 32}, {16, 16}, {8, 16}, {8, 8}, {4, 8}, {4, 4}};
-    for (const auto& o : opts)
-      if (lds_bytes(NW, o[0], o[1]) <= 160 * 1024) return hi ? o[0] : o[1];
+    for (const auto& o : opts) {
+      const int rh = o[0] < cap(LH) ? o[0] : cap(LH), rl = o[1] < cap(LL) ? o[1] : cap(LL);
+      if (lds_bytes(NW, rh, rl) <= 160 * 1024) return hi ? rh : rl;
+    }
     return 0;
   }
   static constexpr int RH = pick_replicas(true), RL = pick_replicas(false);
@@ -667,7 +718,7 @@ __device__ void run_pool(const DecodeArgs& a, Shared<PL>& sm, WaveState<PL::NGV>
   static_assert((1 << S) == NR * Tr::TED * 4, "entry stride");
   constexpr uint32_t KFULL = full_symbols<L, kD, kSlots>(), VFULL = full_symbols<L, kSlots, kD>();
   const uint32_t lb = uint32_t((lane & (NR - 1)) * Tr::TED * 4);
-  const LutRef lut{reinterpret_cast<const uint8_t*>(sm.lut + (POOL ? PL::LUTH : 0)), lb, lb + (216u << S)};
+  const LutRef lut{reinterpret_cast<const uint8_t*>(sm.lut + (POOL ? PL::LUTH : 0)), lb, lb + (uint32_t(Tr::DIV) << S)};
   uint32_t kmask[Tr::NSK], vmask[Tr::NSV];
   segment_masks<L, kD, kSlots>(kg, kmask);
   segment_masks<L, kSlots, kD>(kg, vmask);
@@ -1277,6 +1328,15 @@ int launch_decode(const DecodeArgs& a, hipStream_t s) {
   if (B == 1 && LH == 4 && LL == 3) return launch_dec<1, 4, 3>(a, s);
   if (B == 2 && LH == 6 && LL == 5) return launch_dec<2, 6, 5>(a, s);
   if (B == 2 && LH == 5 && LL == 4) return launch_dec<2, 5, 4>(a, s);
+  // the rest of the level grid (uniform sweeps, Sec. 4.2): metadata per row only
+  if (a.g.G == 128) {
+    if (B == 0 && LH == 8 && LL == 7) return launch_g<0, 8, 7, 128>(a, s);
+    if (B == 0 && LH == 7 && LL == 6) return launch_g<0, 7, 6, 128>(a, s);
+    if (B == 0 && LH == 3 && LL == 2) return launch_g<0, 3, 2, 128>(a, s);
+    if (B == 2 && LH == 8 && LL == 7) return launch_g<2, 8, 7, 128>(a, s);
+    if (B == 2 && LH == 7 && LL == 6) return launch_g<2, 7, 6, 128>(a, s);
+    if (B == 2 && LH == 3 && LL == 2) return launch_g<2, 3, 2, 128>(a, s);
+  }
   return -2;
 }
 
@@ -1290,6 +1350,14 @@ static int decode_query(int base, int LH, int LL, int G, bool waves) {
   if (base == 1 && LH == 4 && LL == 3) return occ_dec<1, 4, 3>(G, waves);
   if (base == 2 && LH == 6 && LL == 5) return occ_dec<2, 6, 5>(G, waves);
   if (base == 2 && LH == 5 && LL == 4) return occ_dec<2, 5, 4>(G, waves);
+  if (G == 128) {
+    if (base == 0 && LH == 8 && LL == 7) return waves ? waves_of<0, 8, 7, 128>() : occupancy<0, 8, 7, 128>();
+    if (base == 0 && LH == 7 && LL == 6) return waves ? waves_of<0, 7, 6, 128>() : occupancy<0, 7, 6, 128>();
+    if (base == 0 && LH == 3 && LL == 2) return waves ? waves_of<0, 3, 2, 128>() : occupancy<0, 3, 2, 128>();
+    if (base == 2 && LH == 8 && LL == 7) return waves ? waves_of<2, 8, 7, 128>() : occupancy<2, 8, 7, 128>();
+    if (base == 2 && LH == 7 && LL == 6) return waves ? waves_of<2, 7, 6, 128>() : occupancy<2, 7, 6, 128>();
+    if (base == 2 && LH == 3 && LL == 2) return waves ? waves_of<2, 3, 2, 128>() : occupancy<2, 3, 2, 128>();
+  }
   return waves ? 8 : 1;
 }
 

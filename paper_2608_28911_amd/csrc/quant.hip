@@ -14,7 +14,7 @@ namespace semkv {
 namespace {
 
 constexpr int kPitch = 132;             // LDS row pitch of the code arrays (bytes)
-constexpr int kMaxBodyWords = 2672 / 4; // largest body: L = 6
+constexpr int kMaxBodyWords = 3072 / 4; // largest body: L = 8
 
 __device__ inline float h2f(uint16_t b) { return __half2float(__ushort_as_half(b)); }
 __device__ inline uint16_t f2h(float f) { return __half_as_ushort(__float2half_rn(f)); }
@@ -536,6 +536,12 @@ int launch_cl(const CloseArgs& a, hipStream_t st) {
   if (BASE == 1 && LH == 4 && LL == 3) return FN<1, 4, 3>(__VA_ARGS__);              \
   if (BASE == 2 && LH == 6 && LL == 5) return FN<2, 6, 5>(__VA_ARGS__);              \
   if (BASE == 2 && LH == 5 && LL == 4) return FN<2, 5, 4>(__VA_ARGS__);              \
+  if (BASE == 0 && LH == 8 && LL == 7) return FN<0, 8, 7>(__VA_ARGS__);              \
+  if (BASE == 0 && LH == 7 && LL == 6) return FN<0, 7, 6>(__VA_ARGS__);              \
+  if (BASE == 0 && LH == 3 && LL == 2) return FN<0, 3, 2>(__VA_ARGS__);              \
+  if (BASE == 2 && LH == 8 && LL == 7) return FN<2, 8, 7>(__VA_ARGS__);              \
+  if (BASE == 2 && LH == 7 && LL == 6) return FN<2, 7, 6>(__VA_ARGS__);              \
+  if (BASE == 2 && LH == 3 && LL == 2) return FN<2, 3, 2>(__VA_ARGS__);              \
   return -2;
 
 int launch_quantize(const QuantArgs& a, hipStream_t s) {

@@ -15,8 +15,13 @@ using namespace semkv;
 
 namespace {
 
+// the adjacent pairs of the rest of the level grid (8/7, 7/6, 3/2 levels),
+// for uniform sweeps (Sec. 4.2): per-row metadata only
+bool grid_pair(int lh, int ll) { return (lh == 8 && ll == 7) || (lh == 7 && ll == 6) || (lh == 3 && ll == 2); }
+
 bool levels_ok(int base, int lh, int ll) {
   if (base == SEMKV_BASE_TQ) return lh == 4 && ll == 3;
+  if (grid_pair(lh, ll)) return true;
   if (base == SEMKV_BASE_ROT_AFFINE) return (lh == 6 && ll == 5) || (lh == 5 && ll == 4);
   static const int pairs[][2] = {{6, 5}, {5, 4}, {6, 4}, {4, 3}, {5, 3}, {6, 3}};
   for (auto& p : pairs)
@@ -199,6 +204,7 @@ int semkv_cache_sizes(const semkv_config* cfg, semkv_sizes* out) {
   if (!levels_ok(k.base, k.L_hi, k.L_lo)) return SEMKV_EUNSUPPORTED;
   if (k.base != SEMKV_BASE_TQ && k.group != 32 && k.group != 64 && k.group != 128) return SEMKV_EUNSUPPORTED;
   if (k.base == SEMKV_BASE_TQ && k.group != 128) return SEMKV_EUNSUPPORTED;
+  if (grid_pair(k.L_hi, k.L_lo) && k.group != 128) return SEMKV_EUNSUPPORTED;
   // the decode kernel needs one 8-wave workgroup's tables and buffers in a
   // compute unit's LDS (6 and 3 levels with 32-channel groups do not fit)
   if (decode_waves(k.base, k.L_hi, k.L_lo, k.group) < 8) return SEMKV_EUNSUPPORTED;

@@ -5,7 +5,9 @@
 // sum_i c_i L^i in the least number of bits.  n is 3 for L = 5 (7 bits, the
 // paper's three-in-seven) and 5 for L = 6 (13 bits, five-in-thirteen); the
 // TurboQuant-MSE levels of Sec. 4.9 use 4 codes of L = 4 (8 bits) and 5 codes
-// of L = 3 (8 bits).  A K line is one token row (128 channels); a V line is one
+// of L = 3 (8 bits).  The rest of the integer-level grid swept in Sec. 4.2:
+// 8 codes of L = 2 (8 bits), 2 of L = 8 (6 bits) and 7 of L = 7 (20 bits,
+// 2.857 bits per value; the paper gives no 7-level packing).  A K line is one token row (128 channels); a V line is one
 // channel column over the 64 slots of a tile.  Segment j of a line holds its
 // symbols p = j, j+4, j+8, ...; a body is segment 0 of all lines, then
 // segments 1, 2, 3, LSB first, zero padded to 16 bytes.
@@ -23,7 +25,7 @@ constexpr int kSlots = 64;   // token slots per tile
 constexpr int kD = 128;      // head dimension
 
 __host__ __device__ constexpr int sym_digits(int L) {
-  return L == 3 ? 5 : L == 4 ? 4 : L == 5 ? 3 : L == 6 ? 5 : 0;
+  return L == 2 ? 8 : L == 3 ? 5 : L == 4 ? 4 : L == 5 ? 3 : L == 6 ? 5 : L == 7 ? 7 : L == 8 ? 2 : 0;
 }
 
 __host__ __device__ constexpr int width_of(int L, int nd) {

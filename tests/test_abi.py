@@ -50,7 +50,7 @@ def cfg_for(abi, **kw):
 def test_sizes_match_the_format(abi):
     from paper_2608_28911_amd import cache_sizes
     for base, L_hi, L_lo, G in ((0, 6, 5, 128), (0, 6, 5, 32), (1, 4, 3, 128), (0, 5, 4, 64), (2, 6, 5, 128),
-                                (2, 5, 4, 32)):
+                                (2, 5, 4, 32), (0, 8, 7, 128), (0, 7, 6, 128), (2, 3, 2, 128)):
         s = cache_sizes(cfg_for(abi, base=base, L_hi=L_hi, L_lo=L_lo, group=G))
         assert s.tile_bytes_hi == O.tile_bytes(L_hi) and s.tile_bytes_lo == O.tile_bytes(L_lo)
         assert s.record_bytes_hi == O.record_bytes(base, L_hi, G)
@@ -64,6 +64,7 @@ def test_sizes_match_the_format(abi):
     (dict(head_dim=64), -2), (dict(n_q_heads=16), -2), (dict(block=32), -2), (dict(L_hi=7), -2),
     (dict(base=1, L_hi=6, L_lo=5), -2), (dict(base=1, L_hi=4, L_lo=3, group=32), -2), (dict(group=16), -2),
     (dict(base=2, L_hi=4, L_lo=3), -2), (dict(base=2, group=16), -2), (dict(base=3), -2),
+    (dict(L_hi=8, L_lo=7, group=32), -2), (dict(L_hi=8, L_lo=6), -2), (dict(base=1, L_hi=3, L_lo=2), -2),
     (dict(r_num=3, r_den=2), -1), (dict(r_den=0), -1), (dict(batch=0), -1), (dict(max_prompt=-1), -1)])
 def test_config_validation(abi, bad, status):
     s = abi.Sizes()

@@ -92,6 +92,12 @@ def test_generation_on_the_rotated_affine_base():
     run_generation(cfgw, 200, 64 + 5, check_steps={0, 63, 64, 68})
 
 
+@pytest.mark.parametrize("levels", [(8, 7), (3, 2)])
+def test_generation_on_the_level_grid(levels):
+    cfgw = get_config(3, L_hi=levels[0], L_lo=levels[1], n_layers=1, batch=1, n_kv_heads=2, n_q_heads=8)
+    run_generation(cfgw, 130, 64 + 3, check_steps={0, 64, 66}, flush=True)
+
+
 def test_generation_g32():
     cfgw = get_config(3, n_layers=1, batch=1, n_kv_heads=1, n_q_heads=4, group=32)
     run_generation(cfgw, 64, 64 * 3, check_steps={10, 100, 191})

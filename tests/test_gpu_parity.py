@@ -121,6 +121,19 @@ def test_rotated_affine_ragged(T):
     _check_decode(cache, cfgw, T, flags, [0])
 
 
+@pytest.mark.parametrize("base", ["affine", "rot_affine"])
+@pytest.mark.parametrize("r", [(0, 1), (1, 1), (35, 100)])
+@pytest.mark.parametrize("levels", [(8, 7), (7, 6), (3, 2)])
+def test_level_grid_pairs(levels, r, base):
+    """The rest of the integer-level grid (Sec. 4.2): 8, 7 and 2 levels (7
+    codes in 20 bits, 2 in 6 bits, 8 in a byte); r = 0 and 1 are the uniform
+    grid points of the cliff sweep, 35 % a mix."""
+    cfgw = get_config(0, base=base, L_hi=levels[0], L_lo=levels[1], group=128, r_num=r[0], r_den=r[1],
+                      n_kv_heads=2, n_q_heads=8)
+    cache, flags = _check_prefill(cfgw, 700)
+    _check_decode(cache, cfgw, 700, flags, [0])
+
+
 def test_constant_rows_quantize_exactly():
     import torch
     cfgw = get_config(0, n_kv_heads=1, n_q_heads=4, group=32)
