@@ -68,6 +68,8 @@ def parse():
     ap.add_argument("--base", default=None, choices=["affine", "rot_affine"],
                     help="override an affine workload's base (rot_affine: the affine quantizer of the "
                          "Hadamard-rotated row)")
+    ap.add_argument("--levels", default=None, help="override an affine workload's level pair, e.g. 8,7")
+    ap.add_argument("--ratio", default=None, help="override the high-precision fraction r, e.g. 0/1 or 35/100")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-indicators", dest="indicators", action="store_false",
                     help="skip timing the token-importance indicators")
@@ -381,13 +383,19 @@ def main():
     cfgw = get_config(args.workload)
     if cfgw.turns:
         return multiturn(args, cfgw)
-    if args.group or args.base:
+    if args.group or args.base or args.levels or args.ratio:
         from dataclasses import replace
-        if args.base and cfgw.base == "tq":
-            sys.exit("--base applies to the affine workloads")
+        if (args.base or args.levels) and cfgw.base == "tq":
+            sys.exit("--base and --levels apply to the affine workloads")
         cfgw = replace(cfgw, group=args.group or cfgw.group, base=args.base or cfgw.base)
         if cfgw.base == "rot_affine":
             cfgw = replace(cfgw, name=cfgw.name.replace("_affine", "_rot_affine"))
+        if args.levels:
+            lh, ll = (int(x) for x in args.levels.split(","))
+            cfgw = replace(cfgw, L_hi=lh, L_lo=ll, name=cfgw.name + "_L%d%d" % (lh, ll))
+        if args.ratio:
+            rn, rd = (int(x) for x in args.ratio.split("/"))
+            cfgw = replace(cfgw, r_num=rn, r_den=rd, name=cfgw.name + "_r%d_%d" % (rn, rd))
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     B, H, Hq, T, nL = cfgw.batch, cfgw.n_kv_heads, cfgw.n_q_heads, cfgw.prompt_len, cfgw.n_layers

@@ -1,9 +1,9 @@
 """Size arithmetic of the packed format (the same rules as csrc/semkv_fmt.h),
 for byte accounting in the benchmark: a symbol packs n codes of base L in the
-least number of bits, n = 5, 4, 3, 5 for L = 3, 4, 5, 6 (mixed-radix packing,
-SemKV Sec. 4.1)."""
+least number of bits, n = 8, 5, 4, 3, 5, 7, 2 for L = 2 .. 8 (mixed-radix
+packing, SemKV Sec. 4.1)."""
 
-DIGITS = {3: 5, 4: 4, 5: 3, 6: 5}
+DIGITS = {2: 8, 3: 5, 4: 4, 5: 3, 6: 5, 7: 7, 8: 2}
 
 
 def width(L, nd):
