@@ -215,6 +215,16 @@ int semkv_append_decode(semkv_cache* c, int32_t layer, const uint16_t* k_new, co
                         const uint16_t* q, float* out, void* workspace, size_t ws_bytes,
                         hipStream_t stream);
 
+/* Test and inspection aid: the values decode attention reads from the pools
+ * of `layer`, dequantized to fp32 (affine: fmaf(c, scale, zero); rotated
+ * affine: sign . H y / 8 of the affine values y; tq: sign . H (rho mu[c]) /
+ * 128, the transforms summed in fp32).  k_hat, v_hat: device fp32
+ * [batch][n_kv_heads][n_hi + n_lo][128], 16-byte aligned: rows 0 .. n_hi-1
+ * are the high pool's slots, then the low pool's, each in slot order
+ * (ascending token position, prompt first, then closed blocks; the flag
+ * bitmap gives each slot's token).  The fp16 tail is not included. */
+int semkv_dequant(const semkv_cache* c, int32_t layer, float* k_hat, float* v_hat, hipStream_t stream);
+
 /* Token-importance indicators (Sec. 3.3): device fp32 scores [batch][T] for
  * semkv_rank (which uses only their order), from tensors the model already
  * computes.  Hidden-state family, over the hidden states of the last m+1

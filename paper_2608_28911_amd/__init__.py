@@ -114,6 +114,19 @@ class SemKVCache:
         check(lib().semkv_quantize_pack(ctypes.byref(self.c), layer, _ptr(K), _ptr(V), sL, sB, sH, sT, T,
                                         _ptr(hi_idx), _ptr(lo_idx), _stream()), "semkv_quantize_pack")
 
+    def dequant(self, layer):
+        """fp32 (K_hat, V_hat) [B, H_kv, n_hi + n_lo, 128] of `layer`: the high
+        pool's slots, then the low pool's, as decode attention reads them."""
+        import torch
+        n = self.c.n_hi + self.c.n_lo
+        shape = (self.cfg.batch, self.cfg.n_kv_heads, n, 128)
+        k = torch.empty(shape, dtype=torch.float32, device=self.pools.device)
+        v = torch.empty_like(k)
+        if n == 0:
+            return k, v
+        check(lib().semkv_dequant(ctypes.byref(self.c), layer, _ptr(k), _ptr(v), _stream()), "semkv_dequant")
+        return k, v
+
     def score_kv_norm(self, X, scores=None):
         """Key-norm (X = K) or value-norm (X = V) of every token: X fp16
         [n_layers, B, H_kv, T, 128] -> fp32 [B, T] (Sec. 3.3)."""

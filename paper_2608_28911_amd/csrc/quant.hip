@@ -107,8 +107,7 @@ __device__ uint32_t affine_quarter(const float x[32], int G, uint32_t code[8]) {
 // H diag(sign) x of one row quarter: sign flip, then the unnormalized
 // Walsh-Hadamard transform, stages 1..16 inside the lane and 32, 64 across
 // the lanes of the row's quad.
-__device__ inline void rotate_quarter(const float x[32], int q, const uint32_t* sw, float u[32]) {
-  const uint32_t sbits = sw[q];
+__device__ inline void rotate_quarter(const float x[32], int q, uint32_t sbits, float u[32]) {
 #pragma unroll
   for (int i = 0; i < 32; ++i) u[i] = ((sbits >> i) & 1u) ? -x[i] : x[i];
 #pragma unroll
@@ -142,7 +141,7 @@ template <int L>
 __device__ uint16_t tq_quarter(const float x[32], int q, const uint32_t* sw, const float* tau,
                                uint32_t code[8]) {
   float u[32], a[32];
-  rotate_quarter(x, q, sw, u);
+  rotate_quarter(x, q, sw[q], u);
 #pragma unroll
   for (int i = 0; i < 32; ++i) a[i] = x[i] * x[i];
 #pragma unroll
@@ -183,7 +182,7 @@ __device__ uint16_t tq_quarter(const float x[32], int q, const uint32_t* sw, con
 template <int L>
 __device__ uint32_t rot_affine_quarter(const float x[32], int q, const uint32_t* sw, int G, uint32_t code[8]) {
   float y[32];
-  rotate_quarter(x, q, sw, y);
+  rotate_quarter(x, q, sw[q], y);
   float mn = INFINITY, mx = -INFINITY;
 #pragma unroll
   for (int i = 0; i < 32; ++i) {
@@ -495,6 +494,80 @@ __global__ __launch_bounds__(256) void close_kernel(CloseArgs a) {
   else close_record<BASE, LL>(a, s, row_of[1], m, 1, int(tile), b, l, h);
 }
 
+// ------------------------------------------------------------ dequant --
+
+// The values one record holds, as decode attention sees them: affine
+// x = fmaf(c, scale, zero); rotated affine x = sign . H y / 8 with y the
+// affine value; tq x = sign . H (rho mu[c]) / 128.  One workgroup per record:
+// the bodies are unpacked into LDS as for a block close, four lanes per slot.
+template <int BASE, int L>
+__device__ void dequant_record(const DequantArgs& a, Lds& s, int pool, int tile, int b, int h) {
+  const PoolGeom& g = a.g;
+  const int tid = threadIdx.x, r = tid >> 2, q = tid & 3;
+  constexpr int tb = tile_bytes(L);
+  const uint8_t* rec = g.pools + unit_offset(g, b, a.layer, h) + (pool ? g.lo_offset : 0) +
+                       int64_t(tile) * g.rec_bytes[pool];
+  for (int i = tid; i < kMaxBodyWords + 8; i += 256) s.bk[i] = s.bv[i] = 0u;
+  __syncthreads();
+  const uint32_t* gk = reinterpret_cast<const uint32_t*>(rec);
+  const uint32_t* gv = reinterpret_cast<const uint32_t*>(rec + tb);
+  for (int i = tid; i < tb / 4; i += 256) {
+    s.bk[i] = gk[i];
+    s.bv[i] = gv[i];
+  }
+  __syncthreads();
+  unpack_segment<L, kD, kSlots>(s.bk, tid & 63, tid >> 6, s.ck + (tid & 63) * kPitch, 1);
+#pragma unroll
+  for (int e = 0; e < 2; ++e) {
+    const int sg = tid + 256 * e;
+    unpack_segment<L, kSlots, kD>(s.bv, sg & 127, sg >> 7, s.cv + (sg & 127), kPitch);
+  }
+  __syncthreads();
+  const int64_t slot = int64_t(tile) * kSlots + r;
+  const bool valid = slot < a.n_rows[pool];
+  const int64_t N = a.n_rows[0] + a.n_rows[1];
+  const int64_t row = (pool ? a.n_rows[0] : 0) + slot;
+  const uint32_t sbits = BASE != 0 ? g.signs[(int64_t(a.layer) * g.n_kv_heads + h) * 4 + q] : 0u;
+#pragma unroll
+  for (int kv = 0; kv < 2; ++kv) {
+    const uint8_t* c = (kv ? s.cv : s.ck) + r * kPitch + 32 * q;
+    const uint8_t* meta = rec + 2 * tb + kv * g.meta_bytes;
+    float x[32];
+    if (BASE != 1) {
+      const uint32_t m = reinterpret_cast<const uint32_t*>(meta)[((32 * q) / g.G) * kSlots + r];
+      const float sc = h2f(uint16_t(m & 0xFFFFu)), z = h2f(uint16_t(m >> 16));
+#pragma unroll
+      for (int i = 0; i < 32; ++i) x[i] = fmaf(float(c[i]), sc, z);
+    } else {
+      const float rho = h2f(reinterpret_cast<const uint16_t*>(meta)[r]);
+      const float* mu = a.mu[pool];
+#pragma unroll
+      for (int i = 0; i < 32; ++i) x[i] = rho * mu[c[i] < L ? c[i] : 0];
+    }
+    if (BASE != 0) {                       // sign . H x, scaled back
+      float u[32];
+      rotate_quarter(x, q, 0u, u);
+      const float k = BASE == 2 ? 0.125f : 1.0f / 128.0f;
+#pragma unroll
+      for (int i = 0; i < 32; ++i) x[i] = ((sbits >> i) & 1u) ? -u[i] * k : u[i] * k;
+    }
+    float* dst = (kv ? a.v_hat : a.k_hat) + ((int64_t(b) * g.n_kv_heads + h) * N + row) * kD + 32 * q;
+    if (valid) {
+#pragma unroll
+      for (int i = 0; i < 32; i += 4) *reinterpret_cast<float4*>(dst + i) = make_float4(x[i], x[i + 1], x[i + 2], x[i + 3]);
+    }
+  }
+}
+
+template <int BASE, int LH, int LL>
+__global__ __launch_bounds__(256) void dequant_kernel(DequantArgs a) {
+  __shared__ Lds s;
+  const int tile = blockIdx.x, pool = blockIdx.y & 1, h = blockIdx.y >> 1, b = blockIdx.z;
+  if (int64_t(tile) * kSlots >= a.n_rows[pool]) return;
+  if (pool == 0) dequant_record<BASE, LH>(a, s, 0, tile, b, h);
+  else dequant_record<BASE, LL>(a, s, 1, tile, b, h);
+}
+
 __global__ void append_kernel(AppendArgs a) {
   // one block per (layer, b, kv head); 64 threads copy K and V rows
   int z = blockIdx.x;
@@ -514,6 +587,14 @@ template <int BASE, int LH, int LL>
 int launch_qp(const QuantArgs& a, hipStream_t st) {
   dim3 grid(a.max_tiles, 2 * a.g.n_kv_heads, a.g.batch * a.n_layers_launched);
   hipLaunchKernelGGL((quantize_pack_kernel<BASE, LH, LL>), grid, dim3(256), 0, st, a);
+  return hipGetLastError() == hipSuccess ? 0 : -5;
+}
+
+template <int BASE, int LH, int LL>
+int launch_dq(const DequantArgs& a, hipStream_t st) {
+  const int64_t mt = ((a.n_rows[0] > a.n_rows[1] ? a.n_rows[0] : a.n_rows[1]) + kSlots - 1) / kSlots;
+  dim3 grid(unsigned(mt), 2 * a.g.n_kv_heads, a.g.batch);
+  hipLaunchKernelGGL((dequant_kernel<BASE, LH, LL>), grid, dim3(256), 0, st, a);
   return hipGetLastError() == hipSuccess ? 0 : -5;
 }
 
@@ -550,6 +631,10 @@ int launch_quantize(const QuantArgs& a, hipStream_t s) {
 
 int launch_close(const CloseArgs& a, hipStream_t s) {
   SEMKV_DISPATCH_LEVELS(a.g.base, a.g.L[0], a.g.L[1], launch_cl, a, s)
+}
+
+int launch_dequant(const DequantArgs& a, hipStream_t s) {
+  SEMKV_DISPATCH_LEVELS(a.g.base, a.g.L[0], a.g.L[1], launch_dq, a, s)
 }
 
 int launch_append(const AppendArgs& a, hipStream_t s) {

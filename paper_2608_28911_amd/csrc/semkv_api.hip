@@ -472,6 +472,24 @@ int semkv_append_decode(semkv_cache* c, int32_t layer, const uint16_t* k_new, co
   return SEMKV_OK;
 }
 
+int semkv_dequant(const semkv_cache* c, int32_t layer, float* k_hat, float* v_hat, hipStream_t stream) {
+  if (!c || !k_hat || !v_hat) return SEMKV_EINVAL;
+  if (layer < 0 || layer >= c->cfg.n_layers) return SEMKV_EINVAL;
+  if ((uintptr_t(k_hat) | uintptr_t(v_hat)) & 15) return SEMKV_EINVAL;
+  if (c->n_hi + c->n_lo == 0) return SEMKV_OK;
+  DequantArgs a;
+  memset(&a, 0, sizeof(a));
+  a.g = geom(c);
+  a.layer = layer;
+  a.n_rows[0] = c->n_hi;
+  a.n_rows[1] = c->n_lo;
+  memcpy(a.mu[0], c->mu_hi, sizeof(a.mu[0]));
+  memcpy(a.mu[1], c->mu_lo, sizeof(a.mu[1]));
+  a.k_hat = k_hat;
+  a.v_hat = v_hat;
+  return launch_dequant(a, stream);
+}
+
 int semkv_score_hidden(int32_t indicator, const void* hidden, int32_t dtype, int32_t m, int32_t batch,
                        int64_t T, int32_t d_model, int64_t s_state, int64_t s_batch, int64_t s_token,
                        float* scores, hipStream_t stream) {

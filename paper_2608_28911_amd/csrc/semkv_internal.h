@@ -76,6 +76,15 @@ struct DecodeArgs {
   float mu[2][16];         // tq codebooks
 };
 
+struct DequantArgs {
+  PoolGeom g;
+  int32_t layer;
+  int64_t n_rows[2];       // rows in the high / low pool
+  float mu[2][16];         // tq codebooks
+  float* k_hat;            // [b][kvh][n_rows[0] + n_rows[1]][128]: high pool, then low pool
+  float* v_hat;
+};
+
 struct HiddenArgs {
   const uint16_t* h;       // state k, sequence b, token t at k*s_state + b*s_batch + t*s_token
   int64_t s_state, s_batch, s_token;
@@ -99,6 +108,7 @@ int launch_rank(const RankArgs& a, int batch, hipStream_t s);
 int launch_quantize(const QuantArgs& a, hipStream_t s);
 int launch_append(const AppendArgs& a, hipStream_t s);
 int launch_close(const CloseArgs& a, hipStream_t s);
+int launch_dequant(const DequantArgs& a, hipStream_t s);
 int launch_decode(const DecodeArgs& a, hipStream_t s);
 int launch_score_hidden(const HiddenArgs& a, hipStream_t s);
 int launch_kv_norm(const KvNormArgs& a, hipStream_t s);
