@@ -90,6 +90,14 @@ def test_calls_validate_before_touching_the_device(abi):
     assert lib.semkv_strerror(-3) == b"capacity exceeded"
     tq = cfg_for(abi, base=1, L_hi=4, L_lo=3)
     assert lib.semkv_cache_init(ctypes.byref(c), ctypes.byref(tq), fake, fake, fake, fake, None, fake) == -1
+    assert lib.semkv_cache_reset(None, None) == -1
+    assert lib.semkv_dequant(ctypes.byref(c), 0, None, fake, None) == -1
+    assert lib.semkv_dequant(ctypes.byref(c), 7, fake, fake, None) == -1             # layer out of range
+    assert lib.semkv_dequant(ctypes.byref(c), 0, ctypes.c_void_p(0x1004), fake, None) == -1   # alignment
+    assert lib.semkv_dequant(ctypes.byref(c), 0, fake, fake, None) == 0              # empty cache: nothing to do
+    assert lib.semkv_score_kv_norm(ctypes.byref(c), fake, 0, 0, 0, 64, 16, fake, None) == -1   # sT < 128
+    assert lib.semkv_score_kv_norm(ctypes.byref(c), None, 0, 0, 0, 128, 16, fake, None) == -1
+    assert lib.semkv_score_hidden(0, fake, 0, 4, 1, 0, 64, 64, 64, 64, fake, None) == -1      # T = 0
     rot = cfg_for(abi, base=2)                                                        # needs sign masks too
     assert lib.semkv_cache_init(ctypes.byref(c), ctypes.byref(rot), fake, fake, fake, fake, None, fake) == -1
     assert lib.semkv_cache_init(ctypes.byref(c), ctypes.byref(rot), fake, fake, fake, fake, fake, fake) == 0
