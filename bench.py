@@ -13,7 +13,7 @@ cache (pools resident in HBM).  The K timed steps are one HIP graph replay
 bracketed by events and device synchronization.  The prefill path (rank,
 quantize + pack) is timed separately and reported beside it.
 
-Prints one JSON line.  --gpus N with N > 1 is refused: this build runs on
+Prints one JSON line.  --gpus N with N > 1 is refused: the library runs on
 one GPU.
 """
 import argparse
@@ -373,7 +373,7 @@ def multiturn(args, cfgw):
 def main():
     args = parse()
     if args.gpus != 1:
-        print("bench.py: this build runs on one GPU; --gpus %d is not supported "
+        print("bench.py: the library runs on one GPU; --gpus %d is not supported "
               "(the multi-GPU sharding plan is described in DESIGN.md)" % args.gpus, file=sys.stderr)
         sys.exit(2)
     import torch
