@@ -374,7 +374,7 @@ def main():
     args = parse()
     if args.gpus != 1:
         print("bench.py: the library runs on one GPU; --gpus %d is not supported "
-              "(the multi-GPU sharding plan is described in DESIGN.md)" % args.gpus, file=sys.stderr)
+              "(how the path would shard over GPUs is described with the design notes)" % args.gpus, file=sys.stderr)
         sys.exit(2)
     import torch
     import paper_2608_28911_amd as P
