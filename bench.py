@@ -158,6 +158,18 @@ def cpu_baseline(cfgw, seconds):
     per_unit = t_attn / units
     units_per_step = cfgw.n_layers * cfgw.batch * cfgw.n_kv_heads
     threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    # the indicators (Sec. 3.3) on 1024 tokens: delta-norm over 5 hidden states
+    # of width 4096, key-norm over every layer and kv head (single thread)
+    rng = np.random.default_rng(0)
+    n_tok = 1024
+    Hs = rng.standard_normal((LAST_M + 1, n_tok, HIDDEN_DIM), dtype=np.float32).astype(np.float16)
+    t0 = time.perf_counter()
+    O.score_hidden(O.DELTA_NORM, Hs)
+    t_dn = time.perf_counter() - t0
+    Ks = rng.standard_normal((cfgw.n_layers * cfgw.n_kv_heads, n_tok, 128), dtype=np.float32).astype(np.float16)
+    t0 = time.perf_counter()
+    O.score_kv_norm(Ks)
+    t_kn = time.perf_counter() - t0
     return {
         "value": 1.0 / (per_unit * units_per_step) * cfgw.batch,
         "unit": "tokens/s",
@@ -168,6 +180,7 @@ def cpu_baseline(cfgw, seconds):
                   % (units, T, per_unit, units_per_step),
         "quantize_pack_gbps": q_bytes / t_quant / 1e9,
         "quantize_pack_cores": threads,
+        "delta_norm_tokens_per_s": n_tok / t_dn, "key_norm_tokens_per_s": n_tok / t_kn, "indicator_cores": 1,
     }
 
 
