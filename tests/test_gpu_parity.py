@@ -184,3 +184,33 @@ def test_tq_norm_rounding_edge_rows():
     u = U.oracle_unit(cfgw, 0, 0, 0, f, T, kv=lambda l: (K, V))
     for p in (0, 1):
         assert np.array_equal(U.gpu_records(cache, 0, 0, 0, p, u.count(p)), u.records(p)), "pool %d" % p
+
+
+def test_max_batch():
+    """1024 sequences (the most semkv_append_commit takes): rank, quantize,
+    decode, a generated token and a residual flush, sampled sequences checked."""
+    import torch
+    cfgw = get_config(0, batch=1024, n_kv_heads=1, n_q_heads=4, n_gen=2)
+    T = 100
+    cache = U.make_cache(cfgw, T, n_layers=1, max_new=2)
+    scores, hi, lo = U.prefill(cache, cfgw, T)
+    hi, lo = hi.cpu().numpy(), lo.cpu().numpy()
+    q = synth.query(cfgw, 0, 0)
+    k = torch.from_numpy(np.stack([synth.unit_gen_kv(cfgw, 0, b, 0, 1)[0] for b in range(1024)])[:, None, 0]).cuda()
+    v = torch.from_numpy(np.stack([synth.unit_gen_kv(cfgw, 0, b, 0, 1)[1] for b in range(1024)])[:, None, 0]).cuda()
+    out = cache.append_decode_attn(0, k, v, torch.from_numpy(q).cuda()).cpu().numpy()
+    cache.append_commit(torch.arange(1024, dtype=torch.float32).cuda())
+    cache.flush()
+    torch.cuda.synchronize()
+    assert cache.status() == 0 and cache.c.n_hi + cache.c.n_lo == T + 1
+    for b in (0, 1, 511, 1023):
+        flag, ohi, olo = O.rank(scores[b], cfgw.r_num, cfgw.r_den)
+        assert np.array_equal(hi[b], ohi) and np.array_equal(lo[b], olo)
+        u = U.oracle_unit(cfgw, 0, b, 0, flag, T)
+        u.append_kv(k[b, 0].cpu().numpy(), v[b, 0].cpu().numpy())
+        U.assert_attention_close(out[b], u.attend(q[b].astype(np.float64)), "sequence %d" % b)
+        u.commit(float(b))
+        u.flush()
+        for p in (0, 1):
+            n = u.count(p)
+            assert np.array_equal(U.gpu_records(cache, b, 0, 0, p, n), u.records(p)), "sequence %d pool %d" % (b, p)
