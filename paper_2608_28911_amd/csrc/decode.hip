@@ -451,7 +451,11 @@ struct Geo {
   // chunk's operand at once.  Row 4h + s holds byte s of head h's weights;
   // rows 4h + 3, pad slots and slots past token 63 are never written and
   // stay zero.
-  static constexpr int CHB = 4 * 16 * 16;                    // bytes per chunk
+  // lane groups 272 bytes apart (16 rows of 16 slots, then 16 bytes of pad):
+  // the byte writes of consecutive symbols, which sit in consecutive lane
+  // groups, land in different LDS banks rather than all in one
+  static constexpr int KGS = 16 * 16 + 16;                   // bytes per lane group
+  static constexpr int CHB = 4 * KGS;                        // bytes per chunk
   static constexpr int PV = Tr::NCV * CHB;                   // bytes per wave
   static_assert(RB % 16 == 0, "record pieces");
 };
@@ -742,7 +746,7 @@ __device__ void run_pool(const DecodeArgs& a, Shared<PL>& sm, WaveState<PL::NGV>
 #pragma unroll
   for (int blk = 0; blk < 4; ++blk) {
     const int t = 16 * blk + n, p = t / Tr::n, d = t - p * Tr::n, k = p >> 2;
-    pvwr[blk] = (k / Tr::SPC) * Ge::CHB + (p & 3) * 256 + 64 * r + (k % Tr::SPC) * Tr::STRIDE + digit_slot<BASE, L>(d);
+    pvwr[blk] = (k / Tr::SPC) * Ge::CHB + (p & 3) * Ge::KGS + 64 * r + (k % Tr::SPC) * Tr::STRIDE + digit_slot<BASE, L>(d);
   }
   static_assert(Ge::PV % 16 == 0, "weight array pieces");
   for (int i = lane; i < Ge::PV / 16; i += 64) reinterpret_cast<uint4*>(pvw)[i] = make_uint4(0u, 0u, 0u, 0u);
@@ -909,7 +913,7 @@ __device__ void run_pool(const DecodeArgs& a, Shared<PL>& sm, WaveState<PL::NGV>
         __builtin_amdgcn_wave_barrier();
 #pragma unroll
         for (int c = 0; c < Tr::NCV; ++c) {
-          const uint4 v = *reinterpret_cast<const uint4*>(pvw + c * Ge::CHB + kg * 256 + n * 16);
+          const uint4 v = *reinterpret_cast<const uint4*>(pvw + c * Ge::CHB + kg * Ge::KGS + n * 16);
           Aw[c] = __builtin_bit_cast(int4v, uint4v{v.x, v.y, v.z, v.w});
         }
       }
