@@ -197,6 +197,10 @@ int semkv_workspace_bytes(const semkv_cache* c, size_t* bytes);
  * t of the sequence: both pools (dequantized on the fly) and the fp16 tail
  * rows appended so far, including this layer's current token if appended.
  * q: device fp16 [batch][n_q_heads][128]; out: device fp32, same shape.
+ * layer == -1: every layer in one launch, q and out [n_layers][batch]
+ * [n_q_heads][128] (for queries known up front, as in a benchmark; a model
+ * computes layer l's query from layer l-1's output); every layer must have
+ * appended the current token, or none (else SEMKV_ESTATE).
  * workspace: device, ws_bytes >= semkv_workspace_bytes(); it starts with
  * per-(sequence, kv head) counters that must be zero before the first call
  * (allocate it zeroed); every call leaves them zero again.  One workspace may

@@ -169,7 +169,8 @@ class SemKVCache:
         return self._ws
 
     def decode_attn(self, layer, q, out=None, workspace=None):
-        """q: fp16 [B, H_q, 128] -> fp32 [B, H_q, 128]."""
+        """q: fp16 [B, H_q, 128] -> fp32 [B, H_q, 128]; layer = -1: every layer
+        in one launch, q fp16 [n_layers, B, H_q, 128] -> fp32 of that shape."""
         import torch
         q = q.contiguous()
         if out is None:

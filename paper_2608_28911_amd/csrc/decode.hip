@@ -999,12 +999,12 @@ __device__ inline float fwht_rows(float x, float (*xch)[kD]) {
 // fp16 tail of generated tokens (at most 64 rows), plain vector arithmetic;
 // its state goes to sm.tfin.
 template <int BASE, class PL>
-__device__ void tail_split(const DecodeArgs& a, Shared<PL>& sm, int b, int kvh) {
+__device__ void tail_split(const DecodeArgs& a, Shared<PL>& sm, int b, int layer, int kvh) {
   const PoolGeom& g = a.g;
   const int tid = threadIdx.x;
   const int nt = a.n_tail;
   TailScratch& ts = sm.ts;
-  const uint16_t* kt = a.tail + ((((int64_t(b) * g.n_layers + a.layer) * g.n_kv_heads + kvh) * 2) * kSlots) * kD;
+  const uint16_t* kt = a.tail + ((((int64_t(b) * g.n_layers + layer) * g.n_kv_heads + kvh) * 2) * kSlots) * kD;
   const uint16_t* vt = kt + kSlots * kD;
   if (tid < 4 * nt) {
     const int t = tid >> 2, h = tid & 3;
@@ -1031,7 +1031,7 @@ __device__ void tail_split(const DecodeArgs& a, Shared<PL>& sm, int b, int kvh) 
   if (tid < 4 * kD) {
     for (int t = 0; t < nt; ++t) o += ts.lg[h][t] * hf(vt[t * kD + c]);
     if (BASE != 0) {                       // into the rotated domain: H (sign . o) / 128
-      const uint32_t* sw = g.signs + (int64_t(a.layer) * g.n_kv_heads + kvh) * 4;
+      const uint32_t* sw = g.signs + (int64_t(layer) * g.n_kv_heads + kvh) * 4;
       o = ((sw[c >> 5] >> (c & 31)) & 1u) ? -o : o;
     }
   }
@@ -1045,21 +1045,22 @@ __device__ void tail_split(const DecodeArgs& a, Shared<PL>& sm, int b, int kvh) 
   }
 }
 
-// Merge of the partials of one (sequence, kv head), run by the last workgroup
-// to finish: log-sum-exp over the partials, then for the rotated bases the
-// inverse rotation o = sign . H o_rot.
+// Merge of the partials of one (layer, sequence, kv head), run by the last
+// workgroup to finish: log-sum-exp over the partials, then for the rotated
+// bases the inverse rotation o = sign . H o_rot.  vb indexes the launch's
+// (layer, sequence) pairs: partials, counters, queries and outputs.
 template <int BASE, class PL>
-__device__ void merge_splits(const DecodeArgs& a, Shared<PL>& sm, int b, int kvh) {
+__device__ void merge_splits(const DecodeArgs& a, Shared<PL>& sm, int vb, int layer, int kvh) {
   const int tid = threadIdx.x;
   const int ns = a.nsplit;
-  const float* unit = a.ws + (int64_t(b) * a.g.n_kv_heads + kvh) * ns * 4 * kPartial;
+  const float* unit = a.ws + (int64_t(vb) * a.g.n_kv_heads + kvh) * ns * 4 * kPartial;
   // thread (head h, quarter q, channel quad cq) takes the splits s = q, q+4,
   // ... with 16-byte loads at the coherent level (cache policy sc1, as the
   // agent-scope loads), then the four quarters merge in LDS
   const bool mine = tid < 4 * kD;
   const int h = (tid >> 7) & 3, q = (tid >> 5) & 3, cq = tid & 31;
   // the sign of this thread's output channel (rotated bases), loaded first
-  const uint32_t sbits = BASE != 0 && mine ? a.g.signs[(int64_t(a.layer) * a.g.n_kv_heads + kvh) * 4 + ((tid & 127) >> 5)] : 0u;
+  const uint32_t sbits = BASE != 0 && mine ? a.g.signs[(int64_t(layer) * a.g.n_kv_heads + kvh) * 4 + ((tid & 127) >> 5)] : 0u;
   const __amdgpu_buffer_rsrc_t rs =
       __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(unit), 0, ns * 4 * kPartial * 4, kBufferWord3);
   constexpr int kCoherent = 16;              // sc1
@@ -1127,7 +1128,7 @@ __device__ void merge_splits(const DecodeArgs& a, Shared<PL>& sm, int b, int kvh
     r = fwht_rows(r, sm.ts.o);
     r = ((sbits >> (c & 31)) & 1u) ? -r : r;
   }
-  if (mine) a.out[((int64_t(b) * a.g.n_kv_heads + kvh) * 4 + hc) * kD + c] = r;
+  if (mine) a.out[((int64_t(vb) * a.g.n_kv_heads + kvh) * 4 + hc) * kD + c] = r;
 }
 
 template <int BASE, int LH, int LL, int G>
@@ -1137,7 +1138,10 @@ __global__ __launch_bounds__((Plan<BASE, LH, LL, G>::NT)) void decode_kernel(Dec
   __shared__ Shared<PL> sm;
   static_assert(sizeof(Shared<PL>) <= 160 * 1024, "LDS");
   static_assert(NT >= 4 * kD, "one thread per (head, channel) of the query and the output");
-  const int split = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
+  // blockIdx.z = (layer of the launch) x batch + sequence: an all-layers
+  // launch covers n_layers_launched layers from a.layer
+  const int split = blockIdx.x, kvh = blockIdx.y, vb = blockIdx.z;
+  const int li = vb / a.g.batch, b = vb - li * a.g.batch, layer = a.layer + li;
   const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
   const PoolGeom& g = a.g;
 
@@ -1147,7 +1151,7 @@ __global__ __launch_bounds__((Plan<BASE, LH, LL, G>::NT)) void decode_kernel(Dec
   const int first = wave * a.nsplit + split;
   const int count = first < nt ? (nt - first + stride - 1) / stride : 0;
   const int nhi = first < nt0 ? (nt0 - first + stride - 1) / stride : 0;
-  const uint8_t* unit = g.pools + unit_offset(g, b, a.layer, kvh);
+  const uint8_t* unit = g.pools + unit_offset(g, b, layer, kvh);
 
   // ---- fused append (Alg. 2): the workgroup that attends over the fp16 tail
   // first stores this layer's new K/V row in it, as its last row (read back
@@ -1156,7 +1160,7 @@ __global__ __launch_bounds__((Plan<BASE, LH, LL, G>::NT)) void decode_kernel(Dec
     const int kv = tid >> 6, w = tid & 63;                // 64 dwords each of K and V
     const uint32_t* src = reinterpret_cast<const uint32_t*>((kv ? a.v_new : a.k_new) + (int64_t(b) * g.n_kv_heads + kvh) * kD);
     uint32_t* dst = reinterpret_cast<uint32_t*>(
-        a.tail + ((((int64_t(b) * g.n_layers + a.layer) * g.n_kv_heads + kvh) * 2 + kv) * kSlots + (a.n_tail - 1)) * kD);
+        a.tail + ((((int64_t(b) * g.n_layers + layer) * g.n_kv_heads + kvh) * 2 + kv) * kSlots + (a.n_tail - 1)) * kD);
     dst[w] = src[w];
   }
 
@@ -1164,9 +1168,9 @@ __global__ __launch_bounds__((Plan<BASE, LH, LL, G>::NT)) void decode_kernel(Dec
   // work takes the first 4 x 128 threads, one per (head, channel)
   const bool qt = tid < 4 * kD;
   const int h = qt ? tid >> 7 : 0, c = tid & 127;
-  const uint16_t qbits = qt ? a.q[((int64_t(b) * g.n_kv_heads * 4) + kvh * 4 + h) * kD + c] : uint16_t(0);
+  const uint16_t qbits = qt ? a.q[((int64_t(vb) * g.n_kv_heads * 4) + kvh * 4 + h) * kD + c] : uint16_t(0);
   // rotated bases: the sign word of this thread's channel, in flight with the query
-  const uint32_t qsign = BASE != 0 && qt ? g.signs[(int64_t(a.layer) * g.n_kv_heads + kvh) * 4 + (c >> 5)] : 0u;
+  const uint32_t qsign = BASE != 0 && qt ? g.signs[(int64_t(layer) * g.n_kv_heads + kvh) * 4 + (c >> 5)] : 0u;
   constexpr int NTH = (PL::LUTH / 4 + NT - 1) / NT, NTL = (PL::LUTL / 4 + NT - 1) / NT;
   uint4 th[NTH], tl[NTL];
 #pragma unroll
@@ -1221,7 +1225,7 @@ __global__ __launch_bounds__((Plan<BASE, LH, LL, G>::NT)) void decode_kernel(Dec
   __syncthreads();
   const bool tail = split == a.nsplit - 1 && a.n_tail > 0;
   if (tail) {
-    tail_split<BASE>(a, sm, b, kvh);
+    tail_split<BASE>(a, sm, b, layer, kvh);
     __syncthreads();
   }
 
@@ -1244,7 +1248,7 @@ __global__ __launch_bounds__((Plan<BASE, LH, LL, G>::NT)) void decode_kernel(Dec
       Lsum += sm.tfin.l[h] * sc;
       o += sm.tfin.o[h][c] * sc;
     }
-    float* dst = a.ws + ((int64_t(b) * g.n_kv_heads + kvh) * a.nsplit + split) * 4 * kPartial + h * kPartial;
+    float* dst = a.ws + ((int64_t(vb) * g.n_kv_heads + kvh) * a.nsplit + split) * 4 * kPartial + h * kPartial;
     if (c == 0) {
       st_agent(dst, M);
       st_agent(dst + 1, Lsum);
@@ -1256,14 +1260,14 @@ __global__ __launch_bounds__((Plan<BASE, LH, LL, G>::NT)) void decode_kernel(Dec
   __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
   if (tid == 0) {
-    uint32_t* ctr = a.counters + b * g.n_kv_heads + kvh;
+    uint32_t* ctr = a.counters + vb * g.n_kv_heads + kvh;
     const uint32_t old = __hip_atomic_fetch_add(ctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     sm.last = old == uint32_t(a.nsplit - 1);
     if (sm.last) __hip_atomic_store(ctr, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
   __syncthreads();
   if (!sm.last) return;
-  merge_splits<BASE>(a, sm, b, kvh);
+  merge_splits<BASE>(a, sm, vb, layer, kvh);
 }
 
 template <int BASE, int LH, int LL, int G>
@@ -1291,7 +1295,7 @@ int launch_g(const DecodeArgs& a, hipStream_t st) {
   if constexpr (!fits<BASE, LH, LL, G>()) {
     return -2;
   } else {
-    dim3 grid(a.nsplit, a.g.n_kv_heads, a.g.batch);
+    dim3 grid(a.nsplit, a.g.n_kv_heads, a.g.batch * a.n_layers_launched);
     hipLaunchKernelGGL((decode_kernel<BASE, LH, LL, G>), grid, dim3(Plan<BASE, LH, LL, G>::NT), 0, st, a);
     return hipGetLastError() == hipSuccess ? 0 : -5;
   }

@@ -117,23 +117,26 @@ int64_t decode_slots(const semkv_config& k) {
 // nsplit * waves), so that the whole grid is resident at once and every wave
 // has a record.  The fp16 tail rides with the last workgroup.  0: nothing
 // cached.
-int plan(const semkv_cache* c, int n_tail) {
+// A launch of `layers` layers plans over all their units together.
+int plan(const semkv_cache* c, int n_tail, int layers = 1) {
   const int64_t nt = (c->n_hi + kSlots - 1) / kSlots + (c->n_lo + kSlots - 1) / kSlots;
   if (nt == 0) return n_tail > 0 ? 1 : 0;
-  const int64_t units = int64_t(c->cfg.batch) * c->cfg.n_kv_heads;
+  const int64_t units = int64_t(c->cfg.batch) * c->cfg.n_kv_heads * layers;
   int64_t ns = decode_slots(c->cfg) / units;
   const int nw = decode_waves(c->cfg.base, c->cfg.L_hi, c->cfg.L_lo, c->cfg.group);
   if (ns > nt / nw) ns = nt / nw;
-  if (ns > kMaxSplits) ns = kMaxSplits;
+  if (ns > kMaxSplits / layers) ns = kMaxSplits / layers;
   if (ns < 1) ns = 1;
   return int(ns);
 }
 
 // workspace: [b][kvh] uint32 counters (padded to 256 bytes), then the partials
-size_t counter_bytes(const semkv_config& k) { return size_t((int64_t(k.batch) * k.n_kv_heads * 4 + 255) / 256 * 256); }
+size_t counter_bytes(const semkv_config& k, int layers) {
+  return size_t((int64_t(layers) * k.batch * k.n_kv_heads * 4 + 255) / 256 * 256);
+}
 
-size_t workspace_need(const semkv_config& k, int nsplit) {
-  return counter_bytes(k) + size_t(int64_t(k.batch) * k.n_kv_heads * nsplit * 4 * kPartial * 4);
+size_t workspace_need(const semkv_config& k, int nsplit, int layers) {
+  return counter_bytes(k, layers) + size_t(int64_t(layers) * k.batch * k.n_kv_heads * nsplit * 4 * kPartial * 4);
 }
 
 int close_block(semkv_cache* c, int n, hipStream_t stream) {
@@ -229,7 +232,10 @@ int semkv_cache_sizes(const semkv_config* cfg, semkv_sizes* out) {
   out->flag_bytes = size_t(k.batch * out->flag_words * 4);
   int64_t max_split = out->cap_hi_tiles + out->cap_lo_tiles;
   if (max_split > kMaxSplits) max_split = kMaxSplits;
-  out->workspace_bytes = workspace_need(k, int(max_split));
+  int64_t max_split_all = kMaxSplits / k.n_layers < 1 ? 1 : kMaxSplits / k.n_layers;   // all-layers launch
+  if (max_split_all > max_split) max_split_all = max_split;
+  const size_t one = workspace_need(k, int(max_split), 1), all = workspace_need(k, int(max_split_all), k.n_layers);
+  out->workspace_bytes = one > all ? one : all;
   return SEMKV_OK;
 }
 
@@ -414,30 +420,33 @@ int semkv_flush(semkv_cache* c, hipStream_t stream) {
 
 int semkv_workspace_bytes(const semkv_cache* c, size_t* bytes) {
   if (!c || !bytes) return SEMKV_EINVAL;
-  *bytes = workspace_need(c->cfg, plan(c, 1));
+  const size_t one = workspace_need(c->cfg, plan(c, 1), 1);
+  const size_t all = workspace_need(c->cfg, plan(c, 1, c->cfg.n_layers), c->cfg.n_layers);
+  *bytes = one > all ? one : all;
   return SEMKV_OK;
 }
 
 // Decode launch of one layer; with k_new/v_new, the launch also stores them
 // as the layer's current tail row (the fused append).
-static int decode_launch(const semkv_cache* c, int32_t layer, int n_tail, const uint16_t* k_new,
+static int decode_launch(const semkv_cache* c, int32_t layer, int layers, int n_tail, const uint16_t* k_new,
                          const uint16_t* v_new, const uint16_t* q, float* out, void* workspace, size_t ws_bytes,
                          hipStream_t stream) {
   const semkv_config& k = c->cfg;
   DecodeArgs a;
   memset(&a, 0, sizeof(a));
-  const int nsplit = plan(c, n_tail);
+  const int nsplit = plan(c, n_tail, layers);
   if (nsplit == 0) return SEMKV_ESTATE;      // nothing cached yet
-  if (ws_bytes < workspace_need(k, nsplit)) return SEMKV_EINVAL;
+  if (ws_bytes < workspace_need(k, nsplit, layers)) return SEMKV_EINVAL;
   a.g = geom(c);
   a.tail = c->tail;
   a.k_new = k_new;
   a.v_new = v_new;
   a.q = q;
   a.counters = static_cast<uint32_t*>(workspace);
-  a.ws = reinterpret_cast<float*>(static_cast<uint8_t*>(workspace) + counter_bytes(k));
+  a.ws = reinterpret_cast<float*>(static_cast<uint8_t*>(workspace) + counter_bytes(k, layers));
   a.out = out;
   a.layer = layer;
+  a.n_layers_launched = layers;
   a.n_rows[0] = c->n_hi;
   a.n_rows[1] = c->n_lo;
   a.n_tail = n_tail;
@@ -451,10 +460,16 @@ int semkv_decode_attn(const semkv_cache* c, int32_t layer, const uint16_t* q, fl
                       void* workspace, size_t ws_bytes, hipStream_t stream) {
   if (!c || !q || !out || !workspace) return SEMKV_EINVAL;
   const semkv_config& k = c->cfg;
-  if (layer < 0 || layer >= k.n_layers) return SEMKV_EINVAL;
+  if (layer < -1 || layer >= k.n_layers) return SEMKV_EINVAL;
   if ((uintptr_t(q) & 3) || (uintptr_t(workspace) & 15)) return SEMKV_EINVAL;
+  if (layer == -1) {                         // every layer in one launch: one tail length for all
+    const bool all = all_appended(c), none = none_appended(c);
+    if (!all && !none) return SEMKV_ESTATE;
+    return decode_launch(c, 0, k.n_layers, c->n_scored + (all ? 1 : 0), nullptr, nullptr, q, out, workspace,
+                         ws_bytes, stream);
+  }
   const int n_tail = c->n_scored + (((c->appended[layer >> 5] >> (layer & 31)) & 1u) ? 1 : 0);
-  return decode_launch(c, layer, n_tail, nullptr, nullptr, q, out, workspace, ws_bytes, stream);
+  return decode_launch(c, layer, 1, n_tail, nullptr, nullptr, q, out, workspace, ws_bytes, stream);
 }
 
 int semkv_append_decode(semkv_cache* c, int32_t layer, const uint16_t* k_new, const uint16_t* v_new,
@@ -466,7 +481,7 @@ int semkv_append_decode(semkv_cache* c, int32_t layer, const uint16_t* k_new, co
   if (((c->appended[layer >> 5] >> (layer & 31)) & 1u) != 0) return SEMKV_ESTATE;   // appended already
   if (c->n_hi + c->n_lo + c->n_scored + 1 > k.max_prompt + k.max_new) return SEMKV_ECAPACITY;
   if (c->n_scored >= kSlots) return SEMKV_ESTATE;
-  const int st = decode_launch(c, layer, c->n_scored + 1, k_new, v_new, q, out, workspace, ws_bytes, stream);
+  const int st = decode_launch(c, layer, 1, c->n_scored + 1, k_new, v_new, q, out, workspace, ws_bytes, stream);
   if (st) return st;
   c->appended[layer >> 5] |= 1u << (layer & 31);
   return SEMKV_OK;

@@ -66,12 +66,13 @@ struct DecodeArgs {
   const uint16_t* k_new;   // fused append: this layer's new K/V rows [b][kvh][128], or null
   const uint16_t* v_new;
   const uint16_t* q;       // [b][Hq][128]
-  float* ws;               // partials [b][kvh][nsplit][4][132]
-  uint32_t* counters;      // [b][kvh] finished-split counters, zero between calls
+  float* ws;               // partials [layer of the launch][b][kvh][nsplit][4][132]
+  uint32_t* counters;      // [layer of the launch][b][kvh] finished-split counters, zero between calls
   float* out;              // [b][Hq][128]
-  int32_t layer;
+  int32_t layer;           // first layer of the launch
+  int32_t n_layers_launched; // layers of the launch (q, out, partials, counters: [layer][b]...)
   int64_t n_rows[2];       // rows in the high / low pool
-  int32_t n_tail;          // fp16 tail rows visible to this layer (taken by the last split)
+  int32_t n_tail;          // fp16 tail rows visible to each layer (taken by the last split)
   int32_t nsplit;          // balanced runs of tiles per unit, one workgroup each
   float mu[2][16];         // tq codebooks
 };

@@ -214,3 +214,42 @@ def test_max_batch():
         for p in (0, 1):
             n = u.count(p)
             assert np.array_equal(U.gpu_records(cache, b, 0, 0, p, n), u.records(p)), "sequence %d pool %d" % (b, p)
+
+
+@pytest.mark.parametrize("wl", [0, 4])
+def test_all_layers_launch(wl):
+    """semkv_decode_attn with layer -1 attends over every layer in one launch
+    (queries of all layers given up front); each layer's output is checked
+    against the oracle, before and after the current token is appended to
+    every layer (then read from the fp16 tail)."""
+    import torch
+    from paper_2608_28911_amd import SemKVError
+    cfgw = get_config(wl, n_layers=3, batch=2, n_kv_heads=2, n_q_heads=8)
+    T = 900
+    cache = U.make_cache(cfgw, T, n_layers=3, max_new=4)
+    scores, _, _ = U.prefill(cache, cfgw, T)
+    q = np.stack([synth.query(cfgw, l, 0) for l in range(3)])
+    units = {}
+    for l in range(3):
+        for b in range(2):
+            flag = O.rank(scores[b], cfgw.r_num, cfgw.r_den)[0]
+            for h in range(2):
+                units[(b, l, h)] = U.oracle_unit(cfgw, l, b, h, flag, T)
+    gen = {key: synth.unit_gen_kv(cfgw, key[1], key[0], key[2], 1) for key in units}
+    for step in range(2):
+        out = cache.decode_attn(-1, torch.from_numpy(q).cuda()).cpu().numpy()
+        for (b, l, h), u in units.items():
+            U.assert_attention_close(out[l, b, 4 * h:4 * h + 4], u.attend(q[l, b, 4 * h:4 * h + 4].astype(np.float64)),
+                                     "step %d unit %s" % (step, (b, l, h)))
+        if step == 1:
+            break
+        for l in range(3):
+            k = np.stack([np.stack([gen[(b, l, h)][0][0] for h in range(2)]) for b in range(2)])
+            v = np.stack([np.stack([gen[(b, l, h)][1][0] for h in range(2)]) for b in range(2)])
+            cache.append_kv(l, torch.from_numpy(k).cuda(), torch.from_numpy(v).cuda())
+            for (b, ll, h), u in units.items():
+                if ll == l:
+                    u.append_kv(gen[(b, l, h)][0][0], gen[(b, l, h)][1][0])
+            if l == 0:
+                with pytest.raises(SemKVError):              # layers disagree on the tail length
+                    cache.decode_attn(-1, torch.from_numpy(q).cuda())
