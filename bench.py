@@ -170,6 +170,16 @@ def cpu_baseline(cfgw, seconds):
     t0 = time.perf_counter()
     O.score_kv_norm(Ks)
     t_kn = time.perf_counter() - t0
+    # one thread: the attention of one (layer, kv head) unit at this context
+    K, V = synth.unit_kv(cfgw, 0, 0, 0, T)
+    u1 = O.UnitCache(base, cfgw.L_hi, cfgw.L_lo, cfgw.group, cfgw.r_num, cfgw.r_den,
+                     sign_words=synth.sign_words(cfgw, 0, 0) if cfgw.rotated else None)
+    u1.prefill(K, V, flag)
+    O.set_threads(1)
+    t0 = time.perf_counter()
+    u1.attend(synth.query(cfgw, 0, 0)[0, 0:4].astype(np.float64))
+    t_one = time.perf_counter() - t0
+    O.set_threads(threads)
     return {
         "value": 1.0 / (per_unit * units_per_step) * cfgw.batch,
         "unit": "tokens/s",
@@ -181,6 +191,7 @@ def cpu_baseline(cfgw, seconds):
         "quantize_pack_gbps": q_bytes / t_quant / 1e9,
         "quantize_pack_cores": threads,
         "delta_norm_tokens_per_s": n_tok / t_dn, "key_norm_tokens_per_s": n_tok / t_kn, "indicator_cores": 1,
+        "single_thread_tokens_per_s": 1.0 / (t_one * units_per_step) * cfgw.batch,
     }
 
 

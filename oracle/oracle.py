@@ -72,6 +72,7 @@ def lib():
             "oq_score_hidden": (i32, [i32, P, i32, i64, i32, P]),
             "oq_score_kv_norm": (i32, [P, i32, i64, P]),
             "oq_bf16_to_f32_n": (None, [P, i64, P]),
+            "oq_set_threads": (None, [i32]),
             "oq_f32_to_f16_n": (None, [P, i64, P]),
             "oq_f16_to_f32_n": (None, [P, i64, P]),
         }
@@ -79,6 +80,11 @@ def lib():
             f = getattr(_lib, name)
             f.restype, f.argtypes = res, args
     return _lib
+
+
+def set_threads(n: int) -> None:
+    """OpenMP threads of the row-parallel oracle calls (timing runs only)."""
+    lib().oq_set_threads(int(n))
 
 
 def _p(a: np.ndarray):

@@ -13,6 +13,7 @@
 #include "semkv_oracle.h"
 
 #include <math.h>
+#include <omp.h>
 #include <stdlib.h>
 #include <string.h>
 
@@ -518,3 +519,5 @@ void oq_f32_to_f16_n(const float* x, int64_t n, uint16_t* out) {
 void oq_f16_to_f32_n(const uint16_t* h, int64_t n, float* out) {
   for (int64_t i = 0; i < n; i++) out[i] = oq_f16_to_f32(h[i]);
 }
+
+void oq_set_threads(int n) { omp_set_num_threads(n > 0 ? n : 1); }

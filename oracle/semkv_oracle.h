@@ -98,6 +98,9 @@ void oq_bf16_to_f32_n(const uint16_t* h, int64_t n, float* out);
 void oq_attention(const double* q, int nq, const double* k, const double* v,
                   int64_t n, int D, double* out);
 
+/* OpenMP threads of the row-parallel oracle calls (timing runs). */
+void oq_set_threads(int n);
+
 /* Array forms of the conversions (used by the pins). */
 void oq_f32_to_f16_n(const float* x, int64_t n, uint16_t* out);
 void oq_f16_to_f32_n(const uint16_t* h, int64_t n, float* out);
