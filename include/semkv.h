@@ -67,7 +67,7 @@ enum { SEMKV_STATUS_NAN_SCORE = 1, SEMKV_STATUS_NONFINITE_KV = 2, SEMKV_STATUS_B
  *  block:  deferred block size B of Alg. 2; must be 64.
  *  head_dim must be 128, n_q_heads = 4 * n_kv_heads (GQA group of 4).
  *  max_prompt, max_new: capacity in tokens per sequence (together at most
- *  2^29). */
+ *  2^29).  batch * n_layers at most 65535, n_layers at most 128. */
 typedef struct semkv_config {
   int32_t n_layers, n_kv_heads, n_q_heads, head_dim, batch;
   int32_t base, L_hi, L_lo, group;
@@ -241,7 +241,8 @@ int semkv_dequant(const semkv_cache* c, int32_t layer, float* k_hat, float* v_ha
  * hidden: device, fp16 (SEMKV_DTYPE_F16) or bfloat16 (SEMKV_DTYPE_BF16);
  * element (k, b, t, j) at k*s_state + b*s_batch + t*s_token + j (elements;
  * the norm and variance read state m only, m may be 0).  d_model: a multiple
- * of 8, at most 8192; strides multiples of 8; hidden 16-byte aligned.
+ * of 8, at most 8192; strides multiples of 8; hidden 16-byte aligned;
+ * batch * T below 2^33 (one wave per token).
  * Sums run in fp32 (the score's relative error is below 1e-5 for d <= 8192).
  * A non-finite state gives a non-finite score, which semkv_rank reports. */
 enum { SEMKV_IND_DELTA_NORM = 0, SEMKV_IND_NORM = 1, SEMKV_IND_VARIANCE = 2, SEMKV_IND_COSINE_DELTA = 3 };

@@ -201,6 +201,8 @@ int semkv_cache_sizes(const semkv_config* cfg, semkv_sizes* out) {
   if (k.r_den <= 0 || k.r_num < 0 || k.r_num > k.r_den || k.max_prompt < 0 || k.max_new < 0)
     return SEMKV_EINVAL;
   if (k.max_prompt + k.max_new > (int64_t(1) << 29)) return SEMKV_EINVAL;   // decode splits use 32-bit tile math
+  // launch grids put (sequence x layer) and (kv head x pool) in dimensions of at most 65535
+  if (int64_t(k.batch) * k.n_layers > 65535 || k.n_kv_heads > 4096) return SEMKV_EUNSUPPORTED;
   if (k.head_dim != 128 || k.n_q_heads != 4 * k.n_kv_heads || k.block != 64) return SEMKV_EUNSUPPORTED;
   if (k.base != SEMKV_BASE_AFFINE && k.base != SEMKV_BASE_TQ && k.base != SEMKV_BASE_ROT_AFFINE)
     return SEMKV_EUNSUPPORTED;
@@ -514,6 +516,7 @@ int semkv_score_hidden(int32_t indicator, const void* hidden, int32_t dtype, int
   if ((indicator == SEMKV_IND_DELTA_NORM || indicator == SEMKV_IND_COSINE_DELTA) && m < 1) return SEMKV_EINVAL;
   if (d_model < 8 || d_model % 8) return SEMKV_EINVAL;
   if (d_model > 8192) return SEMKV_EUNSUPPORTED;
+  if ((int64_t(batch) * T + 3) / 4 > int64_t(INT32_MAX)) return SEMKV_EUNSUPPORTED;   // one wave per token
   if ((uintptr_t(hidden) & 15) || (uintptr_t(scores) & 3) || ((s_state | s_batch | s_token) & 7)) return SEMKV_EINVAL;
   HiddenArgs a;
   a.h = static_cast<const uint16_t*>(hidden);

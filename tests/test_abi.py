@@ -65,6 +65,7 @@ def test_sizes_match_the_format(abi):
     (dict(base=1, L_hi=6, L_lo=5), -2), (dict(base=1, L_hi=4, L_lo=3, group=32), -2), (dict(group=16), -2),
     (dict(base=2, L_hi=4, L_lo=3), -2), (dict(base=2, group=16), -2), (dict(base=3), -2),
     (dict(L_hi=8, L_lo=7, group=32), -2), (dict(L_hi=8, L_lo=6), -2), (dict(base=1, L_hi=3, L_lo=2), -2),
+    (dict(batch=1024, n_layers=64), -2),
     (dict(r_num=3, r_den=2), -1), (dict(r_den=0), -1), (dict(batch=0), -1), (dict(max_prompt=-1), -1)])
 def test_config_validation(abi, bad, status):
     s = abi.Sizes()
@@ -98,6 +99,7 @@ def test_calls_validate_before_touching_the_device(abi):
     assert lib.semkv_score_kv_norm(ctypes.byref(c), fake, 0, 0, 0, 64, 16, fake, None) == -1   # sT < 128
     assert lib.semkv_score_kv_norm(ctypes.byref(c), None, 0, 0, 0, 128, 16, fake, None) == -1
     assert lib.semkv_score_hidden(0, fake, 0, 4, 1, 0, 64, 64, 64, 64, fake, None) == -1      # T = 0
+    assert lib.semkv_score_hidden(0, fake, 0, 4, 4, 1 << 32, 64, 64, 64, 64, fake, None) == -2  # grid too large
     rot = cfg_for(abi, base=2)                                                        # needs sign masks too
     assert lib.semkv_cache_init(ctypes.byref(c), ctypes.byref(rot), fake, fake, fake, fake, None, fake) == -1
     assert lib.semkv_cache_init(ctypes.byref(c), ctypes.byref(rot), fake, fake, fake, fake, fake, fake) == 0
