@@ -89,14 +89,15 @@ __device__ uint32_t affine_quarter(const float x[32], int G, uint32_t code[8]) {
   uint16_t s16 = f2h(__fdiv_rn(mx - mn, float(L - 1)));
   float sf = h2f(s16);
   float inv = sf == 0.0f ? 0.0f : __fdiv_rn(1.0f, sf);
-  // rint, clamp to [0, L-1] (NaN -> 0), then one convert-and-insert per code
+  // clamp to [0, L-1] (NaN -> 0), then one convert-and-insert per code: the
+  // convert rounds to nearest even, and with integer bounds clamping before
+  // rounding gives the code rounding before clamping gives
 #pragma unroll
   for (int k = 0; k < 8; ++k) {
     uint32_t w = 0;
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      float c = rintf((x[4 * k + e] - zero) * inv);
-      c = fminf(fmaxf(c, 0.0f), float(L - 1));
+      const float c = fminf(fmaxf((x[4 * k + e] - zero) * inv, 0.0f), float(L - 1));
       w = __builtin_amdgcn_cvt_pk_u8_f32(c, e, w);
     }
     code[k] = w;
@@ -209,9 +210,8 @@ __device__ uint32_t rot_affine_quarter(const float x[32], int q, const uint32_t*
   for (int k = 0; k < 8; ++k) {
     uint32_t w = 0;
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      float c = rintf((y[4 * k + e] - zero) * inv);
-      c = fminf(fmaxf(c, 0.0f), float(L - 1));
+    for (int e = 0; e < 4; ++e) {                         // clamp, then round in the convert
+      const float c = fminf(fmaxf((y[4 * k + e] - zero) * inv, 0.0f), float(L - 1));
       w = __builtin_amdgcn_cvt_pk_u8_f32(c, e, w);
     }
     code[k] = w;
