@@ -59,10 +59,12 @@ __device__ inline void load_quarter(const uint16_t* src, float x[32], bool& nonf
 }
 
 // The value of lane (this lane xor 1), xor 2, or of lane 0 of this lane's
-// quad: exact DPP moves within a quad at full VALU rate.
+// quad: exact DPP moves within a quad at full VALU rate.  Every lane has a
+// source lane, so the move needs no prior value (none to materialize, and the
+// compiler may fold the move into the add that uses it).
 template <int CTRL>
 __device__ inline float quad_mov(float x) {
-  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), CTRL, 0xF, 0xF, false));
+  return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, x), CTRL, 0xF, 0xF, true));
 }
 constexpr int kQuadXor1 = 0xB1, kQuadXor2 = 0x4E, kQuadLane0 = 0x00;
 
@@ -110,7 +112,7 @@ __device__ uint32_t affine_quarter(const float x[32], int G, uint32_t code[8]) {
 // the lanes of the row's quad.
 __device__ inline void rotate_quarter(const float x[32], int q, uint32_t sbits, float u[32]) {
 #pragma unroll
-  for (int i = 0; i < 32; ++i) u[i] = ((sbits >> i) & 1u) ? -x[i] : x[i];
+  for (int i = 0; i < 32; ++i) u[i] = __uint_as_float(__float_as_uint(x[i]) ^ ((sbits << (31 - i)) & 0x80000000u));
 #pragma unroll
   for (int h = 1; h < 32; h <<= 1)
 #pragma unroll
