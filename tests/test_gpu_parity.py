@@ -150,6 +150,36 @@ def test_constant_rows_quantize_exactly():
     U.assert_attention_close(out[0, :4], want, "constant rows")
 
 
+@pytest.mark.parametrize("G", [32, 128])
+def test_affine_code_ties_round_to_even(G):
+    """Rows built so that every group's scale is exactly 1 (range L-1, L the
+    level count the token's rank gives) and half the values sit exactly
+    halfway between two codes: the codes round half to even, bit-exact
+    against the oracle, in both pools."""
+    cfgw = get_config(0, n_kv_heads=1, n_q_heads=4, group=G)
+    T = 256
+    s = synth.all_scores(cfgw, T)
+    f, _, _ = O.rank(s[0], cfgw.r_num, cfgw.r_den)
+    rng = np.random.default_rng(31 + G)
+    X = np.zeros((2, T, 128), np.float32)
+    for kv in range(2):
+        for t in range(T):
+            L = cfgw.L_hi if f[t] else cfgw.L_lo
+            for g in range(128 // G):
+                lo = float(rng.choice([-3.0, -1.5, 0.0, 2.0]))
+                row = lo + rng.integers(0, 2 * (L - 1) + 1, G) / 2.0
+                row[0], row[1] = lo, lo + (L - 1)
+                X[kv, t, g * G:(g + 1) * G] = row
+    assert np.mean(np.abs(X - np.round(X)) == 0.5) > 0.3          # ties are really there
+    K, V = X[0].astype(np.float16)[None, None], X[1].astype(np.float16)[None, None]
+    cache = U.make_cache(cfgw, T, max_new=0)
+    U.prefill(cache, cfgw, T, scores=s, kv=lambda l: (K, V))
+    assert cache.status() == 0
+    u = U.oracle_unit(cfgw, 0, 0, 0, f, T, kv=lambda l: (K, V))
+    for p in (0, 1):
+        assert np.array_equal(U.gpu_records(cache, 0, 0, 0, p, u.count(p)), u.records(p)), "pool %d" % p
+
+
 def test_status_word_reports_nan_and_inf():
     import torch
     cfgw = get_config(0, n_kv_heads=1, n_q_heads=4)
