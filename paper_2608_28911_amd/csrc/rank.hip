@@ -6,8 +6,9 @@
 // keys are taken by increasing token index).  Importance scores are heavily
 // tied (integer Zipf draws, peaked accumulated-attention weights), so the
 // histogram passes put most keys of a wave in one bin: each wave keeps its
-// own histogram and adds its most common bin with a single atomic.  The
-// flag and compaction pass then stages the keys through LDS in segments,
+// own histogram and adds its most common bin with a single atomic.  The keys
+// of the bin the first pass picks are gathered into LDS when they fit, and
+// the remaining passes count only them.  The flag and compaction pass then stages the keys through LDS in segments,
 // loaded coalesced, so that each thread owns a contiguous run of 16 tokens:
 // block-wide prefix counts give every token its tie rank and its slot in the
 // ascending high and low slot lists.
@@ -62,41 +63,58 @@ __global__ __launch_bounds__(kThreads) void rank_kernel(RankArgs a) {
   __shared__ uint32_t wsum[kWaves + 1];
   __shared__ uint32_t s_prefix;
   __shared__ int64_t s_krem;
+  __shared__ uint32_t s_cand, s_ncand;
   const int b = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const float* s = a.scores + int64_t(b) * a.ld_s;
   const int64_t T = a.T, K = a.K;
 
-  // ---- radix select of the K-th largest key, 8 bits per pass
+  // ---- radix select of the K-th largest key, 8 bits per pass.  After the
+  // first pass only the keys of the chosen bin can still decide theta: when
+  // they fit the LDS key buffer they are gathered there once, and the later
+  // passes count them alone instead of reading every score again.
   bool nan_seen = false;
   uint32_t prefix = 0, pmask = 0;
   int64_t krem = K;
   if (K > 0) {
+    bool staged = false;                     // candidates in keys[0, ncand)
+    uint32_t ncand = 0;
     for (int d = 3; d >= 0; --d) {
       for (int i = tid; i < kWaves * 256; i += kThreads) (&hist[0][0])[i] = 0u;
       __syncthreads();
-      for (int64_t i0 = 0; i0 < T; i0 += kBatch * kThreads) {
-        float v[kBatch];                     // all loads of the batch in flight at once
-#pragma unroll
-        for (int j = 0; j < kBatch; ++j) {
-          const int64_t i = i0 + j * kThreads + tid;
-          v[j] = i < T ? s[i] : 0.0f;
+      // add key k (counted when `in`) to this wave's histogram of digit d
+      auto count = [&](uint32_t k, bool in) {
+        const uint32_t bin = (k >> (8 * d)) & 255u;
+        const uint64_t act = __ballot(in);
+        if (act != 0) {
+          // the wave's first counted key's bin in one atomic, the rest singly
+          const int lead = __builtin_ctzll(act);
+          const uint32_t b0 = __shfl(bin, lead);
+          const uint64_t same = __ballot(in && bin == b0);
+          if (lane == lead) atomicAdd(&hist[wave][b0], uint32_t(__popcll(same)));
+          if (in && bin != b0) atomicAdd(&hist[wave][bin], 1u);
         }
+      };
+      if (!staged) {
+        for (int64_t i0 = 0; i0 < T; i0 += kBatch * kThreads) {
+          float v[kBatch];                   // all loads of the batch in flight at once
 #pragma unroll
-        for (int j = 0; j < kBatch; ++j) {
-          const int64_t i = i0 + j * kThreads + tid;
-          nan_seen |= i < T && isnan(v[j]);
-          const uint32_t k = order_key(v[j]);
-          const bool in = i < T && (k & pmask) == prefix;
-          const uint32_t bin = (k >> (8 * d)) & 255u;
-          const uint64_t act = __ballot(in);
-          if (act != 0) {
-            // the wave's first counted key's bin in one atomic, the rest singly
-            const int lead = __builtin_ctzll(act);
-            const uint32_t b0 = __shfl(bin, lead);
-            const uint64_t same = __ballot(in && bin == b0);
-            if (lane == lead) atomicAdd(&hist[wave][b0], uint32_t(__popcll(same)));
-            if (in && bin != b0) atomicAdd(&hist[wave][bin], 1u);
+          for (int j = 0; j < kBatch; ++j) {
+            const int64_t i = i0 + j * kThreads + tid;
+            v[j] = i < T ? s[i] : 0.0f;
           }
+#pragma unroll
+          for (int j = 0; j < kBatch; ++j) {
+            const int64_t i = i0 + j * kThreads + tid;
+            nan_seen |= i < T && isnan(v[j]);
+            const uint32_t k = order_key(v[j]);
+            count(k, i < T && (k & pmask) == prefix);
+          }
+        }
+      } else {
+        for (uint32_t i0 = 0; i0 < ncand; i0 += kThreads) {
+          const uint32_t i = i0 + tid;
+          const uint32_t k = i < ncand ? keys[i] : 0u;
+          count(k, i < ncand && (k & pmask) == prefix);
         }
       }
       __syncthreads();
@@ -112,11 +130,42 @@ __global__ __launch_bounds__(kThreads) void rank_kernel(RankArgs a) {
       if (tid < 256 && int64_t(above) < krem && int64_t(above) + cnt >= krem) {
         s_prefix = prefix | (uint32_t(255 - tid) << (8 * d));
         s_krem = krem - above;
+        s_cand = cnt;
       }
       __syncthreads();
       prefix = s_prefix;
       krem = s_krem;
       pmask |= 255u << (8 * d);
+      if (d > 0 && !staged && s_cand <= uint32_t(kSeg)) {
+        // gather the chosen bin's keys (exactly s_cand of them) into LDS
+        if (tid == 0) s_ncand = 0u;
+        __syncthreads();
+        for (int64_t i0 = 0; i0 < T; i0 += kBatch * kThreads) {
+          float v[kBatch];
+#pragma unroll
+          for (int j = 0; j < kBatch; ++j) {
+            const int64_t i = i0 + j * kThreads + tid;
+            v[j] = i < T ? s[i] : 0.0f;
+          }
+#pragma unroll
+          for (int j = 0; j < kBatch; ++j) {
+            const int64_t i = i0 + j * kThreads + tid;
+            const uint32_t k = order_key(v[j]);
+            const bool in = i < T && (k & pmask) == prefix;
+            const uint64_t act = __ballot(in);
+            if (act != 0) {
+              const int lead = __builtin_ctzll(act);
+              uint32_t base = 0u;
+              if (lane == lead) base = atomicAdd(&s_ncand, uint32_t(__popcll(act)));
+              base = __shfl(base, lead);
+              if (in) keys[base + uint32_t(__popcll(act & ((uint64_t(1) << lane) - 1u)))] = k;
+            }
+          }
+        }
+        __syncthreads();
+        ncand = s_ncand;
+        staged = true;
+      }
       __syncthreads();
     }
   }
