@@ -114,6 +114,17 @@ int oq_rank_k(const float* s, int64_t T, int64_t k, uint8_t* flag) {
 
 /* ------------------------------------------------------ affine quantizer -- */
 
+/* The two fp16 parameters of a group are finite for finite input (reading
+ * R18): an fp16 rounding that overflows to +-inf is stored as +-65504, the
+ * largest finite binary16, and the codes are taken against the stored pair
+ * (clamped to [0, L-1]).  Only 2 levels can overflow the plain affine scale
+ * ((max - min) / 1 may reach 131008); under a rotation the rotated
+ * coordinates themselves may exceed 65504. */
+static uint16_t sat_f16(uint16_t h) {
+  if ((h & 0x7FFFu) == 0x7C00u) return (uint16_t)((h & 0x8000u) | 0x7BFFu);
+  return h;
+}
+
 int oq_affine_row(const uint16_t* x, int L, int G, uint8_t* codes, uint16_t* meta) {
   if (L < 2 || L > 16 || G <= 0 || 128 % G) return OQ_EINVAL;
   int status = OQ_OK;
@@ -127,7 +138,7 @@ int oq_affine_row(const uint16_t* x, int L, int G, uint8_t* codes, uint16_t* met
     }
     float zero = mn + 0.0f;                   /* -0 -> +0 */
     float s32 = (mx - mn) / (float)(L - 1);   /* asymmetric range / (L-1) */
-    uint16_t s16 = oq_f32_to_f16(s32);
+    uint16_t s16 = sat_f16(oq_f32_to_f16(s32));
     float sf = oq_f16_to_f32(s16);
     float inv = sf == 0.0f ? 0.0f : 1.0f / sf;
     meta[2 * g] = s16;
@@ -232,7 +243,8 @@ int oq_tq_row(const uint16_t* x, const uint32_t* sign_words, int L, const float*
  * map, which the affine quantizer does not see apart from fp16 range.  The
  * rotation is summed in fp32 in the order of oq_tq_row, then divided by 16
  * (exact).  Per group of G rotated coordinates: zero = fp16(min y) (-0 taken
- * as +0), scale = fp16(max(0, (max y - zero) / (L-1))), codes as in
+ * as +0), scale = fp16(max(0, (max y - zero) / (L-1))), both saturated to
+ * +-65504 (reading R18: y reaches 128 * 65504 / 16 in magnitude), codes as in
  * oq_affine_row with the stored parameters. */
 int oq_rotaffine_row(const uint16_t* x, const uint32_t* sign_words, int L, int G,
                      uint8_t* codes, uint16_t* meta) {
@@ -258,12 +270,12 @@ int oq_rotaffine_row(const uint16_t* x, const uint32_t* sign_words, int L, int G
       if (y[j] < mn) mn = y[j];
       if (y[j] > mx) mx = y[j];
     }
-    uint16_t z16 = oq_f32_to_f16(mn);
+    uint16_t z16 = sat_f16(oq_f32_to_f16(mn));
     if (z16 == 0x8000u) z16 = 0;
     float zf = oq_f16_to_f32(z16);
     float s32 = (mx - zf) / (float)(L - 1);
     if (!(s32 > 0.0f)) s32 = 0.0f;            /* zero rounded above every value */
-    uint16_t s16 = oq_f32_to_f16(s32);
+    uint16_t s16 = sat_f16(oq_f32_to_f16(s32));
     float sf = oq_f16_to_f32(s16);
     float inv = sf == 0.0f ? 0.0f : 1.0f / sf;
     meta[2 * g] = s16;

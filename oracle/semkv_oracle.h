@@ -33,7 +33,9 @@ int oq_rank_k(const float* s, int64_t T, int64_t k, uint8_t* flag);
 
 /* Affine base quantizer (Sec. 4.1): per group of G channels of one 128-dim
  * row, two fp16 parameters.  codes[128] in [0, L-1]; meta[2*(128/G)] =
- * {scale, zero} per group as fp16 bits. */
+ * {scale, zero} per group as fp16 bits.  A scale whose fp16 rounding
+ * overflows (2 levels, a range above 65504) is stored as 65504 (reading
+ * R18), so finite input always gives finite parameters. */
 int oq_affine_row(const uint16_t* x, int L, int G, uint8_t* codes, uint16_t* meta);
 
 /* Lloyd-Max codebook of the unit Gaussian with L levels (Sec. 4.9), by the
@@ -49,7 +51,8 @@ int oq_tq_row(const uint16_t* x, const uint32_t* sign_words, int L, const float*
 /* Affine base under a Hadamard rotation (Sec. 4.1, Sec. 4.9): the affine
  * quantizer of y = H diag(sign) x / 16 (H the unnormalized Sylvester matrix),
  * per group of G rotated coordinates; zero = fp16(min y), scale =
- * fp16(max(0, (max y - zero) / (L-1))).  meta as oq_affine_row. */
+ * fp16(max(0, (max y - zero) / (L-1))), each saturated to +-65504 where the
+ * fp16 rounding overflows (reading R18).  meta as oq_affine_row. */
 int oq_rotaffine_row(const uint16_t* x, const uint32_t* sign_words, int L, int G,
                      uint8_t* codes, uint16_t* meta);
 
