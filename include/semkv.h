@@ -52,6 +52,10 @@ enum { SEMKV_STATUS_NAN_SCORE = 1, SEMKV_STATUS_NONFINITE_KV = 2, SEMKV_STATUS_B
  *  base:   SEMKV_BASE_AFFINE -- per group of `group` channels, an asymmetric
  *          affine quantizer with two fp16 parameters (scale, zero) (Sec. 4.1);
  *          L_hi, L_lo in {6, 5} (2.585/2.322 bits) or any two of {3,4,5,6}.
+ *          A parameter whose fp16 rounding overflows (the scale at 2 levels
+ *          over a range above 65504; zero or scale of the rotated affine base)
+ *          is stored as +-65504 and the codes follow the stored pair, so
+ *          finite K/V always give finite parameters.
  *          SEMKV_BASE_TQ -- TurboQuant-MSE: random-sign Hadamard rotation and a
  *          Lloyd-Max codebook of the unit Gaussian, one fp16 scalar (the row
  *          norm) per row (Sec. 4.9); L_hi, L_lo in {4, 3} (2.0/1.585 bits).
@@ -142,6 +146,11 @@ int semkv_cache_init(semkv_cache* c, const semkv_config* cfg, void* pools, void*
                      float* tail_scores, uint32_t* flags, const uint32_t* signs,
                      int32_t* status);
 
+/* Eq. (4) sizes of the slot lists semkv_rank writes for a prompt of T tokens
+ * (1 <= T <= max_prompt): n_hi = floor(r T) high-precision tokens, n_lo =
+ * T - n_hi, per sequence.  Pure host arithmetic; enqueues nothing. */
+int semkv_rank_sizes(const semkv_cache* c, int64_t T, int64_t* n_hi, int64_t* n_lo);
+
 /* Eq. (4)-(5) for every sequence: K = floor(r T); the K tokens with the
  * highest scores get the high precision, equal scores ordered by lower token
  * index, -0 equal to +0.  scores: device fp32 [batch][T].  Writes the flag
@@ -192,19 +201,26 @@ int semkv_cache_reset(semkv_cache* c, hipStream_t stream);
  * (semkv_sizes.workspace_bytes bounds it for every count). */
 int semkv_workspace_bytes(const semkv_cache* c, size_t* bytes);
 
-/* Decode attention of one layer: for each sequence b and query head h (KV head
- * h/4), out[b][h] = softmax(q[b][h] . k_t / sqrt(128)) . v_t over every token
- * t of the sequence: both pools (dequantized on the fly) and the fp16 tail
- * rows appended so far, including this layer's current token if appended.
+/* Decode attention of one layer over the mixed-precision cache: the cache
+ * the method builds before decoding is what attention reads at every decoding
+ * step (Sec. 3.1, Fig. 1; Alg. 1, last step), every token at its own
+ * precision, its K and V of every layer and KV head at the same level (Sec.
+ * 3.5, Fig. 5), and the latest partial block of generated tokens at full
+ * precision (Alg. 2).  For each sequence b and query head h (KV head h/4),
+ * out[b][h] = softmax(q[b][h] . k_t / sqrt(128)) . v_t over every token t of
+ * the sequence: both pools (dequantized on the fly) and the fp16 tail rows
+ * appended so far, including this layer's current token if appended.
  * q: device fp16 [batch][n_q_heads][128]; out: device fp32, same shape.
  * layer == -1: every layer in one launch, q and out [n_layers][batch]
  * [n_q_heads][128] (for queries known up front, as in a benchmark; a model
  * computes layer l's query from layer l-1's output); every layer must have
  * appended the current token, or none (else SEMKV_ESTATE).
  * workspace: device, ws_bytes >= semkv_workspace_bytes(); it starts with
- * per-(sequence, kv head) counters that must be zero before the first call
+ * one counter per (layer, sequence, kv head) of the cache -- sized for every
+ * layer whichever kind of launch -- that must be zero before the first call
  * (allocate it zeroed); every call leaves them zero again.  One workspace may
- * serve successive calls on one stream, not concurrent calls. */
+ * serve successive calls of either kind on one stream, not concurrent
+ * calls. */
 int semkv_decode_attn(const semkv_cache* c, int32_t layer, const uint16_t* q, float* out,
                       void* workspace, size_t ws_bytes, hipStream_t stream);
 

@@ -18,6 +18,12 @@ constexpr int kMaxBodyWords = 3072 / 4; // largest body: L = 8
 
 __device__ inline float h2f(uint16_t b) { return __half2float(__ushort_as_half(b)); }
 __device__ inline uint16_t f2h(float f) { return __half_as_ushort(__float2half_rn(f)); }
+// fp16 bits with +-inf replaced by +-65504, the largest finite binary16: the
+// two parameters of a group stay finite for finite input, and the codes are
+// taken against the stored (saturated) pair
+__device__ inline uint16_t sat16(uint16_t h) {
+  return (h & 0x7FFFu) == 0x7C00u ? uint16_t((h & 0x8000u) | 0x7BFFu) : h;
+}
 
 // Correctly rounded fp32 square root of a >= 0.  The hardware result is within
 // one ulp; the neighbour whose rounding interval holds sqrt(a) is chosen by
@@ -89,6 +95,9 @@ __device__ uint32_t affine_quarter(const float x[32], int G, uint32_t code[8]) {
   }
   float zero = mn + 0.0f;                               // -0 -> +0
   uint16_t s16 = f2h(__fdiv_rn(mx - mn, float(L - 1)));
+  // only 2 levels can overflow: (max - min) / 1 reaches 131008, while for
+  // L >= 3 the quotient is at most 65504
+  if constexpr (L == 2) s16 = sat16(s16);
   float sf = h2f(s16);
   float inv = sf == 0.0f ? 0.0f : __fdiv_rn(1.0f, sf);
   // clamp to [0, L-1] (NaN -> 0), then one convert-and-insert per code: the
@@ -180,7 +189,8 @@ __device__ uint16_t tq_quarter(const float x[32], int q, const uint32_t* sw, con
 // Affine quantizer of the rotated row (Sec. 4.1 with its Hadamard rotation):
 // y = H diag(sign) x / 16 (the division is exact), then per group of G
 // rotated coordinates zero = fp16(min y) (-0 stored as +0) and scale =
-// fp16(max(0, (max y - zero) / (L-1))), codes against the stored pair.
+// fp16(max(0, (max y - zero) / (L-1))), each saturated at +-65504, codes
+// against the stored pair.
 // Returns {scale, zero} as fp16 bits (low half = scale).
 template <int L>
 __device__ uint32_t rot_affine_quarter(const float x[32], int q, const uint32_t* sw, int G, uint32_t code[8]) {
@@ -201,11 +211,13 @@ __device__ uint32_t rot_affine_quarter(const float x[32], int q, const uint32_t*
     mn = fminf(mn, quad_mov<kQuadXor2>(mn));
     mx = fmaxf(mx, quad_mov<kQuadXor2>(mx));
   }
-  uint16_t z16 = f2h(mn);
+  // rotated coordinates reach 128 * 65504 / 16 in magnitude: both parameters
+  // saturate at +-65504
+  uint16_t z16 = sat16(f2h(mn));
   z16 = z16 == 0x8000u ? uint16_t(0) : z16;
   const float zero = h2f(z16);
   const float s32 = __fdiv_rn(mx - zero, float(L - 1));
-  const uint16_t s16 = f2h(s32 > 0.0f ? s32 : 0.0f);
+  const uint16_t s16 = sat16(f2h(s32 > 0.0f ? s32 : 0.0f));
   const float sf = h2f(s16);
   const float inv = sf == 0.0f ? 0.0f : __fdiv_rn(1.0f, sf);
 #pragma unroll

@@ -283,3 +283,115 @@ def test_all_layers_launch(wl):
             if l == 0:
                 with pytest.raises(SemKVError):              # layers disagree on the tail length
                     cache.decode_attn(-1, torch.from_numpy(q).cuda())
+
+
+def test_one_workspace_serves_both_launch_kinds():
+    """One workspace serves one-layer and all-layers launches in any order: the
+    counter prefix covers every layer (here 4 x 3 x 8 counters, 384 bytes, more
+    than one 256-byte block), so the partials of a one-layer launch never land
+    on counters an all-layers launch reads.  Every unit of every launch is
+    checked against the oracle."""
+    import torch
+    cfgw = get_config(0, n_layers=4, batch=3, n_kv_heads=8, n_q_heads=32)
+    T = 300
+    cache = U.make_cache(cfgw, T, n_layers=4, max_new=0)
+    scores, _, _ = U.prefill(cache, cfgw, T)
+    ws = torch.zeros((cache.sz.workspace_bytes + 3) // 4, dtype=torch.float32, device="cuda")
+    q = np.stack([synth.query(cfgw, l, 0) for l in range(4)])
+    want = {}
+    for b in range(3):
+        flag = O.rank(scores[b], cfgw.r_num, cfgw.r_den)[0]
+        for l in range(4):
+            for h in range(8):
+                u = U.oracle_unit(cfgw, l, b, h, flag, T)
+                want[(b, l, h)] = u.attend(q[l, b, 4 * h:4 * h + 4].astype(np.float64))
+    qd = torch.from_numpy(q).cuda()
+    for kind in ("layer", "all", "layer", "all", "all"):
+        if kind == "layer":
+            out = np.stack([cache.decode_attn(l, qd[l], workspace=ws).cpu().numpy() for l in range(4)])
+        else:
+            out = cache.decode_attn(-1, qd, workspace=ws).cpu().numpy()
+        for (b, l, h), w in want.items():
+            U.assert_attention_close(out[l, b, 4 * h:4 * h + 4], w, "%s launch, unit %s" % (kind, (b, l, h)))
+    nctr = 4 * 3 * 8
+    assert np.all(ws[:nctr].view(torch.int32).cpu().numpy() == 0), "counters left non-zero"
+
+
+def _huge_rows(rng, n):
+    """fp16 rows over the whole finite range: halves at -+60000 (a range above
+    65504), constant rows of +-9000 (rotated coordinate +-72000), random bit
+    patterns, and unit-scale rows."""
+    X = rng.standard_normal((n, 128)).astype(np.float32)
+    q = n // 4
+    X[:q, :64], X[:q, 64:] = -60000, 60000
+    X[q:2 * q] = rng.choice([-9000.0, 9000.0], (q, 1))
+    bits = rng.integers(0, 0x7C00, (q, 128), dtype=np.uint32).astype(np.uint16)
+    bits |= (rng.integers(0, 2, (q, 128)) << 15).astype(np.uint16)
+    X[2 * q:3 * q] = bits.view(np.float16).astype(np.float32)
+    X = X.astype(np.float16)
+    return X[rng.permutation(n)]
+
+
+@pytest.mark.parametrize("base,lh,ll,G", [("affine", 3, 2, 128), ("rot_affine", 3, 2, 128),
+                                          ("rot_affine", 6, 5, 32), ("rot_affine", 6, 5, 128)])
+def test_huge_rows_saturate_the_parameters(base, lh, ll, G):
+    """Rows whose 2-level affine scale or rotated-affine zero/scale would
+    overflow fp16 (Sec. 4.1's two fp16 parameters, saturated at +-65504):
+    records of both pools bit-exact with the oracle, no inf/NaN stored, and
+    attention finite and close to the oracle's.  Values reach 6e4 here, so
+    the max-abs bar is taken relative to the largest reconstructed value
+    (scaling V scales the output and its error alike)."""
+    import torch
+    cfgw = get_config(0, n_layers=1, n_kv_heads=1, n_q_heads=4, base=base, L_hi=lh, L_lo=ll, group=G)
+    T = 300
+    rng = np.random.default_rng([lh, ll, G, len(base)])
+    K = _huge_rows(rng, T)[None, None]
+    V = _huge_rows(rng, T)[None, None]
+    s = synth.all_scores(cfgw, T)
+    cache = U.make_cache(cfgw, T, max_new=0)
+    U.prefill(cache, cfgw, T, scores=s, kv=lambda l: (K, V))
+    assert cache.status() == 0
+    f = O.rank(s[0], cfgw.r_num, cfgw.r_den)[0]
+    u = U.oracle_unit(cfgw, 0, 0, 0, f, T, kv=lambda l: (K, V))
+    for p in (0, 1):
+        got = U.gpu_records(cache, 0, 0, 0, p, u.count(p))
+        assert np.array_equal(got, u.records(p)), "pool %d" % p
+        kc, km, vc, vm, _ = u.pool(p)
+        assert np.all((km & 0x7C00) != 0x7C00) and np.all((vm & 0x7C00) != 0x7C00)
+    q = (synth.query(cfgw, 0, 0).astype(np.float32) * 1e-3).astype(np.float16)
+    out = cache.decode_attn(0, torch.from_numpy(q).cuda()).cpu().numpy()
+    _, kh, vh = u.dequantized()
+    assert np.all(np.isfinite(kh)) and np.all(np.isfinite(vh))
+    want = u.attend(q[0].astype(np.float64))
+    assert np.all(np.isfinite(out))
+    d = np.abs(out[0] - want).max()
+    assert d <= U.TOL * max(1.0, np.abs(vh).max()), d
+
+
+@pytest.mark.parametrize("pool", [0, 1])
+def test_tq_threshold_ties_bit_exact(pool):
+    """Rows with a rotated coordinate exactly on fl32(rho * tau) for every
+    Lloyd-Max threshold of the pool's level count (and on the zero threshold
+    of 4 levels): strict >, the tie goes to the lower cell, as in the pinned
+    oracle.  All rows go to one pool (r = 1 or r = 0)."""
+    from tests.tie_rows import tq_tie_rows
+    cfgw = get_config(4, n_layers=1, n_kv_heads=1, n_q_heads=4, r_num=1 - pool, r_den=1)
+    mu32, tau32 = O.codebook32(cfgw.L_hi if pool == 0 else cfgw.L_lo)
+    rows = tq_tie_rows(tau32, per_threshold=4)
+    T = 2 * len(rows) + 70
+    X = np.zeros((2, T, 128), np.float16)
+    X[0, :len(rows)] = rows
+    X[1, len(rows):2 * len(rows)] = rows
+    X[:, 2 * len(rows):] = synth.unit_kv(cfgw, 0, 0, 0, 70)[0]
+    K, V = X[0][None, None], X[1][None, None]
+    s = synth.all_scores(cfgw, T)
+    cache = U.make_cache(cfgw, T, max_new=0)
+    # the workload's sign masks would move the ties: use all-positive signs
+    cache.signs.zero_()
+    U.prefill(cache, cfgw, T, scores=s, kv=lambda l: (K, V))
+    assert cache.status() == 0
+    f = O.rank(s[0], cfgw.r_num, cfgw.r_den)[0]
+    u = O.UnitCache(O.TQ, cfgw.L_hi, cfgw.L_lo, 128, cfgw.r_num, cfgw.r_den, sign_words=np.zeros(4, np.uint32))
+    u.prefill(X[0], X[1], f)
+    assert u.count(pool) == T
+    assert np.array_equal(U.gpu_records(cache, 0, 0, 0, pool, T), u.records(pool))
