@@ -282,11 +282,14 @@ def generation(cfgw, cache, gen, dev, outlier_ch):
     }
 
 
-def all_layers_launch(cache, q, ws, args, nL, B, Hq, alg, dev):
+def all_layers_launch(cache, q, ws, args, nL, B, Hq, alg, dev, per_layer_out):
     """The same decode steps with every layer in one launch (queries of all
     layers known up front, which a model does not allow: layer l's query needs
     layer l-1's output).  Reported beside the per-layer headline, labelled: it
-    shows what the kernel sustains once the per-launch latency is amortized."""
+    shows what the kernel sustains once the per-launch latency is amortized.
+    The launch shares the per-layer legs' workspace; its output of the last
+    step must match the per-layer output of that step (other split counts
+    merge in another order: within 2e-3)."""
     import torch
     out_all = torch.empty((nL, B, Hq, 128), dtype=torch.float32, device=dev)
     n_steps = q.shape[0]
@@ -308,10 +311,12 @@ def all_layers_launch(cache, q, ws, args, nL, B, Hq, alg, dev):
     g.replay()
     e1.record()
     torch.cuda.synchronize()
+    diff = (out_all - per_layer_out).abs().max().item()
+    assert diff <= 2e-3, "all-layers launch differs from the per-layer launches by %g" % diff
     us = e0.elapsed_time(e1) * 1e3 / args.steps
     gbps = alg * nL / (us * 1e-6) / 1e9
     return {"us_per_step": round(us, 2), "us_per_layer": round(us / nL, 3), "effective_hbm_gbps": round(gbps, 1),
-            "effective_hbm_frac": round(gbps / HBM_PEAK_GBS, 4),
+            "effective_hbm_frac": round(gbps / HBM_PEAK_GBS, 4), "max_abs_vs_per_layer": diff,
             "note": "all layers in one launch per step (queries given up front); not the headline"}
 
 
@@ -560,7 +565,7 @@ def main():
     alg = algorithmic_decode_bytes(cfgw, n_hi, n_lo)
     achieved = alg / (avg_launch_us * 1e-6) / 1e9
     tokens_per_s = B * args.steps / (ms * 1e-3)
-    all_layers = all_layers_launch(cache, q, ws, args, nL, B, Hq, alg, dev) if args.all_layers else None
+    all_layers = all_layers_launch(cache, q, ws, args, nL, B, Hq, alg, dev, eager_last) if args.all_layers else None
     # streaming-read reference: the key-norm kernel of the indicator leg reads
     # the prompt's K once with trivial arithmetic
     stream_gbps = ind["key_norm_gbps"] if ind is not None else None

@@ -130,13 +130,17 @@ int plan(const semkv_cache* c, int n_tail, int layers = 1) {
   return int(ns);
 }
 
-// workspace: [b][kvh] uint32 counters (padded to 256 bytes), then the partials
-size_t counter_bytes(const semkv_config& k, int layers) {
-  return size_t((int64_t(layers) * k.batch * k.n_kv_heads * 4 + 255) / 256 * 256);
+// workspace: [layer][b][kvh] uint32 counters (padded to 256 bytes), then the
+// partials.  The counter prefix is sized for every layer whatever the launch:
+// a one-layer launch uses its first batch x kv-head counters, an all-layers
+// launch all of them, and the partials of either kind start past the whole
+// prefix, so no launch writes partials where another kind keeps counters.
+size_t counter_bytes(const semkv_config& k) {
+  return size_t((int64_t(k.n_layers) * k.batch * k.n_kv_heads * 4 + 255) / 256 * 256);
 }
 
 size_t workspace_need(const semkv_config& k, int nsplit, int layers) {
-  return counter_bytes(k, layers) + size_t(int64_t(layers) * k.batch * k.n_kv_heads * nsplit * 4 * kPartial * 4);
+  return counter_bytes(k) + size_t(int64_t(layers) * k.batch * k.n_kv_heads * nsplit * 4 * kPartial * 4);
 }
 
 int close_block(semkv_cache* c, int n, hipStream_t stream) {
@@ -303,6 +307,14 @@ int semkv_cache_init(semkv_cache* c, const semkv_config* cfg, void* pools, void*
   return SEMKV_OK;
 }
 
+int semkv_rank_sizes(const semkv_cache* c, int64_t T, int64_t* n_hi, int64_t* n_lo) {
+  if (!c || !n_hi || !n_lo || T < 1) return SEMKV_EINVAL;
+  if (T > c->cfg.max_prompt) return SEMKV_ECAPACITY;
+  *n_hi = top_count(T, c->cfg.r_num, c->cfg.r_den);
+  *n_lo = T - *n_hi;
+  return SEMKV_OK;
+}
+
 int semkv_rank(semkv_cache* c, const float* scores, int64_t T, int32_t* hi_idx, int32_t* lo_idx,
                hipStream_t stream) {
   if (!c || !scores || T < 1) return SEMKV_EINVAL;
@@ -445,7 +457,7 @@ static int decode_launch(const semkv_cache* c, int32_t layer, int layers, int n_
   a.v_new = v_new;
   a.q = q;
   a.counters = static_cast<uint32_t*>(workspace);
-  a.ws = reinterpret_cast<float*>(static_cast<uint8_t*>(workspace) + counter_bytes(k, layers));
+  a.ws = reinterpret_cast<float*>(static_cast<uint8_t*>(workspace) + counter_bytes(k));
   a.out = out;
   a.layer = layer;
   a.n_layers_launched = layers;
