@@ -90,14 +90,21 @@ class SemKVCache:
         self._ws = None
 
     # -- the hot path ------------------------------------------------------
+    def rank_sizes(self, T):
+        """(n_hi, n_lo): the slot-list lengths semkv_rank writes for T tokens."""
+        n_hi, n_lo = ctypes.c_int64(), ctypes.c_int64()
+        check(lib().semkv_rank_sizes(ctypes.byref(self.c), T, ctypes.byref(n_hi), ctypes.byref(n_lo)),
+              "semkv_rank_sizes")
+        return n_hi.value, n_lo.value
+
     def rank(self, scores):
         """scores: fp32 [B, T] on the device -> (hi_idx [B, K], lo_idx [B, T-K]) int32."""
         import torch
         scores = scores.contiguous()
         B, T = scores.shape
-        K = self.cfg.r_num * T // self.cfg.r_den
-        hi = torch.empty((B, K), dtype=torch.int32, device=scores.device)
-        lo = torch.empty((B, T - K), dtype=torch.int32, device=scores.device)
+        n_hi, n_lo = self.rank_sizes(T)
+        hi = torch.empty((B, n_hi), dtype=torch.int32, device=scores.device)
+        lo = torch.empty((B, n_lo), dtype=torch.int32, device=scores.device)
         check(lib().semkv_rank(ctypes.byref(self.c), _ptr(scores), T, _ptr(hi), _ptr(lo), _stream()),
               "semkv_rank")
         return hi, lo

@@ -44,6 +44,7 @@ EXPORTS = {
     "semkv_tq_codebook": (ctypes.c_int, [ctypes.c_int, vp, vp]),
     "semkv_cache_init": (ctypes.c_int, [ctypes.POINTER(Cache), ctypes.POINTER(Config), vp, vp, vp, vp,
                                         vp, vp]),
+    "semkv_rank_sizes": (ctypes.c_int, [ctypes.POINTER(Cache), i64, ctypes.POINTER(i64), ctypes.POINTER(i64)]),
     "semkv_rank": (ctypes.c_int, [ctypes.POINTER(Cache), vp, i64, vp, vp, vp]),
     "semkv_quantize_pack": (ctypes.c_int, [ctypes.POINTER(Cache), i32, vp, vp, i64, i64, i64, i64, i64,
                                            vp, vp, vp]),

@@ -80,6 +80,12 @@ def test_calls_validate_before_touching_the_device(abi):
     assert lib.semkv_cache_init(ctypes.byref(c), ctypes.byref(cfg), None, fake, fake, fake, None, fake) == -1
     assert lib.semkv_cache_init(ctypes.byref(c), ctypes.byref(cfg), fake, fake, fake, fake, None, fake) == 0
     assert c.sz.unit_stride > 0 and c.n_hi == 0
+    nh, nl = ctypes.c_int64(), ctypes.c_int64()
+    for T in (1, 3, 100, 1000):                                                   # Eq. (4) sizes
+        assert lib.semkv_rank_sizes(ctypes.byref(c), T, ctypes.byref(nh), ctypes.byref(nl)) == 0
+        assert nh.value == O.top_count(T, cfg.r_num, cfg.r_den) and nh.value + nl.value == T
+    assert lib.semkv_rank_sizes(ctypes.byref(c), 0, ctypes.byref(nh), ctypes.byref(nl)) == -1
+    assert lib.semkv_rank_sizes(ctypes.byref(c), 4096, ctypes.byref(nh), ctypes.byref(nl)) == -3
     assert lib.semkv_rank(ctypes.byref(c), None, 16, fake, fake, None) == -1
     assert lib.semkv_rank(ctypes.byref(c), fake, 4096, fake, fake, None) == -3          # T > max_prompt
     assert lib.semkv_quantize_pack(ctypes.byref(c), 5, fake, fake, 0, 128, 128, 128, 16, fake, fake, None) == -1
