@@ -70,21 +70,36 @@ def _prefill_and_check(cfgw, n_layers, sampled, max_new=0):
     return cache, oracle
 
 
-def _check_decode(cache, cfgw, oracle, step=0):
+def _check_decode(cache, cfgw, oracle, steps=(0,)):
+    """Attention of the sampled units at the given decode steps (a step's
+    queries are drawn per (layer, step)); the cache is not changed."""
     import torch
-    for l in sorted({l for (_, l, _) in oracle}):
-        q = synth.query(cfgw, l, step)
-        out = cache.decode_attn(l, torch.from_numpy(q).cuda()).cpu().numpy()
-        for (b, ll, h), u in oracle.items():
-            if ll == l:
-                want = u.attend(q[b, 4 * h:4 * h + 4].astype(np.float64))
-                U.assert_attention_close(out[b, 4 * h:4 * h + 4], want, "unit %s" % ((b, l, h),))
+    for step in steps:
+        for l in sorted({l for (_, l, _) in oracle}):
+            q = synth.query(cfgw, l, step)
+            out = cache.decode_attn(l, torch.from_numpy(q).cuda()).cpu().numpy()
+            for (b, ll, h), u in oracle.items():
+                if ll == l:
+                    want = u.attend(q[b, 4 * h:4 * h + 4].astype(np.float64))
+                    U.assert_attention_close(out[b, 4 * h:4 * h + 4], want, "step %d unit %s" % (step, (b, l, h)))
+
+
+def _first_one_last(cfgw):
+    return (0, 1, cfgw.decode_steps - 1)
 
 
 def test_llama8b_b1_t32768_affine_full_size():
     cfgw = get_config("llama8b_kv_b1_t32768_affine")
     cache, oracle = _prefill_and_check(cfgw, 2, [(0, 0, 0), (0, 1, 5)])
-    _check_decode(cache, cfgw, oracle)
+    _check_decode(cache, cfgw, oracle, _first_one_last(cfgw))
+
+
+def test_llama8b_b1_t32768_affine_g32_full_size():
+    """The headline shape with fp16 scale/zero per 32 channels (the metadata
+    granularity of the single-layer workload, Sec. 4.1's parameters)."""
+    cfgw = get_config("llama8b_kv_b1_t32768_affine", group=32)
+    cache, oracle = _prefill_and_check(cfgw, 2, [(0, 0, 7), (0, 1, 2)])
+    _check_decode(cache, cfgw, oracle, _first_one_last(cfgw))
 
 
 def test_llama8b_b1_t32768_rot_affine_full_size():
@@ -97,47 +112,61 @@ def test_llama8b_b1_t32768_rot_affine_full_size():
 def test_batched_b16_t16384_dirichlet_full_size():
     cfgw = get_config("llama8b_kv_b16_t16384_affine_dirichlet")
     cache, oracle = _prefill_and_check(cfgw, 1, [(0, 0, 2), (15, 0, 7), (9, 0, 0)])
-    _check_decode(cache, cfgw, oracle)
+    _check_decode(cache, cfgw, oracle, _first_one_last(cfgw))
 
 
 def test_tq_b1_t131072_full_size():
     cfgw = get_config("llama8b_kv_b1_t131072_tq")
     cache, oracle = _prefill_and_check(cfgw, 1, [(0, 0, 6)])
-    _check_decode(cache, cfgw, oracle)
+    _check_decode(cache, cfgw, oracle, _first_one_last(cfgw))
 
 
 def test_mistral_b4_t32768_generation_full_size():
-    """Prompt of 32768 tokens in 4 sequences, then 130 generated tokens
-    (two closed blocks and an fp16 tail of 2) through the deferred path."""
+    """Prompt of 32768 tokens in 4 sequences, then all 2048 generated tokens
+    through the deferred path (Alg. 2: 32 block closes of 17 high + 47 low
+    rows).  Attention of the sampled units at steps 0, 63, 64, 1023, 2047 and
+    at the step after every close (the new token attends to itself at fp16),
+    and after the last close; at the end the sampled units' pools bit-exact
+    and every sequence's flags of the generated tokens as the block ranking
+    gives them."""
     import torch
     cfgw = get_config("mistral7b_kv_b4_t32768_gen2048_deferred")
-    n_gen = 130
+    n_gen, blk, T = cfgw.n_gen, cfgw.block, cfgw.prompt_len
     sampled = [(0, 0, 1), (3, 0, 6)]
-    cache, oracle = _prefill_and_check(cfgw, 1, sampled, max_new=cfgw.n_gen)
+    cache, oracle = _prefill_and_check(cfgw, 1, sampled, max_new=n_gen)
     B, H = cfgw.batch, cfgw.n_kv_heads
     gen = {(b, h): synth.unit_gen_kv(cfgw, 0, b, h, n_gen) for (b, _, h) in sampled}
     gscore = synth.gen_scores(cfgw, n_gen)
     filler = gen[(sampled[0][0], sampled[0][2])]
+    kall = np.empty((n_gen, B, H, 128), np.float16)
+    vall = np.empty_like(kall)
+    kall[:], vall[:] = filler[0][:, None, None, :], filler[1][:, None, None, :]
+    for (b, h), (gk, gv) in gen.items():
+        kall[:, b, h], vall[:, b, h] = gk, gv
+    kd, vd, sd = torch.from_numpy(kall).cuda(), torch.from_numpy(vall).cuda(), torch.from_numpy(gscore).cuda()
+    checks = {0, 63, 64, 1023, 2047} | set(range(blk, n_gen, blk))
     for i in range(n_gen):
-        k = np.empty((B, H, 128), np.float16)
-        v = np.empty((B, H, 128), np.float16)
-        k[:], v[:] = filler[0][i], filler[1][i]
-        for (b, h), (gk, gv) in gen.items():
-            k[b, h], v[b, h] = gk[i], gv[i]
-        cache.append_kv(0, torch.from_numpy(k).cuda(), torch.from_numpy(v).cuda())
+        cache.append_kv(0, kd[i], vd[i])
         for (b, _, h), u in oracle.items():
             u.append_kv(gen[(b, h)][0][i], gen[(b, h)][1][i])
-        if i == 100:                       # mid-block: 37 rows in the fp16 tail
-            _check_decode(cache, cfgw, oracle, step=i)
-        cache.append_commit(torch.from_numpy(gscore[i]).cuda())
+        if i in checks:
+            _check_decode(cache, cfgw, oracle, (i,))
+        cache.append_commit(sd[i])
         for (b, _, h), u in oracle.items():
             u.commit(gscore[i][b])
     torch.cuda.synchronize()
     assert cache.status() == 0
-    _check_decode(cache, cfgw, oracle, step=n_gen)
+    assert cache.c.n_scored == 0 and cache.c.n_hi + cache.c.n_lo == T + n_gen
+    _check_decode(cache, cfgw, oracle, (n_gen,))                 # after the 32nd close
     for (b, l, h), u in oracle.items():
         for p in (0, 1):
             n = u.count(p)
             assert n == (cache.c.n_hi if p == 0 else cache.c.n_lo)
             got = U.gpu_records(cache, b, l, h, p, n)
             assert np.array_equal(got, u.records(p)), "unit %s pool %d after generation" % ((b, l, h), p)
+    kb = O.block_count(blk, cfgw.r_num, cfgw.r_den)
+    for b in range(B):
+        want = np.concatenate([O.rank_k(gscore[k:k + blk, b], kb) for k in range(0, n_gen, blk)])
+        got = U.flags_bits(cache, b, T + n_gen)[T:]
+        assert np.array_equal(got, want), "generated-token flags, sequence %d" % b
+        assert want.sum() == (n_gen // blk) * kb
