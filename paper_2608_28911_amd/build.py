@@ -30,16 +30,19 @@ SOURCES = {
 
 
 def build(verbose: bool = False) -> str:
-    """Compile every source and link libsemkv.so (always recompiles)."""
+    """Compile every source (in parallel) and link libsemkv.so (always recompiles)."""
+    from concurrent.futures import ThreadPoolExecutor
     os.makedirs(BUILD, exist_ok=True)
-    objs = []
+    cmds, objs = [], []
     for src, extra in SOURCES.items():
         obj = os.path.join(BUILD, src.replace(".hip", ".o"))
-        cmd = [HIPCC, "-c", os.path.join(CSRC, src), "-o", obj] + COMMON + extra
-        if verbose:
-            print(" ".join(cmd), flush=True)
-        subprocess.check_call(cmd)
+        cmds.append([HIPCC, "-c", os.path.join(CSRC, src), "-o", obj] + COMMON + extra)
         objs.append(obj)
+    for cmd in cmds if verbose else ():
+        print(" ".join(cmd), flush=True)
+    with ThreadPoolExecutor(max_workers=min(len(cmds), os.cpu_count() or 1)) as ex:
+        for f in [ex.submit(subprocess.check_call, cmd) for cmd in cmds]:
+            f.result()
     tmp = LIB + ".tmp%d" % os.getpid()
     cmd = [HIPCC, "-shared", "-fPIC", "--offload-arch=gfx950", "-o", tmp] + objs
     if verbose:
