@@ -187,6 +187,17 @@ class SemKVCache:
                                       ws.numel() * ws.element_size(), _stream()), "semkv_decode_attn")
         return out
 
+    def decode_attn_noalloc(self, layer, q, out=None):
+        """decode_attn with the library's own device scratch instead of a
+        workspace (semkv_decode_attn_noalloc: the call allocates nothing)."""
+        import torch
+        q = q.contiguous()
+        if out is None:
+            out = torch.empty(q.shape, dtype=torch.float32, device=q.device)
+        check(lib().semkv_decode_attn_noalloc(ctypes.byref(self.c), layer, _ptr(q), _ptr(out), _stream()),
+              "semkv_decode_attn_noalloc")
+        return out
+
     def append_decode_attn(self, layer, k, v, q, out=None, workspace=None):
         """Fused append + decode of one layer: k, v fp16 [B, H_kv, 128] (this
         layer's new token), q fp16 [B, H_q, 128] -> fp32 [B, H_q, 128]."""

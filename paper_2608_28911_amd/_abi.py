@@ -54,6 +54,7 @@ EXPORTS = {
     "semkv_cache_reset": (ctypes.c_int, [ctypes.POINTER(Cache), vp]),
     "semkv_workspace_bytes": (ctypes.c_int, [ctypes.POINTER(Cache), ctypes.POINTER(sz)]),
     "semkv_decode_attn": (ctypes.c_int, [ctypes.POINTER(Cache), i32, vp, vp, vp, sz, vp]),
+    "semkv_decode_attn_noalloc": (ctypes.c_int, [ctypes.POINTER(Cache), i32, vp, vp, vp]),
     "semkv_append_decode": (ctypes.c_int, [ctypes.POINTER(Cache), i32, vp, vp, vp, vp, vp, sz, vp]),
     "semkv_dequant": (ctypes.c_int, [ctypes.POINTER(Cache), i32, vp, vp, vp]),
     "semkv_score_hidden": (ctypes.c_int, [i32, vp, i32, i32, i32, i64, i32, i64, i64, i64, vp, vp]),

@@ -181,6 +181,42 @@ __global__ void zero_words_kernel(uint32_t* p, int64_t n) {
     p[i] = 0u;
 }
 
+// ---- scratch of semkv_decode_attn_noalloc ----------------------------
+// A file-scope device array holds that entry point's finished-split counters
+// (the first kScratchCounterBytes) and its split partials (the rest), so the
+// call needs no workspace and allocates nothing.  Each GPU the library runs
+// on holds its own copy until the process ends; every call on a GPU shares
+// it.  The counters start at zero (cleared once per device by the set-up
+// below) and every call leaves them zero; the partials are written before
+// they are read.  In host code `scratch` names a host-side stand-in, never
+// the device memory: the device address comes from hipGetSymbolAddress.
+constexpr size_t kScratchBytes = size_t(4) << 20;
+constexpr size_t kScratchCounterBytes = size_t(64) << 10;
+static __device__ __align__(256) uint8_t scratch[kScratchBytes];
+
+// Device address of `scratch` on the current device.  The first call on a
+// device looks it up and clears its counters with a fill kernel on `stream`
+// (a kernel, not a memset node, so that a captured graph replays it).
+int scratch_address(hipStream_t stream, uint8_t** out) {
+  static std::mutex mu;
+  static std::map<int, uint8_t*> known;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return SEMKV_EHIP;
+  std::lock_guard<std::mutex> lock(mu);
+  auto it = known.find(dev);
+  if (it == known.end()) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || p == nullptr) return SEMKV_EHIP;
+    const int64_t words = int64_t(kScratchCounterBytes / 4);
+    hipLaunchKernelGGL(zero_words_kernel, dim3(unsigned((words + 255) / 256)), dim3(256), 0, stream,
+                       static_cast<uint32_t*>(p), words);
+    if (hipGetLastError() != hipSuccess) return SEMKV_EHIP;
+    it = known.emplace(dev, static_cast<uint8_t*>(p)).first;
+  }
+  *out = it->second;
+  return SEMKV_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -442,22 +478,36 @@ int semkv_workspace_bytes(const semkv_cache* c, size_t* bytes) {
 
 // Decode launch of one layer; with k_new/v_new, the launch also stores them
 // as the layer's current tail row (the fused append).
+// Where a decode launch keeps its finished-split counters and its split
+// partials: the caller's workspace, or the library's scratch array.
+struct DecodeScratch {
+  uint32_t* counters;       // [layer][b][kvh], zero between calls
+  size_t counter_bytes;     // bytes available for them
+  float* partials;          // split partials
+  size_t partial_bytes;     // bytes available for them
+};
+
+// Decode launch of one layer; with k_new/v_new, the launch also stores them
+// as the layer's current tail row (the fused append).  `too_small` is the
+// status returned when the plan's counters or partials do not fit `sc`.
 static int decode_launch(const semkv_cache* c, int32_t layer, int layers, int n_tail, const uint16_t* k_new,
-                         const uint16_t* v_new, const uint16_t* q, float* out, void* workspace, size_t ws_bytes,
-                         hipStream_t stream) {
+                         const uint16_t* v_new, const uint16_t* q, float* out, const DecodeScratch& sc,
+                         int too_small, hipStream_t stream) {
   const semkv_config& k = c->cfg;
   DecodeArgs a;
   memset(&a, 0, sizeof(a));
   const int nsplit = plan(c, n_tail, layers);
   if (nsplit == 0) return SEMKV_ESTATE;      // nothing cached yet
-  if (ws_bytes < workspace_need(k, nsplit, layers)) return SEMKV_EINVAL;
+  if (sc.counter_bytes < counter_bytes(k) ||
+      sc.partial_bytes < workspace_need(k, nsplit, layers) - counter_bytes(k))
+    return too_small;
   a.g = geom(c);
   a.tail = c->tail;
   a.k_new = k_new;
   a.v_new = v_new;
   a.q = q;
-  a.counters = static_cast<uint32_t*>(workspace);
-  a.ws = reinterpret_cast<float*>(static_cast<uint8_t*>(workspace) + counter_bytes(k));
+  a.counters = sc.counters;
+  a.ws = sc.partials;
   a.out = out;
   a.layer = layer;
   a.n_layers_launched = layers;
@@ -470,6 +520,17 @@ static int decode_launch(const semkv_cache* c, int32_t layer, int layers, int n_
   return launch_decode(a, stream);
 }
 
+// the caller's workspace: counters for every layer, then the partials
+static DecodeScratch workspace_scratch(const semkv_config& k, void* workspace, size_t ws_bytes) {
+  const size_t cb = counter_bytes(k);
+  DecodeScratch sc;
+  sc.counters = static_cast<uint32_t*>(workspace);
+  sc.counter_bytes = ws_bytes < cb ? ws_bytes : cb;
+  sc.partials = reinterpret_cast<float*>(static_cast<uint8_t*>(workspace) + cb);
+  sc.partial_bytes = ws_bytes > cb ? ws_bytes - cb : 0;
+  return sc;
+}
+
 int semkv_decode_attn(const semkv_cache* c, int32_t layer, const uint16_t* q, float* out,
                       void* workspace, size_t ws_bytes, hipStream_t stream) {
   if (!c || !q || !out || !workspace) return SEMKV_EINVAL;
@@ -479,11 +540,36 @@ int semkv_decode_attn(const semkv_cache* c, int32_t layer, const uint16_t* q, fl
   if (layer == -1) {                         // every layer in one launch: one tail length for all
     const bool all = all_appended(c), none = none_appended(c);
     if (!all && !none) return SEMKV_ESTATE;
-    return decode_launch(c, 0, k.n_layers, c->n_scored + (all ? 1 : 0), nullptr, nullptr, q, out, workspace,
-                         ws_bytes, stream);
+    return decode_launch(c, 0, k.n_layers, c->n_scored + (all ? 1 : 0), nullptr, nullptr, q, out,
+                         workspace_scratch(k, workspace, ws_bytes), SEMKV_EINVAL, stream);
   }
   const int n_tail = c->n_scored + (((c->appended[layer >> 5] >> (layer & 31)) & 1u) ? 1 : 0);
-  return decode_launch(c, layer, 1, n_tail, nullptr, nullptr, q, out, workspace, ws_bytes, stream);
+  return decode_launch(c, layer, 1, n_tail, nullptr, nullptr, q, out, workspace_scratch(k, workspace, ws_bytes),
+                       SEMKV_EINVAL, stream);
+}
+
+int semkv_decode_attn_noalloc(const semkv_cache* c, int32_t layer, const uint16_t* q, float* out,
+                              hipStream_t stream) {
+  if (!c || !q || !out) return SEMKV_EINVAL;
+  const semkv_config& k = c->cfg;
+  if (layer < -1 || layer >= k.n_layers) return SEMKV_EINVAL;
+  if (uintptr_t(q) & 3) return SEMKV_EINVAL;
+  // checks that need no device work come before the set-up
+  const bool all = all_appended(c), none = none_appended(c);
+  if (layer == -1 && !all && !none) return SEMKV_ESTATE;
+  const int n_tail = layer == -1 ? c->n_scored + (all ? 1 : 0)
+                                 : c->n_scored + (((c->appended[layer >> 5] >> (layer & 31)) & 1u) ? 1 : 0);
+  if (plan(c, n_tail, layer == -1 ? k.n_layers : 1) == 0) return SEMKV_ESTATE;
+  uint8_t* base = nullptr;
+  const int st = scratch_address(stream, &base);
+  if (st) return st;
+  DecodeScratch sc;
+  sc.counters = reinterpret_cast<uint32_t*>(base);
+  sc.counter_bytes = kScratchCounterBytes;
+  sc.partials = reinterpret_cast<float*>(base + kScratchCounterBytes);
+  sc.partial_bytes = kScratchBytes - kScratchCounterBytes;
+  if (layer == -1) return decode_launch(c, 0, k.n_layers, n_tail, nullptr, nullptr, q, out, sc, SEMKV_ECAPACITY, stream);
+  return decode_launch(c, layer, 1, n_tail, nullptr, nullptr, q, out, sc, SEMKV_ECAPACITY, stream);
 }
 
 int semkv_append_decode(semkv_cache* c, int32_t layer, const uint16_t* k_new, const uint16_t* v_new,
@@ -495,7 +581,8 @@ int semkv_append_decode(semkv_cache* c, int32_t layer, const uint16_t* k_new, co
   if (((c->appended[layer >> 5] >> (layer & 31)) & 1u) != 0) return SEMKV_ESTATE;   // appended already
   if (c->n_hi + c->n_lo + c->n_scored + 1 > k.max_prompt + k.max_new) return SEMKV_ECAPACITY;
   if (c->n_scored >= kSlots) return SEMKV_ESTATE;
-  const int st = decode_launch(c, layer, 1, c->n_scored + 1, k_new, v_new, q, out, workspace, ws_bytes, stream);
+  const int st = decode_launch(c, layer, 1, c->n_scored + 1, k_new, v_new, q, out,
+                               workspace_scratch(k, workspace, ws_bytes), SEMKV_EINVAL, stream);
   if (st) return st;
   c->appended[layer >> 5] |= 1u << (layer & 31);
   return SEMKV_OK;
