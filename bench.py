@@ -13,6 +13,11 @@ cache (pools resident in HBM).  The K timed steps are one HIP graph replay
 bracketed by events and device synchronization.  The prefill path (rank,
 quantize + pack) is timed separately and reported beside it.
 
+After the headline, the default run measures the other workloads the same way
+(batch 16 at 16K, the Mistral-7B geometry with its 2048 generated tokens, the
+TurboQuant-MSE base at 131K, the single-layer case, and the headline shape with
+32-channel metadata) and reports them under "workloads".
+
 Prints one JSON line.  --gpus N with N > 1 is refused: the library runs on
 one GPU.
 """
@@ -78,6 +83,8 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="budget of the oracle sample")
     ap.add_argument("--no-generate", dest="generate", action="store_false",
                     help="skip the generation leg of workloads with generated tokens")
+    ap.add_argument("--no-others", dest="others", action="store_false",
+                    help="measure the headline workload only (by default the other workloads follow it)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="run a device fill and copy of this many MiB first (hardware counter calibration)")
     return ap.parse_args()
@@ -130,19 +137,22 @@ def indicators(cache, K, gen, dev, reps=3):
 
 
 def cpu_baseline(cfgw, seconds):
-    """The oracle, as it stands, on a bounded sample: decode attention of whole
-    (layer, kv head) units at the workload's context length."""
+    """The oracle, as it stands, on a bounded sample of the headline workload:
+    the (layer, kv head) units of sequence 0 at its context length, each
+    quantized + packed (OpenMP across rows), dequantized in fp64, then the
+    decode attention of all sampled units at once (OpenMP across units, every
+    host core).  Scaled to the units of one decode step."""
     from oracle import oracle as O
     from workloads import synth
     T = cfgw.prompt_len
     base = cfgw.base_id
-    units, t_attn, t_quant, q_bytes = 0, 0.0, 0.0, 0
     s = synth.scores(cfgw, 0, T)
     flag, _, _ = O.rank(s, cfgw.r_num, cfgw.r_den)
-    l = 0
-    while t_attn + t_quant < seconds and units < cfgw.n_layers * cfgw.n_kv_heads:
-        h = units % cfgw.n_kv_heads
-        l = units // cfgw.n_kv_heads
+    threads = O.max_threads()
+    units, t_quant, t_deq, q_bytes = [], 0.0, 0.0, 0
+    n_max = cfgw.n_layers * cfgw.n_kv_heads
+    while len(units) < n_max and (t_quant + t_deq) < 0.5 * seconds:
+        l, h = divmod(len(units), cfgw.n_kv_heads)
         K, V = synth.unit_kv(cfgw, l, 0, h, T)
         u = O.UnitCache(base, cfgw.L_hi, cfgw.L_lo, cfgw.group, cfgw.r_num, cfgw.r_den,
                         sign_words=synth.sign_words(cfgw, l, h) if cfgw.rotated else None)
@@ -152,14 +162,22 @@ def cpu_baseline(cfgw, seconds):
         u.records(1)
         t_quant += time.perf_counter() - t0
         q_bytes += K.nbytes + V.nbytes
-        q = synth.query(cfgw, l, 0)[0, 4 * h:4 * h + 4].astype(np.float64)
         t0 = time.perf_counter()
-        u.attend(q)
-        t_attn += time.perf_counter() - t0
-        units += 1
-    per_unit = t_attn / units
+        _, kh, vh = u.dequantized()
+        t_deq += time.perf_counter() - t0
+        q = synth.query(cfgw, l, 0)[0, 4 * h:4 * h + 4].astype(np.float64)
+        units.append((q, kh, vh))
+    t0 = time.perf_counter()
+    O.attention_units(units)
+    t_attn = time.perf_counter() - t0
+    per_unit = (t_deq + t_attn) / len(units)
     units_per_step = cfgw.n_layers * cfgw.batch * cfgw.n_kv_heads
-    threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    # one thread: the attention of one unit at this context
+    O.set_threads(1)
+    t0 = time.perf_counter()
+    O.attention(*units[0])
+    t_one = time.perf_counter() - t0
+    O.set_threads(threads)
     # the indicators (Sec. 3.3) on 1024 tokens: delta-norm over 5 hidden states
     # of width 4096, key-norm over every layer and kv head (single thread)
     rng = np.random.default_rng(0)
@@ -172,24 +190,20 @@ def cpu_baseline(cfgw, seconds):
     t0 = time.perf_counter()
     O.score_kv_norm(Ks)
     t_kn = time.perf_counter() - t0
-    # one thread: the attention of one (layer, kv head) unit at this context
-    K, V = synth.unit_kv(cfgw, 0, 0, 0, T)
-    u1 = O.UnitCache(base, cfgw.L_hi, cfgw.L_lo, cfgw.group, cfgw.r_num, cfgw.r_den,
-                     sign_words=synth.sign_words(cfgw, 0, 0) if cfgw.rotated else None)
-    u1.prefill(K, V, flag)
-    O.set_threads(1)
-    t0 = time.perf_counter()
-    u1.attend(synth.query(cfgw, 0, 0)[0, 0:4].astype(np.float64))
-    t_one = time.perf_counter() - t0
-    O.set_threads(threads)
+    try:
+        affinity = len(os.sched_getaffinity(0))
+    except AttributeError:
+        affinity = None
     return {
         "value": 1.0 / (per_unit * units_per_step) * cfgw.batch,
         "unit": "tokens/s",
-        "cores": min(threads, 4),
+        "cores": threads,
+        "nproc": os.cpu_count(),
+        "affinity_cpus": affinity,
         "kind": "oracle",
-        "sample": "%d (layer, kv head) units of batch 0 at T=%d: fp64 dequantize + softmax "
-                  "attention of 4 query heads, %.2f s/unit, scaled to %d units per token"
-                  % (units, T, per_unit, units_per_step),
+        "sample": "%d (layer, kv head) units of sequence 0 at T=%d: fp64 dequantize (%.3f s) + softmax "
+                  "attention of 4 query heads, all units in one OpenMP region over %d threads (%.3f s); "
+                  "scaled to %d units per decoded token" % (len(units), T, t_deq, threads, t_attn, units_per_step),
         "quantize_pack_gbps": q_bytes / t_quant / 1e9,
         "quantize_pack_cores": threads,
         "delta_norm_tokens_per_s": n_tok / t_dn, "key_norm_tokens_per_s": n_tok / t_kn, "indicator_cores": 1,
@@ -434,39 +448,21 @@ def multiturn(args, cfgw):
     print(json.dumps(line), flush=True)
 
 
-def main():
-    args = parse()
-    if args.gpus != 1:
-        print("bench.py: the library runs on one GPU; --gpus %d is not supported "
-              "(how the path would shard over GPUs is described with the design notes)" % args.gpus, file=sys.stderr)
-        sys.exit(2)
+def run_workload(args, cfgw, headline):
+    """Prefill (rank, quantize + pack) and the timed decode steps of one
+    workload, inputs generated on the device.  The headline also times the
+    indicators and, on request, the all-layers launch.  Returns the measured
+    figures."""
     import torch
     import paper_2608_28911_amd as P
-    from workloads import get_config, synth
-
-    cfgw = get_config(args.workload)
-    if cfgw.turns:
-        return multiturn(args, cfgw)
-    if args.group or args.base or args.levels or args.ratio:
-        from dataclasses import replace
-        if (args.base or args.levels) and cfgw.base == "tq":
-            sys.exit("--base and --levels apply to the affine workloads")
-        cfgw = replace(cfgw, group=args.group or cfgw.group, base=args.base or cfgw.base)
-        if cfgw.base == "rot_affine":
-            cfgw = replace(cfgw, name=cfgw.name.replace("_affine", "_rot_affine"))
-        if args.levels:
-            lh, ll = (int(x) for x in args.levels.split(","))
-            cfgw = replace(cfgw, L_hi=lh, L_lo=ll, name=cfgw.name + "_L%d%d" % (lh, ll))
-        if args.ratio:
-            rn, rd = (int(x) for x in args.ratio.split("/"))
-            cfgw = replace(cfgw, r_num=rn, r_den=rd, name=cfgw.name + "_r%d_%d" % (rn, rd))
+    from workloads import synth
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     B, H, Hq, T, nL = cfgw.batch, cfgw.n_kv_heads, cfgw.n_q_heads, cfgw.prompt_len, cfgw.n_layers
-    base = cfgw.base_id
-    cfg = P.make_config(n_layers=nL, n_kv_heads=H, batch=B, base=base, L_hi=cfgw.L_hi, L_lo=cfgw.L_lo,
+    gen_leg = args.generate and cfgw.n_gen > 0
+    cfg = P.make_config(n_layers=nL, n_kv_heads=H, batch=B, base=cfgw.base_id, L_hi=cfgw.L_hi, L_lo=cfgw.L_lo,
                         group=cfgw.group, r_num=cfgw.r_num, r_den=cfgw.r_den, max_prompt=T,
-                        max_new=cfgw.n_gen if args.generate else 0)
+                        max_new=cfgw.n_gen if gen_leg else 0)
     signs = synth.all_sign_words(cfgw) if cfgw.rotated else None
     cache = P.SemKVCache(cfg, sign_words=signs)
 
@@ -512,11 +508,11 @@ def main():
     n_hi, n_lo = cache.c.n_hi, cache.c.n_lo
     t_hi, t_lo = -(-n_hi // 64), -(-n_lo // 64)
     quant_bytes = 2 * K.numel() * 2 + nL * B * H * (t_hi * cache.sz.record_bytes_hi + t_lo * cache.sz.record_bytes_lo)
-    ind = indicators(cache, K, gen, dev) if args.indicators else None
-    del K, V
+    ind = indicators(cache, K, gen, dev) if headline and args.indicators else None
+    del K, V, hi, lo
     torch.cuda.empty_cache()
 
-    if args.copy_probe_mib > 0:      # known traffic for counter calibration
+    if headline and args.copy_probe_mib > 0:      # known traffic for counter calibration
         nb = args.copy_probe_mib << 20
         src = torch.empty(nb, dtype=torch.uint8, device=dev).fill_(1)
         dst = torch.empty_like(src)
@@ -536,7 +532,6 @@ def main():
     with torch.cuda.stream(s):
         for i in range(args.warmup):
             step(i)
-        eager_last = None
     torch.cuda.current_stream().wait_stream(s)
     torch.cuda.synchronize()
     # eager reference of the last timed step, to check the graph replays
@@ -559,53 +554,134 @@ def main():
     torch.cuda.synchronize()
     assert torch.equal(out, eager_last), "graph replay differs from eager decode"
     ms = e0.elapsed_time(e1)
-    ms_per_step = ms / args.steps
-    launches = args.steps * nL
-    avg_launch_us = ms * 1e3 / launches
+    del graph
+    avg_launch_us = ms * 1e3 / (args.steps * nL)
     alg = algorithmic_decode_bytes(cfgw, n_hi, n_lo)
     achieved = alg / (avg_launch_us * 1e-6) / 1e9
-    tokens_per_s = B * args.steps / (ms * 1e-3)
-    all_layers = all_layers_launch(cache, q, ws, args, nL, B, Hq, alg, dev, eager_last) if args.all_layers else None
+    r = {"cfgw": cfgw, "ms_per_step": ms / args.steps, "tokens_per_s": B * args.steps / (ms * 1e-3),
+         "decode_us_per_layer": avg_launch_us, "achieved_gbps": achieved, "bytes_per_launch": alg,
+         "quantize_pack_gbps": quant_bytes / (quant_ms * 1e-3) / 1e9, "quantize_pack_ms": quant_ms,
+         "rank_us": rank_us, "rows_hi": n_hi, "rows_lo": n_lo, "indicators": ind}
+    if headline and args.all_layers:
+        r["all_layers_launch"] = all_layers_launch(cache, q, ws, args, nL, B, Hq, alg, dev, eager_last)
+    del q
+    if gen_leg:
+        r["generation"] = generation(cfgw, cache, gen, dev, outlier_ch)
+    del cache
+    torch.cuda.empty_cache()
+    return r
+
+
+def config_of(cfgw, r):
+    return {"workload": cfgw.name, "layers": cfgw.n_layers, "batch": cfgw.batch, "context": cfgw.prompt_len,
+            "kv_heads": cfgw.n_kv_heads, "q_heads": cfgw.n_q_heads, "head_dim": 128, "base": cfgw.base,
+            "levels": [cfgw.L_hi, cfgw.L_lo], "r": cfgw.r_num / cfgw.r_den, "group": cfgw.group,
+            "rows_hi": r["rows_hi"], "rows_lo": r["rows_lo"]}
+
+
+def summary(r):
+    """The per-workload figures of a secondary workload."""
+    cfgw = r["cfgw"]
+    d = {"config": config_of(cfgw, r),
+         "decode_us_per_layer": round(r["decode_us_per_layer"], 3),
+         "tokens_per_s": round(r["tokens_per_s"], 2),
+         "effective_hbm_gbps": round(r["achieved_gbps"], 1),
+         "effective_hbm_frac": round(r["achieved_gbps"] / HBM_PEAK_GBS, 4),
+         "bytes_per_launch": int(r["bytes_per_launch"]),
+         "quantize_pack_gbps": round(r["quantize_pack_gbps"], 1),
+         "quantize_pack_ms": round(r["quantize_pack_ms"], 3),
+         "rank_us": round(r["rank_us"], 1)}
+    if cfgw.n_layers * cfgw.batch * cfgw.n_kv_heads * (r["rows_hi"] + r["rows_lo"]) * 90 < 256 << 20:
+        d["note"] = "the packed cache fits the 256 MB last-level cache: not an HBM measurement"
+    if "generation" in r:
+        d["generation"] = r["generation"]
+    return d
+
+
+# the other workloads the default run measures beside the headline (name,
+# label, overrides): every workload of the suite, and the headline shape with
+# fp16 scale/zero per 32 channels
+SECONDARY = [
+    ("llama8b_kv_b1_t32768_affine", "llama8b_kv_b1_t32768_affine_g32", {"group": 32}),
+    ("single_layer_t2048_affine_g32", "single_layer_t2048_affine_g32", {}),
+    ("llama8b_kv_b16_t16384_affine_dirichlet", "llama8b_kv_b16_t16384_affine_dirichlet", {}),
+    ("mistral7b_kv_b4_t32768_gen2048_deferred", "mistral7b_kv_b4_t32768_gen2048_deferred", {}),
+    ("llama8b_kv_b1_t131072_tq", "llama8b_kv_b1_t131072_tq", {}),
+]
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print("bench.py: the library runs on one GPU; --gpus %d is not supported "
+              "(how the path would shard over GPUs is described with the design notes)" % args.gpus, file=sys.stderr)
+        sys.exit(2)
+    import torch
+    from workloads import get_config
+
+    cfgw = get_config(args.workload)
+    if cfgw.turns:
+        return multiturn(args, cfgw)
+    custom = bool(args.group or args.base or args.levels or args.ratio)
+    if custom:
+        from dataclasses import replace
+        if (args.base or args.levels) and cfgw.base == "tq":
+            sys.exit("--base and --levels apply to the affine workloads")
+        cfgw = replace(cfgw, group=args.group or cfgw.group, base=args.base or cfgw.base)
+        if cfgw.base == "rot_affine":
+            cfgw = replace(cfgw, name=cfgw.name.replace("_affine", "_rot_affine"))
+        if args.group:
+            cfgw = replace(cfgw, name=cfgw.name + "_g%d" % args.group)
+        if args.levels:
+            lh, ll = (int(x) for x in args.levels.split(","))
+            cfgw = replace(cfgw, L_hi=lh, L_lo=ll, name=cfgw.name + "_L%d%d" % (lh, ll))
+        if args.ratio:
+            rn, rd = (int(x) for x in args.ratio.split("/"))
+            cfgw = replace(cfgw, r_num=rn, r_den=rd, name=cfgw.name + "_r%d_%d" % (rn, rd))
+    r = run_workload(args, cfgw, headline=True)
+    ind = r["indicators"]
     # streaming-read reference: the key-norm kernel of the indicator leg reads
     # the prompt's K once with trivial arithmetic
     stream_gbps = ind["key_norm_gbps"] if ind is not None else None
-
+    achieved = r["achieved_gbps"]
     line = {
         "metric": "mixed-prec decode attn tokens/s + effective HBM GB/s (% peak); quantize+pack GB/s",
-        "value": round(tokens_per_s, 2),
+        "value": round(r["tokens_per_s"], 2),
         "unit": "tokens/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": round(ms_per_step, 4),
+        "ms_per_step": round(r["ms_per_step"], 4),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f16",
+        "dtype": "i8 MFMA (fixed-point q and softmax weights, exact i32 sums); f32 softmax",
         "data": "synthetic",
-        "config": {"workload": cfgw.name, "layers": nL, "batch": B, "context": T, "kv_heads": H,
-                   "q_heads": Hq, "head_dim": 128, "base": cfgw.base, "levels": [cfgw.L_hi, cfgw.L_lo],
-                   "r": cfgw.r_num / cfgw.r_den, "group": cfgw.group, "rows_hi": n_hi, "rows_lo": n_lo},
+        "config": config_of(cfgw, r),
         "effective_hbm_gbps": round(achieved, 1),
         "effective_hbm_frac": round(achieved / HBM_PEAK_GBS, 4),
-        "decode_us_per_layer": round(avg_launch_us, 3),
-        "quantize_pack_gbps": round(quant_bytes / (quant_ms * 1e-3) / 1e9, 1),
-        "quantize_pack_ms": round(quant_ms, 3),
-        "rank_us": round(rank_us, 1),
+        "decode_us_per_layer": round(r["decode_us_per_layer"], 3),
+        "quantize_pack_gbps": round(r["quantize_pack_gbps"], 1),
+        "quantize_pack_ms": round(r["quantize_pack_ms"], 3),
+        "rank_us": round(r["rank_us"], 1),
         "stream_read_gbps": stream_gbps,
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBS, 4),
                      "frac_of_stream_read": round(achieved / stream_gbps, 4) if stream_gbps else None,
                      "traffic": measured_traffic() if cfgw.name == "llama8b_kv_b1_t32768_affine" else None,
-                     "kernel": "decode_kernel", "bytes_per_launch": int(alg)},
+                     "kernel": "decode_kernel", "bytes_per_launch": int(r["bytes_per_launch"])},
     }
     if ind is not None:
         line["indicators"] = ind
-    if all_layers is not None:
-        line["all_layers_launch"] = all_layers
-    if args.generate and cfgw.n_gen > 0:
-        del q
-        line["generation"] = generation(cfgw, cache, gen, dev, outlier_ch)
+    if "all_layers_launch" in r:
+        line["all_layers_launch"] = r["all_layers_launch"]
+    if "generation" in r:
+        line["generation"] = r["generation"]
+    if not custom and args.workload == "llama8b_kv_b1_t32768_affine" and args.others:
+        line["workloads"] = {}
+        for name, label, over in SECONDARY:
+            print("bench.py: workload %s" % label, file=sys.stderr, flush=True)
+            line["workloads"][label] = summary(run_workload(args, get_config(name, **over), headline=False))
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(cfgw, args.cpu_seconds)
     print(json.dumps(line), flush=True)

@@ -73,6 +73,8 @@ def lib():
             "oq_score_kv_norm": (i32, [P, i32, i64, P]),
             "oq_bf16_to_f32_n": (None, [P, i64, P]),
             "oq_set_threads": (None, [i32]),
+            "oq_max_threads": (i32, []),
+            "oq_attention_units": (None, [i32, P, i32, P, P, P, i32, P]),
             "oq_f32_to_f16_n": (None, [P, i64, P]),
             "oq_f16_to_f32_n": (None, [P, i64, P]),
         }
@@ -85,6 +87,11 @@ def lib():
 def set_threads(n: int) -> None:
     """OpenMP threads of the row-parallel oracle calls (timing runs only)."""
     lib().oq_set_threads(int(n))
+
+
+def max_threads() -> int:
+    """Threads an OpenMP region of the oracle uses."""
+    return lib().oq_max_threads()
 
 
 def _p(a: np.ndarray):
@@ -300,6 +307,21 @@ def attention(q, khat, vhat) -> np.ndarray:
     assert k.shape[0] >= 1
     lib().oq_attention(_p(q), q.shape[0], _p(k), _p(v), k.shape[0], q.shape[1], _p(out))
     return out
+
+
+def attention_units(units) -> list:
+    """attention(q, khat, vhat) of many independent units at once, OpenMP
+    across the units (timing runs).  units: list of (q, khat, vhat)."""
+    qs = [np.ascontiguousarray(q, np.float64) for q, _, _ in units]
+    ks = [np.ascontiguousarray(k, np.float64) for _, k, _ in units]
+    vs = [np.ascontiguousarray(v, np.float64) for _, _, v in units]
+    outs = [np.zeros(q.shape, np.float64) for q in qs]
+    nq, d = qs[0].shape
+    assert all(q.shape == (nq, d) for q in qs) and all(k.shape[0] >= 1 for k in ks)
+    ptrs = lambda xs: (ctypes.c_void_p * len(xs))(*[x.ctypes.data for x in xs])
+    n = np.array([k.shape[0] for k in ks], np.int64)
+    lib().oq_attention_units(len(units), ptrs(qs), nq, ptrs(ks), ptrs(vs), _p(n), d, ptrs(outs))
+    return outs
 
 
 # ---------------------------------------------------------- indicators ----

@@ -522,6 +522,18 @@ void oq_attention(const double* q, int nq, const double* k, const double* v,
   }
 }
 
+/* Many independent (sequence, layer, kv head) units at once, OpenMP across
+ * the units (each unit's heads in one thread): the same arithmetic as
+ * oq_attention per unit.  Unit u: q[u] [nq][D], k[u], v[u] [n[u]][D],
+ * out[u] [nq][D]. */
+void oq_attention_units(int n_units, const double* const* q, int nq, const double* const* k,
+                        const double* const* v, const int64_t* n, int D, double* const* out) {
+#pragma omp parallel for schedule(dynamic)
+  for (int u = 0; u < n_units; u++) oq_attention(q[u], nq, k[u], v[u], n[u], D, out[u]);
+}
+
+int oq_max_threads(void) { return omp_get_max_threads(); }
+
 /* ------------------------------------------------- array helpers (tests) -- */
 
 void oq_f32_to_f16_n(const float* x, int64_t n, uint16_t* out) {

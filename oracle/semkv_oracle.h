@@ -101,8 +101,15 @@ void oq_bf16_to_f32_n(const uint16_t* h, int64_t n, float* out);
 void oq_attention(const double* q, int nq, const double* k, const double* v,
                   int64_t n, int D, double* out);
 
-/* OpenMP threads of the row-parallel oracle calls (timing runs). */
+/* oq_attention of many independent units, OpenMP across the units (timing
+ * runs on every host core).  Unit u: q[u] [nq][D], k[u], v[u] [n[u]][D]. */
+void oq_attention_units(int n_units, const double* const* q, int nq, const double* const* k,
+                        const double* const* v, const int64_t* n, int D, double* const* out);
+
+/* OpenMP threads of the row-parallel oracle calls (timing runs), and the
+ * number a parallel region uses. */
 void oq_set_threads(int n);
+int oq_max_threads(void);
 
 /* Array forms of the conversions (used by the pins). */
 void oq_f32_to_f16_n(const float* x, int64_t n, uint16_t* out);

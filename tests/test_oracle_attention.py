@@ -78,3 +78,13 @@ def test_sixteen_levels_reduce_to_fp16_attention():
     vc, vm = O.quantize_rows(Vc, 0, 16, 32)
     a = O.attention(q, O.dequantize_rows(kc, km, 0, 16, 32), O.dequantize_rows(vc, vm, 0, 16, 32))
     assert np.array_equal(a, O.attention(q, Kc.astype(np.float64), Vc.astype(np.float64)))
+
+
+def test_attention_units_equals_per_unit_attention():
+    """The unit-parallel form (timing runs) computes each unit exactly as the
+    one-unit call, whatever the unit sizes."""
+    rng = np.random.default_rng(11)
+    units = [(rng.standard_normal((4, 128)), rng.standard_normal((n, 128)), rng.standard_normal((n, 128)))
+             for n in (1, 7, 64, 300, 2049)]
+    for (q, k, v), got in zip(units, O.attention_units(units)):
+        assert np.array_equal(got, O.attention(q, k, v))
