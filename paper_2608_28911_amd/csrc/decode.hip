@@ -78,19 +78,20 @@ struct Traits {
   static constexpr int KSEGW = (NSK * W + 31) / 32;          // normalized dwords of a K segment
   static constexpr int VSEGW = (NSV * W + 31) / 32;
   // decode table: symbol -> operand dwords of digit bytes.  L = 6 splits a
-  // symbol into s mod 216 (3 codes) and s div 216 (2 codes), L = 7 into
-  // s mod 2401 (4 codes) and s div 2401 (3 codes), one dword each.
+  // symbol into s mod 1296 (4 codes, one table dword) and s div 1296 (the
+  // fifth code, which is its own operand dword: no table); L = 7 into s mod
+  // 2401 (4 codes) and s div 2401 (3 codes), one table dword each.
   static constexpr bool SPLIT = L == 6 || L == 7;
-  static constexpr int DIV = L == 6 ? 216 : L == 7 ? 2401 : 1;  // the split's divisor
+  static constexpr int DIV = L == 6 ? 1296 : L == 7 ? 2401 : 1;  // the split's divisor
   static constexpr int TED = SPLIT ? 1 : EDW;                // dwords per table entry
-  static constexpr int NENT = SPLIT ? DIV + ipow(L, n) / DIV : ipow(L, n);   // entries (split: both parts)
+  static constexpr int NENT = L == 6 ? DIV : SPLIT ? DIV + ipow(L, n) / DIV : ipow(L, n);   // entries
   static constexpr int LUTDW = NENT * TED;                   // dwords of one copy
 };
 
 template <int BASE, int L>
 __host__ __device__ constexpr int slot_digit(int w) {
   return (BASE == 1 && L == 4) ? w / 2
-       : L == 6 ? (w < 3 ? w : (w == 4 || w == 5) ? w - 1 : -1)
+       : L == 6 ? (w < 5 ? w : -1)
        : L == 5 ? (w < 3 ? w : -1)
        : L == 3 ? (w < 5 ? w : -1)
        : L == 7 ? (w < 7 ? w : -1)
@@ -103,7 +104,7 @@ __host__ __device__ constexpr int slot_plane(int w) { return (BASE == 1 && L == 
 // of slot_digit / slot_plane
 template <int BASE, int L>
 __host__ __device__ constexpr int digit_slot(int d) {
-  return (BASE == 1 && L == 4) ? 2 * d : L == 6 ? (d < 3 ? d : d + 1) : d;
+  return (BASE == 1 && L == 4) ? 2 * d : d;
 }
 template <int BASE, int L>
 __host__ __device__ constexpr bool digit_slot_inverts() {
@@ -165,15 +166,13 @@ __device__ inline uint32_t field(const uint32_t (&seg)[NW]) {
 // ------------------------------------------------------ decode tables ----
 
 // Dword K of table entry E: the digit bytes of operand slots 4K .. 4K+3 of
-// symbol value E (L = 6: entries 0..215 give s mod 216 -> slots 0-3, entries
-// 216..251 give s div 216 -> slots 4-7).
+// symbol value E (L = 6: entry E < 1296 gives the four codes of s mod 1296 ->
+// slots 0-3; slot 4 holds s div 1296 itself).
 template <int BASE, int L, int K>
 __host__ __device__ constexpr uint32_t entry_dword(uint32_t E) {
   using Tr = Traits<BASE, L>;
   if constexpr (L == 6) {
-    const bool hi = E >= 216;
-    const uint32_t v = hi ? E - 216 : E;
-    return hi ? (v % 6) | ((v / 6) << 8) : (v % 6) | ((v / 6 % 6) << 8) | ((v / 36) << 16);
+    return (E % 6) | ((E / 6 % 6) << 8) | ((E / 36 % 6) << 16) | ((E / 216) << 24);
   } else if constexpr (L == 7) {                             // s mod 2401: 4 codes; s div 2401: 3 codes
     const bool hi = E >= 2401;
     const uint32_t v = hi ? E - 2401 : E;
@@ -194,8 +193,8 @@ __host__ __device__ constexpr uint32_t entry_dword(uint32_t E) {
 }
 
 // the digits a table entry gives, checked against plain base-L arithmetic
-// (L = 6: the entries of both parts, which cover every symbol through
-// v mod 216 and v div 216)
+// (L = 6: the four codes of s mod 1296; L = 7: the entries of both parts,
+// which cover every symbol through s mod 2401 and s div 2401)
 template <int BASE, int L>
 __host__ __device__ constexpr bool entries_match_digits() {
   using Tr = Traits<BASE, L>;
@@ -203,13 +202,21 @@ __host__ __device__ constexpr bool entries_match_digits() {
   for (int E = 0; E < nent; ++E) {
     for (int w = 0; w < Tr::STRIDE; ++w) {
       uint32_t byte = 0, want = 0;
-      if (Tr::SPLIT) {
-        // the low part's entry gives the first digits (3 of base 6, 4 of
-        // base 7) in slots 0-3, the high part's the rest from slot 4 on
+      if (L == 6) {
+        // entries are s mod 1296: four codes in slots 0-3 (slot 4, the
+        // quotient, is not tabled)
+        if (w >= 4) continue;
+        byte = (entry_dword<BASE, L, 0>(uint32_t(E)) >> (8 * w)) & 0xFFu;
+        int c = E;
+        for (int t = 0; t < w; ++t) c /= L;
+        want = uint32_t(c % L);
+      } else if (Tr::SPLIT) {
+        // the low part's entry gives the first four digits of base 7 in
+        // slots 0-3, the high part's the rest from slot 4 on
         const bool hi = w >= 4;
         if (hi != (E >= Tr::DIV)) continue;
         byte = (entry_dword<BASE, L, 0>(uint32_t(E)) >> (8 * (w % 4))) & 0xFFu;
-        const int v = hi ? E - Tr::DIV : E, first = L == 6 ? 3 : 4;
+        const int v = hi ? E - Tr::DIV : E, first = 4;
         const int dg = slot_digit<BASE, L>(w) - (hi ? first : 0);
         if (slot_digit<BASE, L>(w) >= 0) {
           int c = v;
@@ -311,7 +318,7 @@ __host__ __device__ constexpr uint32_t full_symbols() {
 }
 
 // A lane's view of its pool's LDS tables: entry e of its replica is at byte
-// (e << S) + lbase of t; for L = 6 the s div 216 part starts at hbase.
+// (e << S) + lbase of t; for L = 7 the s div 2401 part starts at hbase.
 struct LutRef {
   const uint8_t* t;
   uint32_t lbase, hbase;
@@ -319,19 +326,22 @@ struct LutRef {
 
 __host__ __device__ constexpr int ilog2(int x) { return x <= 1 ? 0 : 1 + ilog2(x / 2); }
 
-// floor(v / 216) for v < 6^5 as the high word of x * M with x = (v << S) + b,
-// b < 2^S a multiple of 4 (the lane's replica offset): one multiplier found by
-// search for S = 7; otherwise b must be 0 and M = ceil(2^(32-S) / 216)
-__host__ __device__ constexpr uint32_t magic216(int S, bool with_base) {
-  return with_base ? (S == 7 ? 155345u : 0u) : uint32_t(((uint64_t(1) << (32 - S)) + 215) / 216);
-}
-__host__ __device__ constexpr bool magic216_exact(int S, bool with_base) {
-  const uint64_t M = magic216(S, with_base);
-  if (M == 0 || M >= (1u << 24) || (7775u << S) + (1u << S) >= (1u << 24)) return false;
-  const uint64_t bmax = with_base ? (1u << S) - 4 : 0;     // x * M is monotonic in b
+// floor(v / 1296) for v < 6^5 as the high word of x * M with x = (v << S) + b,
+// b < 2^S a multiple of 4 (the lane's replica offset): the least M above
+// 2^(32-S) / 1296 that is exact for every v at both ends of b (x * M does not
+// decrease with b), found at compile time.
+__host__ __device__ constexpr bool magic1296_ok(int S, uint64_t M) {
+  if (M >= (1u << 24) || (7775u << S) + (1u << S) >= (1u << 24)) return false;
+  const uint64_t bmax = (1u << S) - 4;
   for (uint64_t v = 0; v < 7776; ++v)
-    if (((v << S) * M) >> 32 != v / 216 || (((v << S) + bmax) * M) >> 32 != v / 216) return false;
+    if (((v << S) * M) >> 32 != v / 1296 || (((v << S) + bmax) * M) >> 32 != v / 1296) return false;
   return true;
+}
+__host__ __device__ constexpr uint32_t magic1296(int S) {
+  const uint64_t m0 = ((uint64_t(1) << (32 - S)) + 1295) / 1296;
+  for (uint64_t M = m0; M < m0 + 64; ++M)
+    if (magic1296_ok(S, M)) return uint32_t(M);
+  return 0u;
 }
 
 // floor(v / 2401) for v < 7^7 as the high word of v * 1788825 (v and the
@@ -359,19 +369,31 @@ __device__ inline uint2 l7_symbol(const uint32_t (&seg)[NW], const uint32_t (&ma
                     *reinterpret_cast<const uint32_t*>(lr.t + ((hi << S) + lr.hbase)));
 }
 
-// operand dwords of 6-level symbol K: the s mod 216 and s div 216 entries
+// operand dwords of 6-level symbol K: the s mod 1296 entry (codes 0-3) and
+// s div 1296 (code 4, a value below 6: its own operand dword)
 template <int BASE, int S, uint32_t FULL, int K, int NW, int NS>
 __device__ inline uint2 l6_symbol(const uint32_t (&seg)[NW], const uint32_t (&maskS)[NS], const LutRef& lr) {
-  constexpr bool WB = magic216_exact(S, true);
-  static_assert(WB || magic216_exact(S, false), "digit split");
-  uint32_t x;                                                            // (v << S) + lbase
-  if constexpr (WB) x = sym_addr<BASE, 6, S, FULL, K, NW, NS>(seg, maskS, lr.lbase);
-  else x = sym_addr<BASE, 6, S, FULL, K, NW, NS>(seg, maskS, 0u);
-  const uint32_t hi = mulhi24(x, magic216(S, WB));                       // v div 216
-  if constexpr (!WB) x = and_or(x, 0xFFFFFFFFu, lr.lbase);
-  const uint32_t lo = mad_i24(hi, -(216 << S), x);                       // ((v mod 216) << S) + lbase
-  return make_uint2(*reinterpret_cast<const uint32_t*>(lr.t + lo),
-                    *reinterpret_cast<const uint32_t*>(lr.t + ((hi << S) + lr.hbase)));
+  constexpr uint32_t M = magic1296(S);
+  static_assert(M != 0, "digit split");
+  const uint32_t x = sym_addr<BASE, 6, S, FULL, K, NW, NS>(seg, maskS, lr.lbase);   // (v << S) + lbase
+  const uint32_t hi = mulhi24(x, M);                                                // v div 1296
+  const uint32_t lo = mad_i24(hi, -(1296 << S), x);                                 // ((v mod 1296) << S) + lbase
+  return make_uint2(*reinterpret_cast<const uint32_t*>(lr.t + lo), hi);
+}
+
+// Operand dwords of symbol slot K of a segment.  A slot past the longest
+// segment (K >= NS, known at compile time) holds no symbol in any lane: its
+// digits are zero and no table is read.  Slots of lanes whose segment is one
+// symbol shorter read table entry 0 (all digits zero) through a zero mask.
+template <int BASE, int L, int S, uint32_t FULL, int K, int NW, int NS>
+__device__ inline uint32_t sym_dword(const uint32_t (&seg)[NW], const uint32_t (&maskS)[NS], const LutRef& lr) {
+  if constexpr (K >= NS) return 0u;
+  else return *reinterpret_cast<const uint32_t*>(lr.t + sym_addr<BASE, L, S, FULL, K, NW, NS>(seg, maskS, lr.lbase));
+}
+template <int BASE, int L, int S, uint32_t FULL, int K, int NW, int NS>
+__device__ inline uint2 sym_dword2(const uint32_t (&seg)[NW], const uint32_t (&maskS)[NS], const LutRef& lr) {
+  if constexpr (K >= NS) return make_uint2(0u, 0u);
+  else return *reinterpret_cast<const uint2*>(lr.t + sym_addr<BASE, L, S, FULL, K, NW, NS>(seg, maskS, lr.lbase));
 }
 
 // MFMA operand of chunk C of a segment (symbols SPC*C ..), read from the tables
@@ -379,23 +401,24 @@ template <int BASE, int L, int S, uint32_t FULL, int C, int NW, int NS>
 __device__ inline int4v chunk_operand(const uint32_t (&seg)[NW], const uint32_t (&maskS)[NS], const LutRef& lr) {
   using Tr = Traits<BASE, L>;
   uint4v r;
-  if constexpr (L == 6) {
-    const uint2 p0 = l6_symbol<BASE, S, FULL, 2 * C, NW, NS>(seg, maskS, lr);
-    const uint2 p1 = l6_symbol<BASE, S, FULL, 2 * C + 1, NW, NS>(seg, maskS, lr);
-    r = uint4v{p0.x, p0.y, p1.x, p1.y};
-  } else if constexpr (L == 7) {
-    const uint2 p0 = l7_symbol<BASE, S, FULL, 2 * C, NW, NS>(seg, maskS, lr);
-    const uint2 p1 = l7_symbol<BASE, S, FULL, 2 * C + 1, NW, NS>(seg, maskS, lr);
+  if constexpr (L == 6 || L == 7) {
+    uint2 p0 = make_uint2(0u, 0u), p1 = make_uint2(0u, 0u);
+    if constexpr (L == 6) {
+      if constexpr (2 * C < NS) p0 = l6_symbol<BASE, S, FULL, 2 * C, NW, NS>(seg, maskS, lr);
+      if constexpr (2 * C + 1 < NS) p1 = l6_symbol<BASE, S, FULL, 2 * C + 1, NW, NS>(seg, maskS, lr);
+    } else {
+      if constexpr (2 * C < NS) p0 = l7_symbol<BASE, S, FULL, 2 * C, NW, NS>(seg, maskS, lr);
+      if constexpr (2 * C + 1 < NS) p1 = l7_symbol<BASE, S, FULL, 2 * C + 1, NW, NS>(seg, maskS, lr);
+    }
     r = uint4v{p0.x, p0.y, p1.x, p1.y};
   } else if constexpr (Tr::SPC == 4) {
-    const uint32_t a = *reinterpret_cast<const uint32_t*>(lr.t + sym_addr<BASE, L, S, FULL, 4 * C, NW, NS>(seg, maskS, lr.lbase));
-    const uint32_t b = *reinterpret_cast<const uint32_t*>(lr.t + sym_addr<BASE, L, S, FULL, 4 * C + 1, NW, NS>(seg, maskS, lr.lbase));
-    const uint32_t c = *reinterpret_cast<const uint32_t*>(lr.t + sym_addr<BASE, L, S, FULL, 4 * C + 2, NW, NS>(seg, maskS, lr.lbase));
-    const uint32_t e = *reinterpret_cast<const uint32_t*>(lr.t + sym_addr<BASE, L, S, FULL, 4 * C + 3, NW, NS>(seg, maskS, lr.lbase));
-    r = uint4v{a, b, c, e};
+    r = uint4v{sym_dword<BASE, L, S, FULL, 4 * C, NW, NS>(seg, maskS, lr),
+               sym_dword<BASE, L, S, FULL, 4 * C + 1, NW, NS>(seg, maskS, lr),
+               sym_dword<BASE, L, S, FULL, 4 * C + 2, NW, NS>(seg, maskS, lr),
+               sym_dword<BASE, L, S, FULL, 4 * C + 3, NW, NS>(seg, maskS, lr)};
   } else {
-    const uint2 a = *reinterpret_cast<const uint2*>(lr.t + sym_addr<BASE, L, S, FULL, 2 * C, NW, NS>(seg, maskS, lr.lbase));
-    const uint2 b = *reinterpret_cast<const uint2*>(lr.t + sym_addr<BASE, L, S, FULL, 2 * C + 1, NW, NS>(seg, maskS, lr.lbase));
+    const uint2 a = sym_dword2<BASE, L, S, FULL, 2 * C, NW, NS>(seg, maskS, lr);
+    const uint2 b = sym_dword2<BASE, L, S, FULL, 2 * C + 1, NW, NS>(seg, maskS, lr);
     r = uint4v{a.x, a.y, b.x, b.y};
   }
   return __builtin_bit_cast(int4v, r);
@@ -515,8 +538,9 @@ struct Plan {
   // table replicas per pool: the most that fit, the low pool (the larger
   // share of the tokens) first (32 dword replicas: a conflict-free lookup of
   // any entries)
-  // (the 7-level tables, 2744 entries, keep 4 replicas: 44 KB)
-  static constexpr int cap(int L) { return L == 7 ? 4 : 32; }
+  // (the 7-level tables, 2744 entries, keep 4 replicas: 44 KB; the 6-level
+  // table, 1296 entries, at most 8: 41 KB)
+  static constexpr int cap(int L) { return L == 7 ? 4 : L == 6 ? 8 : 32; }
   static constexpr int pick_replicas(bool hi) {
     constexpr int opts[8][2] = {{32, 32}, {16, 32}, {8, 32}, {16, 16}, {8, 16}, {8, 8}, {4, 8}, {4, 4}};
     for (const auto& o : opts) {
