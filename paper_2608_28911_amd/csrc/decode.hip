@@ -756,12 +756,14 @@ __device__ void run_pool(const DecodeArgs& a, Shared<PL>& sm, WaveState<PL::NGV>
   for (int k = 0; k < Tr::NSV; ++k) vmask[k] <<= S;
   const int koff0 = seg_off<L, kD, kSlots>(kg, n), kstep = 16 * seg_line_bits<L, kD, kSlots>(kg);
   const int voff0 = seg_off<L, kSlots, kD>(kg, n), vstep = 16 * seg_line_bits<L, kSlots, kD>(kg);
-  // softmax lanes: token n of each 16-token block, head r
-  float zws[NG], qsc[NG];                    // per query group of head r: sum of q, 2^-e
+  // softmax lanes: token n of each 16-token block, head r.  Per query group
+  // of head r, times the softmax scale: the sum of q (zero-point term) and
+  // 2^-e (the fixed-point query's scale); tq folds its level offsets in
+  float zwsK[NG], qscK[NG];
 #pragma unroll
   for (int i = 0; i < NG; ++i) {
-    zws[i] = query_sum<BASE, G>(sm, r, i);
-    qsc[i] = ldexpf(1.0f, -query_exp<BASE, L, G>(sm, mu, r, i));
+    zwsK[i] = query_sum<BASE, G>(sm, r, i) * (kScore * (BASE != 1 ? 1.0f : cZ));
+    qscK[i] = ldexpf(kScore * (BASE != 1 ? 1.0f : cS), -query_exp<BASE, L, G>(sm, mu, r, i));
   }
   // softmax lanes: where token 16 blk + n of each block lands in the weight
   // operands (value group 0, plane 0, row 4r)
@@ -805,18 +807,21 @@ __device__ void run_pool(const DecodeArgs& a, Shared<PL>& sm, WaveState<PL::NGV>
         vm[blk][i] = BASE != 1 ? *reinterpret_cast<const uint32_t*>(vmeta + (i * kSlots + t) * 4)
                                : uint32_t(*reinterpret_cast<const uint16_t*>(vmeta + t * 2));
     }
-    // the score of token 16 blk + n from its products, one per query group
+    // the score of token 16 blk + n from its products, one per query group,
+    // in the softmax's base-2 scale: (q . c) 2^-e s + z (sum q) per group
+    // (tq: rho ((q . c) 2^-e cS + cZ sum q)); masked tokens are set apart
     auto score = [&](int blk, const int4v (&acc)[NG]) {
-      float x = 0.0f;
+      float x;
       if constexpr (BASE != 1) {
+        x = hf(km[blk][0] >> 16) * zwsK[0];
 #pragma unroll
-        for (int i = 0; i < NG; ++i)
-          x += comb3_score(acc[i]) * qsc[i] * hf(km[blk][i] & 0xFFFFu) + hf(km[blk][i] >> 16) * zws[i];
+        for (int i = 1; i < NG; ++i) x = fmaf(hf(km[blk][i] >> 16), zwsK[i], x);
+#pragma unroll
+        for (int i = 0; i < NG; ++i) x = fmaf(comb3_score(acc[i]) * qscK[i], hf(km[blk][i] & 0xFFFFu), x);
       } else {
-        const float rho = hf(uint16_t(km[blk][0]));
-        x = comb3_score(acc[0]) * qsc[0] * (rho * cS) + rho * cZ * zws[0];
+        x = fmaf(comb3_score(acc[0]), qscK[0], zwsK[0]) * hf(uint16_t(km[blk][0]));
       }
-      return 16 * blk + n < nvalid ? x * kScore : -INFINITY;
+      return x;
     };
     // software pipeline: the next block's table reads are in flight during
     // the current block's products
@@ -864,16 +869,25 @@ __device__ void run_pool(const DecodeArgs& a, Shared<PL>& sm, WaveState<PL::NGV>
 #pragma unroll
       for (int blk = 0; blk < 4; ++blk) lg[blk] = score(blk, acck[blk]);
     }
-    // ---- online softmax (base 2) for head r over this record's 64 tokens
+    if (nvalid < kSlots) {                   // the pool's last record: slots past its rows
+#pragma unroll
+      for (int blk = 0; blk < 4; ++blk) lg[blk] = 16 * blk + n < nvalid ? lg[blk] : -INFINITY;
+    }
+    // ---- online softmax (base 2) for head r over this record's 64 tokens,
+    // rescaled lazily: the reference maximum st.m moves only when a score
+    // passes it by more than 8 (weights up to 2^8 fit the fixed-point range),
+    // or on the wave's first record
     float mt = fmaxf(fmaxf(lg[0], lg[1]), fmaxf(lg[2], lg[3]));
     mt = row_max16(mt);
-    const float m_new = fmaxf(st.m, mt);
-    const float alpha = __builtin_amdgcn_exp2f(st.m - m_new);
+    const bool grow = !(mt <= st.m + 8.0f);
+    const float m_new = grow ? mt : st.m;
+    const float alpha = grow ? __builtin_amdgcn_exp2f(st.m - m_new) : 1.0f;
     st.m = m_new;
     float lsum = 0.0f, wmax = 0.0f;
     float wv[4][NGV][Ge::NPL];               // value weights of the lane's tokens
+    float zadd[NGV];
 #pragma unroll
-    for (int i = 0; i < NGV; ++i) st.z[i] *= alpha;
+    for (int i = 0; i < NGV; ++i) zadd[i] = 0.0f;
 #pragma unroll
     for (int blk = 0; blk < 4; ++blk) {
       const float p = __builtin_amdgcn_exp2f(lg[blk] - m_new);   // 0 for masked tokens
@@ -885,7 +899,7 @@ __device__ void run_pool(const DecodeArgs& a, Shared<PL>& sm, WaveState<PL::NGV>
           const uint32_t m = vm[blk][i];
           wv[blk][i][0] = pr * hf(m & 0xFFFFu);
           wmax = fmaxf(wmax, wv[blk][i][0]);
-          st.z[i] += pr * hf(m >> 16);
+          zadd[i] = fmaf(pr, hf(m >> 16), zadd[i]);
         }
       } else {
         const float rho = hf(uint16_t(vm[blk][0]));
@@ -894,16 +908,19 @@ __device__ void run_pool(const DecodeArgs& a, Shared<PL>& sm, WaveState<PL::NGV>
           wv[blk][0][pl] = p * rho * cS * wP[pl];
           wmax = fmaxf(wmax, wv[blk][0][pl]);
         }
-        st.z[0] += p * rho * cZ;
+        zadd[0] = fmaf(p * rho, cZ, zadd[0]);
       }
     }
-    st.l = st.l * alpha + lsum;
-    // ---- the integer value sums hold weights of one scale and one running
+    // ---- the integer value sums hold weights of one scale and one reference
     // maximum: fold them into the float sums when the maximum moves or this
-    // record's weights would not fit 21 bits, and re-pick the scale
-    const bool flush = alpha != 1.0f || wmax * st.qw >= 2097152.0f;
+    // record's weights would not fit 21 bits (their rounding stays below
+    // 2^21 - 1, so the top byte stays below 128), and re-pick the scale
+    const bool flush = grow || wmax * st.qw >= 2097151.0f;
     if (__builtin_amdgcn_ballot_w64(flush) != 0) {
       wmax = row_max16(wmax);
+      st.l *= alpha;
+#pragma unroll
+      for (int i = 0; i < NGV; ++i) st.z[i] *= alpha;
 #pragma unroll
       for (int cb = 0; cb < 8; ++cb) {
         st.of[cb] = (st.of[cb] + comb3(st.cv[cb]) * st.qwi) * alpha;
@@ -914,6 +931,9 @@ __device__ void run_pool(const DecodeArgs& a, Shared<PL>& sm, WaveState<PL::NGV>
       st.qw = ldexpf(1.0f, e);
       st.qwi = ldexpf(1.0f, -e);
     }
+    st.l += lsum;
+#pragma unroll
+    for (int i = 0; i < NGV; ++i) st.z[i] += zadd[i];
     // ---- values: C[(h, byte)][channel] += weights (tokens) x V codes, one
     // value group's int8 weights (byte s of rint(w qw) in row 4r + s) at a time
     int4v Aw[Tr::NCV];
@@ -926,9 +946,11 @@ __device__ void run_pool(const DecodeArgs& a, Shared<PL>& sm, WaveState<PL::NGV>
         for (int blk = 0; blk < 4; ++blk)
 #pragma unroll
           for (int pl = 0; pl < Ge::NPL; ++pl) {
-            const uint32_t q = uint32_t(rintf(wv[blk][gv][pl] * st.qw));   // < 2^21
+            // the integer nearest w qw (< 2^21 - 1) in the low mantissa bits
+            // of w qw + 1.5 2^23 (one rounding of the exact sum)
+            const uint32_t q = __float_as_uint(fmaf(wv[blk][gv][pl], st.qw, 12582912.0f));
             uint8_t* w = pvw + pvwr[blk] + pl;
-            w[0] = uint8_t(q >> 14);
+            w[0] = uint8_t((q >> 14) & 127u);
             w[16] = uint8_t((q >> 7) & 127u);
             w[32] = uint8_t(q & 127u);
           }
