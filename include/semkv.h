@@ -227,16 +227,16 @@ int semkv_decode_attn(const semkv_cache* c, int32_t layer, const uint16_t* q, fl
 /* For callers that cannot allocate (code under HIP graph capture, tight
  * serving loops, harnesses that forbid hipMalloc): semkv_decode_attn without
  * a workspace, same arguments, semantics and results otherwise.  The split
- * counters and partials live in a 4 MiB device array of the library (64 KiB
- * of counters, one per (layer, sequence, kv head) of the cache: at most
- * 16384; the rest for the partials, 2112 bytes per split of a (layer,
- * sequence, kv head): a launch needs about max(256 compute units, its units)
- * of them, so one layer up to ~1900 (sequence, kv head) units).  A cache or
- * launch beyond either bound returns SEMKV_ECAPACITY before anything is
- * enqueued.  The array is held by each GPU the library runs on until the
- * process ends; the first call on a GPU also enqueues a kernel that clears
- * its counters.  The call allocates and frees nothing.  All calls on one GPU
- * share the array: calls that overlap in time on one GPU (other streams, other
+ * counters and partials live in an 8 MiB device array of the library (1 MiB
+ * of counters, one per (layer, sequence, kv head) of the cache on its own
+ * 256-byte line: at most 4096; the rest for the partials, 2112 bytes per split
+ * of a (layer, sequence, kv head): a launch needs about max(256 compute units,
+ * its units) of them, so one layer up to ~3400 (sequence, kv head) units).  A
+ * cache or launch beyond either bound returns SEMKV_ECAPACITY before anything
+ * is enqueued.  The array is held by each GPU the library runs on until the
+ * process ends; the first call on a GPU also enqueues a kernel that clears its
+ * counters.  The call allocates and frees nothing.  All calls on one GPU share
+ * the array: calls that overlap in time on one GPU (other streams, other
  * threads, not serialized) race and give wrong results; serialize them. */
 int semkv_decode_attn_noalloc(const semkv_cache* c, int32_t layer, const uint16_t* q, float* out,
                               hipStream_t stream);

@@ -1306,7 +1306,7 @@ __global__ __launch_bounds__((Plan<BASE, LH, LL, G>::NT)) void decode_kernel(Dec
   __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
   if (tid == 0) {
-    uint32_t* ctr = a.counters + vb * g.n_kv_heads + kvh;
+    uint32_t* ctr = a.counters + (vb * g.n_kv_heads + kvh) * kCounterStride;
     const uint32_t old = __hip_atomic_fetch_add(ctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     sm.last = old == uint32_t(a.nsplit - 1);
     if (sm.last) __hip_atomic_store(ctr, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);

@@ -130,13 +130,13 @@ int plan(const semkv_cache* c, int n_tail, int layers = 1) {
   return int(ns);
 }
 
-// workspace: [layer][b][kvh] uint32 counters (padded to 256 bytes), then the
+// workspace: [layer][b][kvh] uint32 counters, one per 256-byte line, then the
 // partials.  The counter prefix is sized for every layer whatever the launch:
 // a one-layer launch uses its first batch x kv-head counters, an all-layers
 // launch all of them, and the partials of either kind start past the whole
 // prefix, so no launch writes partials where another kind keeps counters.
 size_t counter_bytes(const semkv_config& k) {
-  return size_t((int64_t(k.n_layers) * k.batch * k.n_kv_heads * 4 + 255) / 256 * 256);
+  return size_t(int64_t(k.n_layers) * k.batch * k.n_kv_heads * kCounterStride * 4);
 }
 
 size_t workspace_need(const semkv_config& k, int nsplit, int layers) {
@@ -190,8 +190,8 @@ __global__ void zero_words_kernel(uint32_t* p, int64_t n) {
 // below) and every call leaves them zero; the partials are written before
 // they are read.  In host code `scratch` names a host-side stand-in, never
 // the device memory: the device address comes from hipGetSymbolAddress.
-constexpr size_t kScratchBytes = size_t(4) << 20;
-constexpr size_t kScratchCounterBytes = size_t(64) << 10;
+constexpr size_t kScratchBytes = size_t(8) << 20;
+constexpr size_t kScratchCounterBytes = size_t(1) << 20;
 static __device__ __align__(256) uint8_t scratch[kScratchBytes];
 
 // Device address of `scratch` on the current device.  The first call on a

@@ -103,6 +103,10 @@ struct KvNormArgs {
 };
 
 constexpr int kPartial = 132;  // m, l, 2 pad, o[128]
+// dwords between the finished-split counters of two (layer, sequence, kv
+// head) units: one counter per 256-byte line, so the workgroups of different
+// units do not queue their atomics on one line
+constexpr int kCounterStride = 64;
 constexpr int kMaxSplits = 256;   // splits per (sequence, kv head)
 
 int launch_rank(const RankArgs& a, int batch, hipStream_t s);

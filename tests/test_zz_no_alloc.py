@@ -49,7 +49,7 @@ def test_noalloc_matches_workspace_entry_point_twice():
 def test_noalloc_refuses_beyond_the_scratch():
     import torch
     import paper_2608_28911_amd as P
-    # 32 layers x 128 sequences x 8 kv heads = 32768 counters > 16384
+    # 32 layers x 128 sequences x 8 kv heads = 32768 counters > 4096
     cfg = P.make_config(n_layers=32, n_kv_heads=8, batch=128, base=P.BASE_AFFINE, L_hi=6, L_lo=5, group=128,
                         r_num=26, r_den=100, max_prompt=64, max_new=0)
     cache = P.SemKVCache(cfg)
