@@ -1116,20 +1116,20 @@ __device__ void merge_splits(const DecodeArgs& a, Shared<PL>& sm, int vb, int la
   for (int s0 = q; mine && s0 < ns; s0 += 4 * kBatch) {
     float mv[kBatch], lv[kBatch];
     float4v x[kBatch];
+    // all loads issued at once, unconditionally (one round trip): a split
+    // past the last reads zeros through the buffer descriptor and is given
+    // m = -inf afterwards
 #pragma unroll
     for (int k = 0; k < kBatch; ++k) {
       const int sp = s0 + 4 * k;
-      mv[k] = -INFINITY;
-      lv[k] = 0.0f;
-      x[k] = float4v{0, 0, 0, 0};
-      if (sp < ns) {
-        const int off = (sp * 4 + h) * kPartial * 4;
-        const auto ml = __builtin_amdgcn_raw_buffer_load_b64(rs, off, 0, kCoherent);
-        mv[k] = __uint_as_float(ml[0]);
-        lv[k] = __uint_as_float(ml[1]);
-        x[k] = __builtin_bit_cast(float4v, __builtin_amdgcn_raw_buffer_load_b128(rs, off + 16 + 16 * cq, 0, kCoherent));
-      }
+      const int off = (sp * 4 + h) * kPartial * 4;
+      const auto ml = __builtin_amdgcn_raw_buffer_load_b64(rs, off, 0, kCoherent);
+      mv[k] = __uint_as_float(ml[0]);
+      lv[k] = __uint_as_float(ml[1]);
+      x[k] = __builtin_bit_cast(float4v, __builtin_amdgcn_raw_buffer_load_b128(rs, off + 16 + 16 * cq, 0, kCoherent));
     }
+#pragma unroll
+    for (int k = 0; k < kBatch; ++k) mv[k] = s0 + 4 * k < ns ? mv[k] : -INFINITY;
     float Mn = M;
 #pragma unroll
     for (int k = 0; k < kBatch; ++k) Mn = fmaxf(Mn, mv[k]);
