@@ -29,13 +29,24 @@ SLOTS = 64
 D = 128
 
 
+# OQ_SANITIZE=1 selects a separate build instrumented with AddressSanitizer
+# and UndefinedBehaviorSanitizer (any finding aborts the process); the Python
+# process must then start with libasan preloaded (tests/test_oracle_sanitized.py
+# runs the CPU oracle tests that way).
+SANITIZE = os.environ.get("OQ_SANITIZE") == "1"
+if SANITIZE:
+    LIB = os.path.join(HERE, "liboracle_san.so")
+
+
 def build(force: bool = False) -> str:
     """Compile liboracle.so with gcc (IEEE single precision, no contraction)."""
     if force or not os.path.exists(LIB) or os.path.getmtime(LIB) < max(
             os.path.getmtime(SRC), os.path.getmtime(os.path.join(HERE, "semkv_oracle.h"))):
         tmp = LIB + ".tmp%d" % os.getpid()
+        san = ["-fsanitize=address,undefined", "-fno-sanitize-recover=all",
+               "-fno-omit-frame-pointer", "-g"] if SANITIZE else []
         subprocess.check_call(["gcc", "-O2", "-ffp-contract=off", "-fno-fast-math", "-fopenmp",
-                               "-Wall", "-shared", "-fPIC", "-o", tmp, SRC, "-lm"])
+                               "-Wall", "-shared", "-fPIC"] + san + ["-o", tmp, SRC, "-lm"])
         os.replace(tmp, LIB)
     return LIB
 

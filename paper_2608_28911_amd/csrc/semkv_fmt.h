@@ -12,12 +12,8 @@
 // symbols p = j, j+4, j+8, ...; a body is segment 0 of all lines, then
 // segments 1, 2, 3, LSB first, zero padded to 16 bytes.
 #pragma once
+#include <hip/hip_runtime.h>
 #include <stdint.h>
-
-#ifndef __HIPCC__
-#define __host__
-#define __device__
-#endif
 
 namespace semkv {
 
