@@ -100,7 +100,12 @@ typedef struct semkv_config {
  *          generated tokens not yet quantized (Alg. 2).
  *  tail_scores: fp32 [batch][64].
  *  flags:  uint32 [batch][flag_words]: bit i%32 of word i/32 is 1 iff token i
- *          has the high precision (the 1-bit per-token flag of Sec. 4.1).
+ *          has the high precision (the 1-bit per-token flag of Sec. 4.1);
+ *          then (from word batch*flag_words rounded up to a multiple of 64)
+ *          the ranker's scratch for prompts longer than 4096 tokens, per
+ *          sequence three histograms of 2048, 2048 and 1024 words, which are
+ *          zero again when each semkv_rank call ends, 16 words of selection
+ *          state and two counts per 4096-token chunk.  flag_bytes covers both.
  *  workspace: scratch of semkv_decode_attn. */
 typedef struct semkv_sizes {
   size_t pool_bytes, tail_bytes, tail_score_bytes, flag_bytes, workspace_bytes;
@@ -157,7 +162,10 @@ int semkv_rank_sizes(const semkv_cache* c, int64_t T, int64_t* n_hi, int64_t* n_
  * bits of tokens [0, T) and the slot lists hi_idx: device int32
  * [batch][K] (ascending), lo_idx: device int32 [batch][T-K] (ascending); a
  * list with no entries may be NULL.
- * A NaN score sets SEMKV_STATUS_NAN_SCORE. */
+ * A NaN score sets SEMKV_STATUS_NAN_SCORE.  Prompts of up to 4096 tokens take
+ * one launch (one workgroup per sequence); longer ones take five, one
+ * workgroup per 4096-token chunk, with the scratch at the end of `flags`.
+ * Calls that overlap on one cache race. */
 int semkv_rank(semkv_cache* c, const float* scores, int64_t T, int32_t* hi_idx,
                int32_t* lo_idx, hipStream_t stream);
 

@@ -1,0 +1,34 @@
+/* semkv_timeline.h -- the one extra entry point of the tracing build of the
+ * decode kernel (libsemkv_timeline.so, built by
+ * `python paper_2608_28911_amd/build.py --timeline`).  The product library
+ * libsemkv.so does not export it.
+ *
+ * In the tracing build, lane 0 of every wave of the first 4096 workgroups of
+ * each decode launch writes the constant 100 MHz device clock at the end of
+ * each phase of the kernel into a device array; a later launch overwrites it.
+ * Layout: uint64 [4096 workgroups][16 waves][16 events], workgroup index
+ * x + X (y + Y z) of the launch grid (X, Y its x and y extents), events:
+ *   0 start, 1 tables and query operands built, 2 first record in LDS,
+ *   3..8 the wave's 1st..6th record done, 9 the wave's records done,
+ *   10 workgroup partial merged, 11 partial stored, 12 split counter taken,
+ *   13 the last workgroup's merge done.
+ * Slots a launch did not write keep their previous contents (zero at load).
+ */
+#ifndef SEMKV_TIMELINE_H
+#define SEMKV_TIMELINE_H
+#include <stddef.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Copy the stamp array to host memory `host` (caller-owned, `bytes` =
+ * 4096 * 16 * 16 * 8).  Synchronous with respect to the device (waits for
+ * prior work).  SEMKV_EINVAL on a null pointer or another size, SEMKV_EHIP
+ * when the copy fails. */
+int semkv_timeline_read(void* host, size_t bytes);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

@@ -97,14 +97,20 @@ class SemKVCache:
               "semkv_rank_sizes")
         return n_hi.value, n_lo.value
 
-    def rank(self, scores):
-        """scores: fp32 [B, T] on the device -> (hi_idx [B, K], lo_idx [B, T-K]) int32."""
+    def rank(self, scores, out=None):
+        """scores: fp32 [B, T] on the device -> (hi_idx [B, K], lo_idx [B, T-K]) int32
+        (written into out = (hi_idx, lo_idx) when given)."""
         import torch
         scores = scores.contiguous()
         B, T = scores.shape
         n_hi, n_lo = self.rank_sizes(T)
-        hi = torch.empty((B, n_hi), dtype=torch.int32, device=scores.device)
-        lo = torch.empty((B, n_lo), dtype=torch.int32, device=scores.device)
+        if out is None:
+            hi = torch.empty((B, n_hi), dtype=torch.int32, device=scores.device)
+            lo = torch.empty((B, n_lo), dtype=torch.int32, device=scores.device)
+        else:
+            hi, lo = out
+            assert hi.shape == (B, n_hi) and lo.shape == (B, n_lo) and hi.dtype == lo.dtype == torch.int32
+            assert hi.is_contiguous() and lo.is_contiguous()
         check(lib().semkv_rank(ctypes.byref(self.c), _ptr(scores), T, _ptr(hi), _ptr(lo), _stream()),
               "semkv_rank")
         return hi, lo

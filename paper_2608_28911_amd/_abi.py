@@ -71,6 +71,11 @@ def lib():
         if not os.path.exists(LIB_PATH):
             raise RuntimeError("libsemkv.so is not built; run paper_2608_28911_amd/build.py "
                                "(or __graft_entry__.build())")
+        # torch ships its own copy of the HIP runtime (same soname): loaded
+        # first, it is the one the library binds to.  Loaded the other way
+        # round, the process maps two runtimes and the library's launches do
+        # not see torch's streams and allocations.
+        import torch  # noqa: F401
         _lib = ctypes.CDLL(LIB_PATH)
         for name, (res, args) in EXPORTS.items():
             f = getattr(_lib, name)

@@ -13,6 +13,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libsemkv.so")
+LIB_TIMELINE = os.path.join(HERE, "libsemkv_timeline.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 COMMON = ["-O3", "-std=c++17", "--offload-arch=gfx950", "-fPIC", "-fno-fast-math",
@@ -29,29 +30,75 @@ SOURCES = {
 }
 
 
-def build(verbose: bool = False) -> str:
-    """Compile every source (in parallel) and link libsemkv.so (always recompiles)."""
+REMARKS = "-Rpass-analysis=kernel-resource-usage"
+
+
+def _compile(cmd):
+    """Run one hipcc compile; return its kernels' resource remarks as
+    {kernel: {field: value}} and pass every other line of its output on."""
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    usage, name, rest = {}, None, []
+    for line in (r.stdout + r.stderr).splitlines():
+        if REMARKS not in line or "remark:" not in line:
+            rest.append(line)
+            continue
+        field = line.split("remark:", 1)[1].replace("[" + REMARKS + "]", "").strip()
+        key, _, val = field.partition(":")
+        if key == "Function Name":
+            name = val.strip()
+            usage[name] = {}
+        elif name is not None:
+            usage[name][key.strip()] = val.strip()
+    if rest:
+        print("\n".join(rest), file=sys.stderr, flush=True)
+    if r.returncode:
+        raise subprocess.CalledProcessError(r.returncode, cmd)
+    return usage
+
+
+def build(verbose: bool = False, timeline: bool = False) -> str:
+    """Compile every source (in parallel) and link libsemkv.so (always recompiles).
+
+    Fails when any kernel needs private scratch memory (register spills): every
+    kernel here is written to fit the register file, and a spill would put
+    per-lane stack traffic on the hot path.  The compiler's per-kernel figures
+    (registers, LDS, scratch, occupancy) are written to resource_usage.txt
+    beside the objects.
+
+    timeline=True builds the tracing variant libsemkv_timeline.so instead: the
+    decode kernel with its phase stamps compiled in (-DSEMKV_TIMELINE,
+    include/semkv_timeline.h), objects under _build/timeline."""
     from concurrent.futures import ThreadPoolExecutor
-    os.makedirs(BUILD, exist_ok=True)
+    bdir = os.path.join(BUILD, "timeline") if timeline else BUILD
+    lib_out = LIB_TIMELINE if timeline else LIB
+    os.makedirs(bdir, exist_ok=True)
     cmds, objs = [], []
     for src, extra in SOURCES.items():
-        obj = os.path.join(BUILD, src.replace(".hip", ".o"))
-        cmds.append([HIPCC, "-c", os.path.join(CSRC, src), "-o", obj] + COMMON + extra)
+        obj = os.path.join(bdir, src.replace(".hip", ".o"))
+        flag = ["-DSEMKV_TIMELINE"] if timeline and src == "decode.hip" else []
+        cmds.append([HIPCC, "-c", os.path.join(CSRC, src), "-o", obj] + COMMON + extra + flag +
+                    [REMARKS, "-fno-caret-diagnostics"])
         objs.append(obj)
     for cmd in cmds if verbose else ():
         print(" ".join(cmd), flush=True)
     with ThreadPoolExecutor(max_workers=min(len(cmds), os.cpu_count() or 1)) as ex:
-        for f in [ex.submit(subprocess.check_call, cmd) for cmd in cmds]:
-            f.result()
-    tmp = LIB + ".tmp%d" % os.getpid()
+        usage = {}
+        for f in [ex.submit(_compile, cmd) for cmd in cmds]:
+            usage.update(f.result())
+    with open(os.path.join(bdir, "resource_usage.txt"), "w") as fh:
+        for k in sorted(usage):
+            fh.write("%s %s\n" % (k, " ".join("%s=%s" % (f.replace(" ", ""), v) for f, v in usage[k].items())))
+    spills = sorted(k for k, u in usage.items() if u.get("ScratchSize [bytes/lane]", "0") != "0")
+    if not usage or spills:
+        raise RuntimeError("kernels with private scratch (register spills): %s" % (spills or "no resource remarks"))
+    tmp = lib_out + ".tmp%d" % os.getpid()
     cmd = [HIPCC, "-shared", "-fPIC", "--offload-arch=gfx950", "-o", tmp] + objs
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.check_call(cmd)
-    os.replace(tmp, LIB)
-    return LIB
+    os.replace(tmp, lib_out)
+    return lib_out
 
 
 if __name__ == "__main__":
-    build(verbose="-v" in sys.argv)
-    print(LIB)
+    print(build(verbose="-v" in sys.argv, timeline="--timeline" in sys.argv))

@@ -40,6 +40,29 @@
 #include "semkv_internal.h"
 
 namespace semkv {
+
+// ---- tracing build only (-DSEMKV_TIMELINE, libsemkv_timeline.so): lane 0 of
+// every wave of the first kTimelineWGs workgroups of a launch records the
+// constant 100 MHz clock at the ends of the kernel's phases (event ids below);
+// a later launch overwrites the stamps.  The product library compiles every
+// stamp to nothing.
+#ifdef SEMKV_TIMELINE
+constexpr int kTimelineWGs = 4096, kTimelineWaves = 16, kTimelineEvents = 16;
+__device__ unsigned long long g_timeline[kTimelineWGs * kTimelineWaves * kTimelineEvents];
+__device__ inline void timeline_stamp(int ev) {
+  const int wg = blockIdx.x + gridDim.x * (blockIdx.y + gridDim.y * blockIdx.z);
+  if ((threadIdx.x & 63) == 0 && wg < kTimelineWGs)
+    g_timeline[(wg * kTimelineWaves + (threadIdx.x >> 6)) * kTimelineEvents + ev] = wall_clock64();
+}
+#define SEMKV_STAMP(ev) timeline_stamp(ev)
+#else
+#define SEMKV_STAMP(ev) ((void)0)
+#endif
+// 0 start, 1 tables and query operands built, 2 first record in LDS,
+// 3..8 the wave's 1st..6th record done (a 7th and later overwrite 8),
+// 9 the wave's records done, 10 workgroup partial merged, 11 partial stored,
+// 12 split counter taken, 13 the last workgroup's merge done
+
 namespace {
 
 typedef int32_t int4v __attribute__((ext_vector_type(4)));
@@ -602,7 +625,6 @@ __device__ inline float comb3_score(const int4v& c) {
 // piece j of lane l is bytes [1024 j + 16 l, +16) of a record, read through a
 // buffer descriptor bounded by the record's size: pieces past its end read 0
 // without touching memory, so every record takes the same NMAX loads
-constexpr int kBufferWord3 = 0x00020000;   // raw 32-bit data format (gfx9 family)
 
 template <int BASE, int LH, int LL, int G, int NMAX>
 __device__ inline void load_tile(const PoolGeom& g, const uint8_t* unit, int tile, int nt0, uint4 (&r)[NMAX], int lane) {
@@ -972,6 +994,7 @@ __device__ void run_pool(const DecodeArgs& a, Shared<PL>& sm, WaveState<PL::NGV>
     // the next record replaces this one in the wave's buffer (LDS serves a
     // wave's accesses in order: the reads above come first)
     if (more) store_pieces(R, rec, lane);
+    SEMKV_STAMP(3 + (it < 5 ? it : 5));
   }
 }
 
@@ -1190,6 +1213,7 @@ __global__ __launch_bounds__((Plan<BASE, LH, LL, G>::NT)) void decode_kernel(Dec
   const int li = vb / a.g.batch, b = vb - li * a.g.batch, layer = a.layer + li;
   const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
   const PoolGeom& g = a.g;
+  SEMKV_STAMP(0);
 
   // ---- this wave's tiles: first, first + stride, ... (high pool first)
   const int nt0 = int((a.n_rows[0] + kSlots - 1) / kSlots), nt1 = int((a.n_rows[1] + kSlots - 1) / kSlots);
@@ -1251,6 +1275,7 @@ __global__ __launch_bounds__((Plan<BASE, LH, LL, G>::NT)) void decode_kernel(Dec
   build_aq<BASE, LH, G, 0, 0>(a, sm);
   build_aq<BASE, LL, G, 1, PL::GH::NG * PL::NCKH * 64>(a, sm);
   __syncthreads();
+  SEMKV_STAMP(1);
 
   // ---- this wave's records
   WaveState<PL::NGV> st;
@@ -1265,8 +1290,10 @@ __global__ __launch_bounds__((Plan<BASE, LH, LL, G>::NT)) void decode_kernel(Dec
     st.cv[cb] = int4v{0, 0, 0, 0};
   }
   if (count > 0) store_pieces(R, sm.stage[wave], lane);
+  SEMKV_STAMP(2);
   if (nhi > 0) run_pool<BASE, LH, LL, G, 0>(a, sm, st, unit, nt0, first, stride, 0, nhi, count, R);
   if (count > nhi) run_pool<BASE, LH, LL, G, 1>(a, sm, st, unit, nt0, first, stride, nhi, count, count, R);
+  SEMKV_STAMP(9);
   wave_finish<BASE, G>(sm, st);
   __syncthreads();
   const bool tail = split == a.nsplit - 1 && a.n_tail > 0;
@@ -1276,6 +1303,7 @@ __global__ __launch_bounds__((Plan<BASE, LH, LL, G>::NT)) void decode_kernel(Dec
   }
 
   // ---- workgroup partial: merge of the waves' (and the tail's) states
+  SEMKV_STAMP(10);
   if (qt) {
     float M = -INFINITY;
 #pragma unroll
@@ -1305,6 +1333,7 @@ __global__ __launch_bounds__((Plan<BASE, LH, LL, G>::NT)) void decode_kernel(Dec
   // the workgroup's counter increment; the last workgroup reads them after it
   __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
+  SEMKV_STAMP(11);
   if (tid == 0) {
     uint32_t* ctr = a.counters + (vb * g.n_kv_heads + kvh) * kCounterStride;
     const uint32_t old = __hip_atomic_fetch_add(ctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -1312,8 +1341,13 @@ __global__ __launch_bounds__((Plan<BASE, LH, LL, G>::NT)) void decode_kernel(Dec
     if (sm.last) __hip_atomic_store(ctr, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
   __syncthreads();
+  SEMKV_STAMP(12);
   if (!sm.last) return;
   merge_splits<BASE>(a, sm, vb, layer, kvh);
+#ifdef SEMKV_TIMELINE
+  __syncthreads();
+  SEMKV_STAMP(13);
+#endif
 }
 
 template <int BASE, int LH, int LL, int G>
@@ -1419,3 +1453,12 @@ int decode_blocks_per_cu(int base, int LH, int LL, int G) { return decode_query(
 int decode_waves(int base, int LH, int LL, int G) { return decode_query(base, LH, LL, G, true); }
 
 }  // namespace semkv
+
+#ifdef SEMKV_TIMELINE
+#include "semkv.h"
+#include "semkv_timeline.h"
+extern "C" int semkv_timeline_read(void* host, size_t bytes) {
+  if (host == nullptr || bytes != sizeof(semkv::g_timeline)) return SEMKV_EINVAL;
+  return hipMemcpyFromSymbol(host, HIP_SYMBOL(semkv::g_timeline), bytes) == hipSuccess ? SEMKV_OK : SEMKV_EHIP;
+}
+#endif

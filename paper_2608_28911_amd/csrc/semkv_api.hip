@@ -271,7 +271,7 @@ int semkv_cache_sizes(const semkv_config* cfg, semkv_sizes* out) {
   out->tail_bytes = size_t(units * 2 * kSlots * kD * 2);
   out->tail_score_bytes = size_t(k.batch) * kSlots * 4;
   out->flag_words = (k.max_prompt + k.max_new + 31) / 32 + 1;
-  out->flag_bytes = size_t(k.batch * out->flag_words * 4);
+  out->flag_bytes = size_t(rank_scratch_offset(k.batch, out->flag_words) + k.batch * rank_scratch_words(k.max_prompt)) * 4;
   int64_t max_split = out->cap_hi_tiles + out->cap_lo_tiles;
   if (max_split > kMaxSplits) max_split = kMaxSplits;
   int64_t max_split_all = kMaxSplits / k.n_layers < 1 ? 1 : kMaxSplits / k.n_layers;   // all-layers launch
@@ -367,6 +367,8 @@ int semkv_rank(semkv_cache* c, const float* scores, int64_t T, int32_t* hi_idx, 
   a.hi_idx = hi_idx;
   a.lo_idx = lo_idx;
   a.status = c->status;
+  a.scratch = c->flags + rank_scratch_offset(c->cfg.batch, c->sz.flag_words);
+  a.scratch_words = rank_scratch_words(c->cfg.max_prompt);
   return launch_rank(a, c->cfg.batch, stream);
 }
 

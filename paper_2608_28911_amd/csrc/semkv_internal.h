@@ -32,6 +32,7 @@ struct RankArgs {
   uint32_t* flags; int64_t flag_words;
   int32_t* hi_idx; int32_t* lo_idx;
   int32_t* status;
+  uint32_t* scratch; int64_t scratch_words;   // per sequence, zero between calls
 };
 
 struct QuantArgs {
@@ -108,6 +109,22 @@ constexpr int kPartial = 132;  // m, l, 2 pad, o[128]
 // units do not queue their atomics on one line
 constexpr int kCounterStride = 64;
 constexpr int kMaxSplits = 256;   // splits per (sequence, kv head)
+// buffer descriptor word 3 of a raw buffer of 32-bit elements (gfx9 family)
+constexpr int kBufferWord3 = 0x00020000;
+
+// Ranker scratch, per sequence, after the flag bitmaps in the flags buffer
+// (zero at cache init and again after every semkv_rank call): three
+// histograms (2048, 2048 and 1024 bins), 16 words of selection state, then
+// two counts per chunk of kRankChunk tokens.
+constexpr int kRankChunk = 4096;
+constexpr int kRankH1 = 0, kRankH2 = 2048, kRankH3 = 4096, kRankState = 5120, kRankCounts = 5136;
+__host__ __device__ constexpr int64_t rank_chunks(int64_t T) { return (T + kRankChunk - 1) / kRankChunk; }
+__host__ __device__ constexpr int64_t rank_scratch_words(int64_t max_prompt) {
+  return (kRankCounts + 2 * rank_chunks(max_prompt) + 63) / 64 * 64;
+}
+__host__ __device__ constexpr int64_t rank_scratch_offset(int64_t batch, int64_t flag_words) {
+  return (batch * flag_words + 63) / 64 * 64;
+}
 
 int launch_rank(const RankArgs& a, int batch, hipStream_t s);
 int launch_quantize(const QuantArgs& a, hipStream_t s);

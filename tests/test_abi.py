@@ -39,6 +39,16 @@ def test_every_declared_symbol_is_exported(abi):
         assert getattr(lib, n) is not None
 
 
+def test_tracing_entry_point_only_in_the_tracing_build(abi):
+    """include/semkv_timeline.h declares the tracing build's one extra call;
+    the product library must not carry it (its stamps compile to nothing)."""
+    src = open(os.path.join(ROOT, "include", "semkv_timeline.h")).read()
+    names = set(re.findall(r"^\s*\w+\s+(semkv_\w+)\s*\(", src, re.M))
+    assert names == {"semkv_timeline_read"}
+    out = subprocess.check_output(["nm", "-D", "--defined-only", abi.LIB_PATH]).decode()
+    assert not names & set(re.findall(r" T (semkv_\w+)", out))
+
+
 def cfg_for(abi, **kw):
     from paper_2608_28911_amd import make_config
     d = dict(n_layers=2, n_kv_heads=8, batch=1, base=0, L_hi=6, L_lo=5, group=128, r_num=26, r_den=100,

@@ -70,6 +70,81 @@ def test_ragged_lengths_and_groups(T, G):
     _check_decode(cache, cfgw, T, flags, [0])
 
 
+@pytest.mark.parametrize("base,lh,ll,G", [("affine", 6, 5, 128), ("affine", 6, 5, 32), ("tq", 4, 3, 128),
+                                          ("rot_affine", 6, 5, 64), ("affine", 8, 7, 128), ("affine", 3, 2, 128)])
+def test_every_fill_of_a_pools_last_record(base, lh, ll, G):
+    """T = 2 (64 + n), r = 1/2: both pools hold 64 + n rows, so each ends in a
+    record with n valid slots; n runs over 1..64, so the decode mask covers
+    every fill of each 16-token block of a last record, in both pools."""
+    for n in range(1, 65):
+        T = 2 * (64 + n)
+        kw = dict(L_hi=lh, L_lo=ll) if base != "tq" else {}
+        cfgw = get_config(0 if base != "tq" else 4, base=base, group=G, r_num=1, r_den=2, batch=1,
+                          n_kv_heads=1, n_q_heads=4, n_layers=1, **kw)
+        assert O.top_count(T, 1, 2) == T - O.top_count(T, 1, 2) == 64 + n
+        try:
+            cache, flags = _check_prefill(cfgw, T)
+            _check_decode(cache, cfgw, T, flags, [0])
+        except AssertionError as e:
+            raise AssertionError("last record with %d valid slots: %s" % (n, e)) from None
+
+
+def _multi_chunk_scores(T, seed):
+    """Three sequences: integer scores 0..3 (ties across every chunk
+    boundary), all equal, and normal draws with +0, -0, +inf and -inf."""
+    rng = np.random.default_rng(seed)
+    s = np.empty((3, T), np.float32)
+    s[0] = rng.integers(0, 4, T)
+    s[1] = 1.0
+    s[2] = rng.standard_normal(T)
+    s[2, ::3] = 0.0
+    s[2, 1::7] = -0.0
+    s[2, 5], s[2, 6] = np.inf, -np.inf
+    return s
+
+
+@pytest.mark.parametrize("r", [(0, 1), (1, 2), (26, 100), (1, 1)])
+def test_multi_chunk_ranker(r):
+    """Sequences longer than a 4096-token chunk are ranked by one workgroup
+    per chunk over five launches (histograms in scratch after the flag
+    bitmaps, cleared again by each call).  Two calls in a row on one cache,
+    the second shorter, so the second starts from the scratch the first left:
+    flags and slot lists bit-exact against the oracle for both."""
+    import torch
+    cfgw = get_config(0, batch=3, n_kv_heads=1, n_q_heads=4, n_layers=1, r_num=r[0], r_den=r[1])
+    cache = U.make_cache(cfgw, 40000, n_layers=1, max_new=0)
+    for T, seed in ((40000, 1), (8193, 2), (4097, 3), (12288, 4)):
+        s = _multi_chunk_scores(T, seed)
+        hi, lo = cache.rank(torch.from_numpy(s).cuda())
+        torch.cuda.synchronize()
+        hi, lo = hi.cpu().numpy(), lo.cpu().numpy()
+        for b in range(3):
+            f, ohi, olo = O.rank(s[b], r[0], r[1])
+            assert np.array_equal(hi[b], ohi) and np.array_equal(lo[b], olo), "slot lists, T %d seq %d" % (T, b)
+            assert np.array_equal(U.flags_bits(cache, b, T), f), "flags, T %d seq %d" % (T, b)
+        assert cache.status() == 0
+    # per sequence, after the flag bitmaps (rounded up to 64 words): the three
+    # histograms (5120 words) must be zero again; the selection state and
+    # chunk counts that follow them are rewritten before every read
+    words = cache.flags.view(-1).cpu().numpy()
+    off = (3 * cache.sz.flag_words + 63) // 64 * 64
+    stride = (5136 + 2 * ((40000 + 4095) // 4096) + 63) // 64 * 64
+    assert len(words) == off + 3 * stride
+    for b in range(3):
+        assert not words[off + b * stride:off + b * stride + 5120].any(), "histograms of seq %d not cleared" % b
+
+
+def test_multi_chunk_ranker_reports_nan():
+    import torch
+    cfgw = get_config(0, batch=1, n_kv_heads=1, n_q_heads=4, n_layers=1)
+    cache = U.make_cache(cfgw, 9000, n_layers=1, max_new=0)
+    s = np.random.default_rng(5).standard_normal((1, 9000)).astype(np.float32)
+    s[0, 8500] = np.nan
+    cache.rank(torch.from_numpy(s).cuda())
+    torch.cuda.synchronize()
+    assert cache.status() & 1
+
+
 @pytest.mark.parametrize("r", [(0, 1), (1, 1), (1, 2)])
 def test_all_low_all_high_half(r):
     cfgw = get_config(0, r_num=r[0], r_den=r[1], n_kv_heads=2, n_q_heads=8)
