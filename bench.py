@@ -33,6 +33,9 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, AMD published peak
+# what decode attention computes in: the query and the softmax weights as
+# int8 fixed-point digits into exact int32 MFMA sums, the softmax in fp32
+DECODE_DTYPE = "i8 MFMA (fixed-point q and softmax weights, exact i32 sums); f32 softmax"
 PROFILE = os.path.join(ROOT, "profiles", "decode_kernel_llama8b_b1_t32768.md")
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2608_28911_amd", "csrc", f)
                   for f in ("decode.hip", "semkv_internal.h", "semkv_fmt.h")]
@@ -435,7 +438,7 @@ def multiturn(args, cfgw):
         "metric": "multi-turn dialogue: generated tokens/s incl. each turn's re-prefill (rank + quantize/pack)",
         "value": round(tokens_per_s, 2), "unit": "tokens/s", "n_gpus": 1, "steps": n_gen, "warmup": 1,
         "ms_per_step": round(total_ms / n_gen, 4), "higher_is_better": True, "scaling": "weak",
-        "vs_baseline": None, "dtype": "f16", "data": "synthetic",
+        "vs_baseline": None, "dtype": DECODE_DTYPE, "data": "synthetic",
         "config": {"workload": cfgw.name, "layers": nL, "batch": B, "kv_heads": H, "q_heads": Hq,
                    "head_dim": 128, "base": cfgw.base, "levels": [cfgw.L_hi, cfgw.L_lo],
                    "r": cfgw.r_num / cfgw.r_den, "group": cfgw.group, "turns": [list(x) for x in cfgw.turns]},
@@ -656,7 +659,7 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "i8 MFMA (fixed-point q and softmax weights, exact i32 sums); f32 softmax",
+        "dtype": DECODE_DTYPE,
         "data": "synthetic",
         "config": config_of(cfgw, r),
         "effective_hbm_gbps": round(achieved, 1),

@@ -54,14 +54,23 @@ __device__ inline void timeline_stamp(int ev) {
   if ((threadIdx.x & 63) == 0 && wg < kTimelineWGs)
     g_timeline[(wg * kTimelineWaves + (threadIdx.x >> 6)) * kTimelineEvents + ev] = wall_clock64();
 }
+// slots 14 and 15 of a wave count events instead (lane 0 adds one)
+__device__ inline void timeline_count(int ev) {
+  const int wg = blockIdx.x + gridDim.x * (blockIdx.y + gridDim.y * blockIdx.z);
+  if ((threadIdx.x & 63) == 0 && wg < kTimelineWGs)
+    g_timeline[(wg * kTimelineWaves + (threadIdx.x >> 6)) * kTimelineEvents + ev] += 1;
+}
 #define SEMKV_STAMP(ev) timeline_stamp(ev)
+#define SEMKV_COUNT(ev) timeline_count(ev)
 #else
 #define SEMKV_STAMP(ev) ((void)0)
+#define SEMKV_COUNT(ev) ((void)0)
 #endif
 // 0 start, 1 tables and query operands built, 2 first record in LDS,
 // 3..8 the wave's 1st..6th record done (a 7th and later overwrite 8),
 // 9 the wave's records done, 10 workgroup partial merged, 11 partial stored,
-// 12 split counter taken, 13 the last workgroup's merge done
+// 12 split counter taken, 13 the last workgroup's merge done; counts: 14 the
+// wave's value-sum flushes, 15 its records (both cleared at the wave's start)
 
 namespace {
 
@@ -938,7 +947,9 @@ __device__ void run_pool(const DecodeArgs& a, Shared<PL>& sm, WaveState<PL::NGV>
     // record's weights would not fit 21 bits (their rounding stays below
     // 2^21 - 1, so the top byte stays below 128), and re-pick the scale
     const bool flush = grow || wmax * st.qw >= 2097151.0f;
+    SEMKV_COUNT(15);
     if (__builtin_amdgcn_ballot_w64(flush) != 0) {
+      SEMKV_COUNT(14);
       wmax = row_max16(wmax);
       st.l *= alpha;
 #pragma unroll
@@ -1214,6 +1225,15 @@ __global__ __launch_bounds__((Plan<BASE, LH, LL, G>::NT)) void decode_kernel(Dec
   const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
   const PoolGeom& g = a.g;
   SEMKV_STAMP(0);
+#ifdef SEMKV_TIMELINE
+  if ((threadIdx.x & 63) == 0) {
+    const int twg = blockIdx.x + gridDim.x * (blockIdx.y + gridDim.y * blockIdx.z);
+    if (twg < kTimelineWGs) {
+      g_timeline[(twg * kTimelineWaves + (threadIdx.x >> 6)) * kTimelineEvents + 14] = 0;
+      g_timeline[(twg * kTimelineWaves + (threadIdx.x >> 6)) * kTimelineEvents + 15] = 0;
+    }
+  }
+#endif
 
   // ---- this wave's tiles: first, first + stride, ... (high pool first)
   const int nt0 = int((a.n_rows[0] + kSlots - 1) / kSlots), nt1 = int((a.n_rows[1] + kSlots - 1) / kSlots);

@@ -77,6 +77,7 @@ def main(argv=None):
     start = d[:, :, 0]
     t0 = start[start > 0].min()
     rel = np.where(d > 0, (d - t0) * 10, -1) / 1e3                     # us
+    rel[:, :, 14:] = -1                                                  # counts, not stamps
     print("workload %s: %d workgroups, %d waves stamped (last of %d launches per layer, layer %d)"
           % (args.workload, nwg, int((start > 0).sum()), args.launches, nL - 1))
     print()
@@ -88,6 +89,12 @@ def main(argv=None):
         if v.size:
             print("| %s | %d | %.2f | %.2f | %.2f | %.2f |" % (NAMES[ev], v.size, v.min(), np.median(v),
                                                               np.percentile(v, 90), v.max()))
+    counts = buf.reshape(WGS, WAVES, EVENTS)[:nwg, :, 14:16].astype(np.int64)
+    live = start > 0
+    fl, rc = counts[:, :, 0][live], counts[:, :, 1][live]
+    print()
+    print("value-sum flushes: %d of %d records (%.1f %%); per wave: mean %.2f, max %d"
+          % (fl.sum(), rc.sum(), 100.0 * fl.sum() / max(1, rc.sum()), fl.mean(), fl.max()))
     m = np.flatnonzero(rel[:, 0, 13] >= 0)
     print()
     print("merging workgroups (wave 0): %d" % len(m))
