@@ -1235,17 +1235,19 @@ __global__ __launch_bounds__((Plan<BASE, LH, LL, G>::NT)) void decode_kernel(Dec
   }
 #endif
 
-  // ---- this wave's tiles: first, first + stride, ... (high pool first)
-  const int nt0 = int((a.n_rows[0] + kSlots - 1) / kSlots), nt1 = int((a.n_rows[1] + kSlots - 1) / kSlots);
-  const int nt = nt0 + nt1, stride = a.nsplit * NW;
-  const int first = wave * a.nsplit + split;
-  const int count = first < nt ? (nt - first + stride - 1) / stride : 0;
-  const int nhi = first < nt0 ? (nt0 - first + stride - 1) / stride : 0;
-  const uint8_t* unit = g.pools + unit_offset(g, b, layer, kvh);
+  // ---- the query first (the longest wait of the prologue); its work takes
+  // the first 4 x 128 threads, one per (head, channel) -- with 8 waves every
+  // thread, known at compile time, so no branch forces a wait on the load
+  const bool qt = NT == 4 * kD || tid < 4 * kD;
+  const int h = qt ? tid >> 7 : 0, c = tid & 127;
+  const uint16_t qbits = qt ? a.q[((int64_t(vb) * g.n_kv_heads * 4) + kvh * 4 + h) * kD + c] : uint16_t(0);
+  // rotated bases: the sign word of this thread's channel, in flight with the query
+  const uint32_t qsign = BASE != 0 && qt ? g.signs[(int64_t(layer) * g.n_kv_heads + kvh) * 4 + (c >> 5)] : 0u;
 
   // ---- fused append (Alg. 2): the workgroup that attends over the fp16 tail
   // first stores this layer's new K/V row in it, as its last row (read back
-  // by the same workgroup after the barriers below)
+  // by the same workgroup after the barriers below); placed before the record
+  // loads, so that its wait covers the query load only
   if (a.k_new != nullptr && split == a.nsplit - 1 && tid < 2 * kD / 2) {
     const int kv = tid >> 6, w = tid & 63;                // 64 dwords each of K and V
     const uint32_t* src = reinterpret_cast<const uint32_t*>((kv ? a.v_new : a.k_new) + (int64_t(b) * g.n_kv_heads + kvh) * kD);
@@ -1254,22 +1256,25 @@ __global__ __launch_bounds__((Plan<BASE, LH, LL, G>::NT)) void decode_kernel(Dec
     dst[w] = src[w];
   }
 
-  // ---- query and decode tables, then the first record in flight; the query
-  // work takes the first 4 x 128 threads, one per (head, channel)
-  const bool qt = tid < 4 * kD;
-  const int h = qt ? tid >> 7 : 0, c = tid & 127;
-  const uint16_t qbits = qt ? a.q[((int64_t(vb) * g.n_kv_heads * 4) + kvh * 4 + h) * kD + c] : uint16_t(0);
-  // rotated bases: the sign word of this thread's channel, in flight with the query
-  const uint32_t qsign = BASE != 0 && qt ? g.signs[(int64_t(layer) * g.n_kv_heads + kvh) * 4 + (c >> 5)] : 0u;
+  // ---- this wave's tiles: first, first + stride, ... (high pool first),
+  // and the first of them in flight (a wave without records loads tile 0,
+  // unused)
+  const int nt0 = int((a.n_rows[0] + kSlots - 1) / kSlots), nt1 = int((a.n_rows[1] + kSlots - 1) / kSlots);
+  const int nt = nt0 + nt1, stride = a.nsplit * NW;
+  const int first = wave * a.nsplit + split;
+  const int count = first < nt ? (nt - first + stride - 1) / stride : 0;
+  const int nhi = first < nt0 ? (nt0 - first + stride - 1) / stride : 0;
+  const uint8_t* unit = g.pools + unit_offset(g, b, layer, kvh);
+  uint4 R[PL::NLD];
+  load_tile<BASE, LH, LL, G>(g, unit, count > 0 ? first : 0, nt0, R, lane);
+
+  // ---- decode tables (the query and the first record are in flight)
   constexpr int NTH = (PL::LUTH / 4 + NT - 1) / NT, NTL = (PL::LUTL / 4 + NT - 1) / NT;
   uint4 th[NTH], tl[NTL];
 #pragma unroll
   for (int k = 0; k < NTH; ++k) th[k] = lut_piece<BASE, LH, PL::RH>(tid + k * NT < PL::LUTH / 4 ? tid + k * NT : 0);
 #pragma unroll
   for (int k = 0; k < NTL; ++k) tl[k] = lut_piece<BASE, LL, PL::RL>(tid + k * NT < PL::LUTL / 4 ? tid + k * NT : 0);
-  // the wave's first record (a wave without records loads tile 0, unused)
-  uint4 R[PL::NLD];
-  load_tile<BASE, LH, LL, G>(g, unit, count > 0 ? first : 0, nt0, R, lane);
   {
     uint4* d = reinterpret_cast<uint4*>(sm.lut);
 #pragma unroll
