@@ -47,27 +47,30 @@ namespace semkv {
 // a later launch overwrites the stamps.  The product library compiles every
 // stamp to nothing.
 #ifdef SEMKV_TIMELINE
-constexpr int kTimelineWGs = 4096, kTimelineWaves = 16, kTimelineEvents = 16;
+constexpr int kTimelineWGs = 4096, kTimelineWaves = 16, kTimelineEvents = 32;
 __device__ unsigned long long g_timeline[kTimelineWGs * kTimelineWaves * kTimelineEvents];
 __device__ inline void timeline_stamp(int ev) {
   const int wg = blockIdx.x + gridDim.x * (blockIdx.y + gridDim.y * blockIdx.z);
   if ((threadIdx.x & 63) == 0 && wg < kTimelineWGs)
     g_timeline[(wg * kTimelineWaves + (threadIdx.x >> 6)) * kTimelineEvents + ev] = wall_clock64();
 }
-// slots 14 and 15 of a wave count events instead (lane 0 adds one)
-__device__ inline void timeline_count(int ev) {
+// slots 14 and 15 of a wave hold counts, kept in the wave's state and
+// written once (a read-modify-write of memory in the record loop would wait
+// for the loads in flight)
+__device__ inline void timeline_put(int ev, unsigned long long v) {
   const int wg = blockIdx.x + gridDim.x * (blockIdx.y + gridDim.y * blockIdx.z);
   if ((threadIdx.x & 63) == 0 && wg < kTimelineWGs)
-    g_timeline[(wg * kTimelineWaves + (threadIdx.x >> 6)) * kTimelineEvents + ev] += 1;
+    g_timeline[(wg * kTimelineWaves + (threadIdx.x >> 6)) * kTimelineEvents + ev] = v;
 }
 #define SEMKV_STAMP(ev) timeline_stamp(ev)
-#define SEMKV_COUNT(ev) timeline_count(ev)
 #else
 #define SEMKV_STAMP(ev) ((void)0)
-#define SEMKV_COUNT(ev) ((void)0)
 #endif
 // 0 start, 1 tables and query operands built, 2 first record in LDS,
-// 3..8 the wave's 1st..6th record done (a 7th and later overwrite 8),
+// 3..7 the wave's 1st..5th record done, the next record's data stored in LDS
+// (a 6th and later overwrite 7), 8 the first record's arithmetic done (before
+// the next record's data is waited for), 16..18 inside the first record: the
+// next record's loads issued, scores done, softmax and flush done,
 // 9 the wave's records done, 10 workgroup partial merged, 11 partial stored,
 // 12 split counter taken, 13 the last workgroup's merge done; counts: 14 the
 // wave's value-sum flushes, 15 its records (both cleared at the wave's start)
@@ -617,6 +620,9 @@ struct WaveState {
   float qw, qwi;     // scale of the int8 weights (a power of 2) and its inverse
   float of[8];       // flushed value sums, channel 16 cb + n of head r
   int4v cv[8];       // integer value sums since the last flush, rows (head, byte)
+#ifdef SEMKV_TIMELINE
+  int nrec = 0, nflush = 0;   // tracing build: records and flushes of the wave
+#endif
 };
 
 // the integer q . codes of one head from its three byte rows
@@ -813,6 +819,9 @@ __device__ void run_pool(const DecodeArgs& a, Shared<PL>& sm, WaveState<PL::NGV>
     const int tile = first + stride * it;
     const bool more = it + 1 < count;
     if (more) load_tile<BASE, LH, LL, G>(a.g, unit, tile + stride, nt0, R, lane);
+#ifdef SEMKV_TIMELINE
+    if (it == 0) SEMKV_STAMP(16);
+#endif
     const int ptile = POOL ? tile - nt0 : tile;
     const uint8_t* kmeta = rec + 2 * Tr::TB;
     const uint8_t* vmeta = kmeta + Ge::MB;
@@ -904,6 +913,9 @@ __device__ void run_pool(const DecodeArgs& a, Shared<PL>& sm, WaveState<PL::NGV>
 #pragma unroll
       for (int blk = 0; blk < 4; ++blk) lg[blk] = 16 * blk + n < nvalid ? lg[blk] : -INFINITY;
     }
+#ifdef SEMKV_TIMELINE
+    if (it == 0) SEMKV_STAMP(17);
+#endif
     // ---- online softmax (base 2) for head r over this record's 64 tokens,
     // rescaled lazily: the reference maximum st.m moves only when a score
     // passes it by more than 8 (weights up to 2^8 fit the fixed-point range),
@@ -947,9 +959,13 @@ __device__ void run_pool(const DecodeArgs& a, Shared<PL>& sm, WaveState<PL::NGV>
     // record's weights would not fit 21 bits (their rounding stays below
     // 2^21 - 1, so the top byte stays below 128), and re-pick the scale
     const bool flush = grow || wmax * st.qw >= 2097151.0f;
-    SEMKV_COUNT(15);
+#ifdef SEMKV_TIMELINE
+    st.nrec += 1;
+#endif
     if (__builtin_amdgcn_ballot_w64(flush) != 0) {
-      SEMKV_COUNT(14);
+#ifdef SEMKV_TIMELINE
+      st.nflush += 1;
+#endif
       wmax = row_max16(wmax);
       st.l *= alpha;
 #pragma unroll
@@ -967,6 +983,10 @@ __device__ void run_pool(const DecodeArgs& a, Shared<PL>& sm, WaveState<PL::NGV>
     st.l += lsum;
 #pragma unroll
     for (int i = 0; i < NGV; ++i) st.z[i] += zadd[i];
+#ifdef SEMKV_TIMELINE
+    if (it == 0) SEMKV_STAMP(18);
+#endif
+
     // ---- values: C[(h, byte)][channel] += weights (tokens) x V codes, one
     // value group's int8 weights (byte s of rint(w qw) in row 4r + s) at a time
     int4v Aw[Tr::NCV];
@@ -1004,8 +1024,11 @@ __device__ void run_pool(const DecodeArgs& a, Shared<PL>& sm, WaveState<PL::NGV>
     }
     // the next record replaces this one in the wave's buffer (LDS serves a
     // wave's accesses in order: the reads above come first)
+#ifdef SEMKV_TIMELINE
+    if (it == 0) SEMKV_STAMP(8);
+#endif
     if (more) store_pieces(R, rec, lane);
-    SEMKV_STAMP(3 + (it < 5 ? it : 5));
+    SEMKV_STAMP(3 + (it < 4 ? it : 4));
   }
 }
 
@@ -1225,15 +1248,6 @@ __global__ __launch_bounds__((Plan<BASE, LH, LL, G>::NT)) void decode_kernel(Dec
   const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
   const PoolGeom& g = a.g;
   SEMKV_STAMP(0);
-#ifdef SEMKV_TIMELINE
-  if ((threadIdx.x & 63) == 0) {
-    const int twg = blockIdx.x + gridDim.x * (blockIdx.y + gridDim.y * blockIdx.z);
-    if (twg < kTimelineWGs) {
-      g_timeline[(twg * kTimelineWaves + (threadIdx.x >> 6)) * kTimelineEvents + 14] = 0;
-      g_timeline[(twg * kTimelineWaves + (threadIdx.x >> 6)) * kTimelineEvents + 15] = 0;
-    }
-  }
-#endif
 
   // ---- the query first (the longest wait of the prologue); its work takes
   // the first 4 x 128 threads, one per (head, channel) -- with 8 waves every
@@ -1319,6 +1333,10 @@ __global__ __launch_bounds__((Plan<BASE, LH, LL, G>::NT)) void decode_kernel(Dec
   if (nhi > 0) run_pool<BASE, LH, LL, G, 0>(a, sm, st, unit, nt0, first, stride, 0, nhi, count, R);
   if (count > nhi) run_pool<BASE, LH, LL, G, 1>(a, sm, st, unit, nt0, first, stride, nhi, count, count, R);
   SEMKV_STAMP(9);
+#ifdef SEMKV_TIMELINE
+  timeline_put(14, uint32_t(st.nflush));
+  timeline_put(15, uint32_t(st.nrec));
+#endif
   wave_finish<BASE, G>(sm, st);
   __syncthreads();
   const bool tail = split == a.nsplit - 1 && a.n_tail > 0;

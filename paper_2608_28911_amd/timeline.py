@@ -19,11 +19,15 @@ import numpy as np
 from . import _abi as A
 from .build import LIB_TIMELINE
 
-WGS, WAVES, EVENTS = 4096, 16, 16
-NAMES = {0: "start", 1: "tables + query operands", 2: "first record in LDS", 3: "record 1 done",
-         4: "record 2 done", 5: "record 3 done", 6: "record 4 done", 7: "record 5 done",
-         8: "record 6+ done", 9: "wave's records done", 10: "workgroup partial merged",
-         11: "partial stored", 12: "split counter taken", 13: "last workgroup's merge done"}
+WGS, WAVES, EVENTS = 4096, 16, 32
+NAMES = {0: "start", 1: "tables + query operands", 2: "first record in LDS",
+         8: "record 1 arithmetic done", 3: "record 1 done (next record in LDS)",
+         4: "record 2 done", 5: "record 3 done", 6: "record 4 done", 7: "record 5+ done",
+         9: "wave's records done", 10: "workgroup partial merged",
+         11: "partial stored", 12: "split counter taken", 13: "last workgroup's merge done",
+         16: "record 1: next record's loads issued", 17: "record 1: scores done",
+         18: "record 1: softmax and flush done"}
+ORDER = [0, 1, 2, 16, 17, 18, 8, 3, 4, 5, 6, 7, 9, 10, 11, 12, 13]
 
 
 def main(argv=None):
@@ -77,24 +81,40 @@ def main(argv=None):
     start = d[:, :, 0]
     t0 = start[start > 0].min()
     rel = np.where(d > 0, (d - t0) * 10, -1) / 1e3                     # us
-    rel[:, :, 14:] = -1                                                  # counts, not stamps
+    rel[:, :, 14:16] = -1                                                # counts, not stamps
     print("workload %s: %d workgroups, %d waves stamped (last of %d launches per layer, layer %d)"
           % (args.workload, nwg, int((start > 0).sum()), args.launches, nL - 1))
     print()
     print("| phase end | waves | min | median | p90 | max |")
     print("|---|---:|---:|---:|---:|---:|")
-    for ev in sorted(NAMES):
+    for ev in ORDER:
         v = rel[:, :, ev]
         v = v[v >= 0]
         if v.size:
             print("| %s | %d | %.2f | %.2f | %.2f | %.2f |" % (NAMES[ev], v.size, v.min(), np.median(v),
                                                               np.percentile(v, 90), v.max()))
-    counts = buf.reshape(WGS, WAVES, EVENTS)[:nwg, :, 14:16].astype(np.int64)
+    counts = buf.reshape(WGS, WAVES, EVENTS)[:nwg, :, 14:16].astype(np.int64)   # not stamps
     live = start > 0
     fl, rc = counts[:, :, 0][live], counts[:, :, 1][live]
     print()
     print("value-sum flushes: %d of %d records (%.1f %%); per wave: mean %.2f, max %d"
           % (fl.sum(), rc.sum(), 100.0 * fl.sum() / max(1, rc.sum()), fl.mean(), fl.max()))
+    # the first record's arithmetic by its pool: wave w of the workgroup of
+    # split s takes tile w * nsplit + s first (high-pool tiles lead)
+    ns_ = nsplit if nsplit is not None else nwg // max(1, B * H)
+    nt0 = (cache.c.n_hi + 63) // 64
+    wg_idx = np.arange(nwg)[:, None]
+    first = np.arange(WAVES)[None, :] * ns_ + (wg_idx % ns_)
+    dur = rel[:, :, 8] - rel[:, :, 2]
+    ok = (rel[:, :, 8] >= 0) & (rel[:, :, 2] >= 0)
+    for name, sel in (("high-pool (L_hi)", first < nt0), ("low-pool (L_lo)", first >= nt0)):
+        v = dur[ok & sel]
+        if v.size:
+            print("first record's arithmetic, %s first: %d waves, median %.2f us, p90 %.2f" % (name, v.size, np.median(v), np.percentile(v, 90)))
+    d2 = rel[:, :, 4] - rel[:, :, 3]
+    ok2 = (rel[:, :, 4] >= 0) & (rel[:, :, 3] >= 0)
+    if ok2.any():
+        print("second record: %d waves, median %.2f us" % (int(ok2.sum()), np.median(d2[ok2])))
     m = np.flatnonzero(rel[:, 0, 13] >= 0)
     print()
     print("merging workgroups (wave 0): %d" % len(m))
