@@ -1099,52 +1099,118 @@ __device__ inline float fwht_rows(float x, float (*xch)[kD]) {
   return x;
 }
 
-// fp16 tail of generated tokens (at most 64 rows), plain vector arithmetic;
-// its state goes to sm.tfin.
+// fp16 tail of generated tokens (1 to 64 rows): its attention state goes to
+// sm.tfin.  Runs after the workgroup's records, when the decode tables and the
+// weight arrays are free: the K tail is staged in the table area and the V
+// tail in the weight area (both in one round trip), then every thread works:
+// 8 threads per row for the scores, one wave per head for the softmax, one
+// thread per (head, channel) for the values.
 template <int BASE, class PL>
 __device__ void tail_split(const DecodeArgs& a, Shared<PL>& sm, int b, int layer, int kvh) {
+  static_assert(sizeof(sm.lut) >= kSlots * kD * 2 && sizeof(sm.pv) >= kSlots * kD * 2, "tail staging");
+  static_assert(PL::NT == 4 * kD, "one thread per (head, channel)");
   const PoolGeom& g = a.g;
-  const int tid = threadIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int nt = a.n_tail;
   TailScratch& ts = sm.ts;
   const uint16_t* kt = a.tail + ((((int64_t(b) * g.n_layers + layer) * g.n_kv_heads + kvh) * 2) * kSlots) * kD;
   const uint16_t* vt = kt + kSlots * kD;
-  if (tid < 4 * nt) {
-    const int t = tid >> 2, h = tid & 3;
-    float d = 0.0f;
-    for (int c = 0; c < kD; ++c) d += sm.qorig[h][c] * hf(kt[t * kD + c]);
-    ts.lg[h][t] = d * (kLog2e * kRsqrtD);
+  uint4* kl = reinterpret_cast<uint4*>(sm.lut);             // [64 rows][16 pieces of 8 fp16]
+  uint4* vl = reinterpret_cast<uint4*>(&sm.pv[0][0]);
+  {
+    // piece i (8 channels of row i / 16); the two pieces of a thread: i0, i1
+    const int i0 = tid, i1 = tid + PL::NT;
+    const bool in0 = (i0 >> 4) < nt, in1 = (i1 >> 4) < nt;
+    uint4 ka = make_uint4(0u, 0u, 0u, 0u), kb = ka, va = ka, vb2 = ka;
+    if (in0) {
+      ka = reinterpret_cast<const uint4*>(kt)[i0];
+      va = reinterpret_cast<const uint4*>(vt)[i0];
+    }
+    if (in1) {
+      kb = reinterpret_cast<const uint4*>(kt)[i1];
+      vb2 = reinterpret_cast<const uint4*>(vt)[i1];
+    }
+    if (in0) {
+      kl[i0] = ka;
+      vl[i0] = va;
+    }
+    if (in1) {
+      kl[i1] = kb;
+      vl[i1] = vb2;
+    }
   }
   __syncthreads();
-  if (tid < 4) {
-    float M = -INFINITY;
-    for (int t = 0; t < nt; ++t) M = fmaxf(M, ts.lg[tid][t]);
-    float s = 0.0f;
-    for (int t = 0; t < nt; ++t) {
-      const float p = __builtin_amdgcn_exp2f(ts.lg[tid][t] - M);
-      ts.lg[tid][t] = p;
-      s += p;
+  // scores: thread (row t, channel block j of 16) sums its block for the 4
+  // heads; the 8 threads of a row are 8 neighbouring lanes (scalars only:
+  // small arrays here would be placed in memory)
+  {
+    const int t = tid >> 3, j = tid & 7;
+    uint4 k0 = make_uint4(0u, 0u, 0u, 0u), k1 = k0;
+    if (t < nt) {
+      k0 = kl[t * 16 + 2 * j];
+      k1 = kl[t * 16 + 2 * j + 1];
     }
-    ts.mx[tid] = M;
-    ts.sum[tid] = s;
+    auto dot4 = [](const float* q, uint32_t w0, uint32_t w1, float x) {
+      const float4 qv = *reinterpret_cast<const float4*>(q);
+      x = fmaf(qv.x, hf(uint16_t(w0 & 0xFFFFu)), x);
+      x = fmaf(qv.y, hf(uint16_t(w0 >> 16)), x);
+      x = fmaf(qv.z, hf(uint16_t(w1 & 0xFFFFu)), x);
+      return fmaf(qv.w, hf(uint16_t(w1 >> 16)), x);
+    };
+    auto dot16 = [&](int h) {
+      const float* q = &sm.qorig[h][16 * j];
+      float x = dot4(q, k0.x, k0.y, 0.0f);
+      x = dot4(q + 4, k0.z, k0.w, x);
+      x = dot4(q + 8, k1.x, k1.y, x);
+      return dot4(q + 12, k1.z, k1.w, x);
+    };
+    float d0 = dot16(0), d1 = dot16(1), d2 = dot16(2), d3 = dot16(3);
+#pragma unroll
+    for (int m = 1; m < 8; m <<= 1) {
+      d0 += __shfl_xor(d0, m);
+      d1 += __shfl_xor(d1, m);
+      d2 += __shfl_xor(d2, m);
+      d3 += __shfl_xor(d3, m);
+    }
+    if (t < nt && j == 0) {
+      constexpr float sc = kLog2e * kRsqrtD;
+      ts.lg[0][t] = d0 * sc;
+      ts.lg[1][t] = d1 * sc;
+      ts.lg[2][t] = d2 * sc;
+      ts.lg[3][t] = d3 * sc;
+    }
+  }
+  __syncthreads();
+  // softmax: wave h takes head h, lane t token t
+  if (wave < 4) {
+    const float x = lane < nt ? ts.lg[wave][lane] : -INFINITY;
+    float M = x;
+#pragma unroll
+    for (int m = 1; m < 64; m <<= 1) M = fmaxf(M, __shfl_xor(M, m));
+    const float p = lane < nt ? __builtin_amdgcn_exp2f(x - M) : 0.0f;
+    float ssum = p;
+#pragma unroll
+    for (int m = 1; m < 64; m <<= 1) ssum += __shfl_xor(ssum, m);
+    if (lane < nt) ts.lg[wave][lane] = p;
+    if (lane == 0) {
+      ts.mx[wave] = M;
+      ts.sum[wave] = ssum;
+    }
   }
   __syncthreads();
   const int h = tid >> 7, c = tid & 127;
+  const uint16_t* vrow = reinterpret_cast<const uint16_t*>(vl);
   float o = 0.0f;
-  if (tid < 4 * kD) {
-    for (int t = 0; t < nt; ++t) o += ts.lg[h][t] * hf(vt[t * kD + c]);
-    if (BASE != 0) {                       // into the rotated domain: H (sign . o) / 128
-      const uint32_t* sw = g.signs + (int64_t(layer) * g.n_kv_heads + kvh) * 4;
-      o = ((sw[c >> 5] >> (c & 31)) & 1u) ? -o : o;
-    }
+  for (int t = 0; t < nt; ++t) o = fmaf(ts.lg[h][t], hf(vrow[t * kD + c]), o);
+  if (BASE != 0) {                           // into the rotated domain: H (sign . o) / 128
+    const uint32_t* sw = g.signs + (int64_t(layer) * g.n_kv_heads + kvh) * 4;
+    o = ((sw[c >> 5] >> (c & 31)) & 1u) ? -o : o;
+    o = fwht_rows(o, ts.o) * (1.0f / 128.0f);
   }
-  if (BASE != 0) o = fwht_rows(o, ts.o) * (1.0f / 128.0f);
-  if (tid < 4 * kD) {
-    sm.tfin.o[h][c] = o;
-    if (c == 0) {
-      sm.tfin.m[h] = ts.mx[h];
-      sm.tfin.l[h] = ts.sum[h];
-    }
+  sm.tfin.o[h][c] = o;
+  if (c == 0) {
+    sm.tfin.m[h] = ts.mx[h];
+    sm.tfin.l[h] = ts.sum[h];
   }
 }
 
