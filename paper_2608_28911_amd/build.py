@@ -33,12 +33,11 @@ SOURCES = {
 REMARKS = "-Rpass-analysis=kernel-resource-usage"
 
 
-def _compile(cmd):
-    """Run one hipcc compile; return its kernels' resource remarks as
-    {kernel: {field: value}} and pass every other line of its output on."""
-    r = subprocess.run(cmd, capture_output=True, text=True)
+def parse_remarks(text):
+    """The compiler's kernel-resource-usage remarks in `text` as
+    ({kernel: {field: value}}, [the other lines])."""
     usage, name, rest = {}, None, []
-    for line in (r.stdout + r.stderr).splitlines():
+    for line in text.splitlines():
         if REMARKS not in line or "remark:" not in line:
             rest.append(line)
             continue
@@ -49,6 +48,19 @@ def _compile(cmd):
             usage[name] = {}
         elif name is not None:
             usage[name][key.strip()] = val.strip()
+    return usage, rest
+
+
+def spilling(usage):
+    """Kernels of `usage` that need private scratch memory."""
+    return sorted(k for k, u in usage.items() if u.get("ScratchSize [bytes/lane]", "0") != "0")
+
+
+def _compile(cmd):
+    """Run one hipcc compile; return its kernels' resource remarks and pass
+    every other line of its output on."""
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    usage, rest = parse_remarks(r.stdout + r.stderr)
     if rest:
         print("\n".join(rest), file=sys.stderr, flush=True)
     if r.returncode:
@@ -88,7 +100,7 @@ def build(verbose: bool = False, timeline: bool = False) -> str:
     with open(os.path.join(bdir, "resource_usage.txt"), "w") as fh:
         for k in sorted(usage):
             fh.write("%s %s\n" % (k, " ".join("%s=%s" % (f.replace(" ", ""), v) for f, v in usage[k].items())))
-    spills = sorted(k for k, u in usage.items() if u.get("ScratchSize [bytes/lane]", "0") != "0")
+    spills = spilling(usage)
     if not usage or spills:
         raise RuntimeError("kernels with private scratch (register spills): %s" % (spills or "no resource remarks"))
     tmp = lib_out + ".tmp%d" % os.getpid()
