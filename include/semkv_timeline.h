@@ -15,7 +15,9 @@
  *   10 workgroup partial merged, 11 partial stored, 12 split counter taken,
  *   13 the last workgroup's merge done; slots 14 and 15 count the wave's
  *   value-sum flushes and records; 16..18 inside the wave's first record:
- *   the next record's loads issued, scores done, softmax and flush done.
+ *   the next record's loads issued, scores done, softmax and flush done;
+ *   19..21 in the prologue: tables written, query value in hand, query runs
+ *   done.
  * Slots a launch did not write keep their previous contents (zero at load).
  */
 #ifndef SEMKV_TIMELINE_H

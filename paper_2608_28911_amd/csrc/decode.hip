@@ -70,7 +70,8 @@ __device__ inline void timeline_put(int ev, unsigned long long v) {
 // 3..7 the wave's 1st..5th record done, the next record's data stored in LDS
 // (a 6th and later overwrite 7), 8 the first record's arithmetic done (before
 // the next record's data is waited for), 16..18 inside the first record: the
-// next record's loads issued, scores done, softmax and flush done,
+// next record's loads issued, scores done, softmax and flush done, 19..21 in
+// the prologue: tables written, query value in hand, query runs done,
 // 9 the wave's records done, 10 workgroup partial merged, 11 partial stored,
 // 12 split counter taken, 13 the last workgroup's merge done; counts: 14 the
 // wave's value-sum flushes, 15 its records (both cleared at the wave's start)
@@ -1364,18 +1365,21 @@ __global__ __launch_bounds__((Plan<BASE, LH, LL, G>::NT)) void decode_kernel(Dec
     for (int k = 0; k < NTL; ++k)
       if (tid + k * NT < PL::LUTL / 4) d[PL::LUTH / 4 + tid + k * NT] = tl[k];
   }
+  SEMKV_STAMP(19);
   float xq = 0.0f;
   if (qt) {
     xq = hf(qbits);
     sm.qorig[h][c] = xq;
     if (BASE != 0) xq = ((qsign >> (c & 31)) & 1u) ? -xq : xq;
   }
+  SEMKV_STAMP(20);
   if (BASE != 0) xq = fwht_rows(xq, sm.ts.o);    // rotate: H (sign . q)
   if (qt) {
     sm.qf[h][c] = xq;
     if (c < kQPad - kD) sm.qf[h][kD + c] = 0.0f;
     query_runs(xq, h, c, sm);                   // the query the scores use: its runs
   }
+  SEMKV_STAMP(21);
   __syncthreads();
   build_aq<BASE, LH, G, 0, 0>(a, sm);
   build_aq<BASE, LL, G, 1, PL::GH::NG * PL::NCKH * 64>(a, sm);

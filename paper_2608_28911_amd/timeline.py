@@ -26,8 +26,9 @@ NAMES = {0: "start", 1: "tables + query operands", 2: "first record in LDS",
          9: "wave's records done", 10: "workgroup partial merged",
          11: "partial stored", 12: "split counter taken", 13: "last workgroup's merge done",
          16: "record 1: next record's loads issued", 17: "record 1: scores done",
-         18: "record 1: softmax and flush done"}
-ORDER = [0, 1, 2, 16, 17, 18, 8, 3, 4, 5, 6, 7, 9, 10, 11, 12, 13]
+         18: "record 1: softmax and flush done", 19: "prologue: tables written",
+         20: "prologue: query value in hand", 21: "prologue: query runs done"}
+ORDER = [0, 19, 20, 21, 1, 2, 16, 17, 18, 8, 3, 4, 5, 6, 7, 9, 10, 11, 12, 13]
 
 
 def main(argv=None):
