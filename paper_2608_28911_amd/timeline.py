@@ -1,6 +1,7 @@
 """Per-phase timeline of one decode launch, from the tracing build of the
 library (libsemkv_timeline.so: `python paper_2608_28911_amd/build.py
---timeline`; include/semkv_timeline.h).
+--timeline`, or `--timeline-fine` for the stamps inside the prologue and the
+first record; include/semkv_timeline.h).
 
     python -m paper_2608_28911_amd.timeline [--workload NAME] [--launches N]
 
@@ -35,6 +36,7 @@ def main(argv=None):
     ap = argparse.ArgumentParser()
     ap.add_argument("--workload", default="llama8b_kv_b1_t32768_affine")
     ap.add_argument("--launches", type=int, default=5, help="decode launches per layer (the last is shown)")
+    ap.add_argument("--save", default=None, help="also save the raw stamps (uint64 [4096][16][32]) to this .npy file")
     args = ap.parse_args(argv)
     if not os.path.exists(LIB_TIMELINE):
         raise SystemExit("libsemkv_timeline.so is not built: python paper_2608_28911_amd/build.py --timeline")
@@ -74,6 +76,8 @@ def main(argv=None):
 
     buf = np.zeros(WGS * WAVES * EVENTS, np.uint64)
     A.check(lib.semkv_timeline_read(buf.ctypes.data_as(ctypes.c_void_p), buf.nbytes), "semkv_timeline_read")
+    if args.save:
+        np.save(args.save, buf.reshape(WGS, WAVES, EVENTS))
     nsplit = cache.decode_splits() if hasattr(cache, "decode_splits") else None
     d = buf.reshape(WGS, WAVES, EVENTS).astype(np.int64)
     used = np.flatnonzero(d[:, 0, 0] > 0)
