@@ -17,7 +17,8 @@
  *   value-sum flushes and records; 16..18 inside the wave's first record:
  *   the next record's loads issued, scores done, softmax and flush done;
  *   19..21 in the prologue: tables written, query value in hand, query runs
- *   done.
+ *   done (16..21 only in the fine build, `build.py --timeline-fine`: they
+ *   delay the paths they measure).
  * Slots a launch did not write keep their previous contents (zero at load).
  */
 #ifndef SEMKV_TIMELINE_H

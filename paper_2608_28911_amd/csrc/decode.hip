@@ -66,6 +66,13 @@ __device__ inline void timeline_put(int ev, unsigned long long v) {
 #else
 #define SEMKV_STAMP(ev) ((void)0)
 #endif
+// the stamps inside the prologue and the first record (16..21) delay what they
+// measure: compiled in only with -DSEMKV_TIMELINE_FINE as well
+#if defined(SEMKV_TIMELINE) && defined(SEMKV_TIMELINE_FINE)
+#define SEMKV_STAMP_FINE(ev) SEMKV_STAMP(ev)
+#else
+#define SEMKV_STAMP_FINE(ev) ((void)0)
+#endif
 // 0 start, 1 tables and query operands built, 2 first record in LDS,
 // 3..7 the wave's 1st..5th record done, the next record's data stored in LDS
 // (a 6th and later overwrite 7), 8 the first record's arithmetic done (before
@@ -820,9 +827,7 @@ __device__ void run_pool(const DecodeArgs& a, Shared<PL>& sm, WaveState<PL::NGV>
     const int tile = first + stride * it;
     const bool more = it + 1 < count;
     if (more) load_tile<BASE, LH, LL, G>(a.g, unit, tile + stride, nt0, R, lane);
-#ifdef SEMKV_TIMELINE
-    if (it == 0) SEMKV_STAMP(16);
-#endif
+    if (it == 0) SEMKV_STAMP_FINE(16);
     const int ptile = POOL ? tile - nt0 : tile;
     const uint8_t* kmeta = rec + 2 * Tr::TB;
     const uint8_t* vmeta = kmeta + Ge::MB;
@@ -914,9 +919,7 @@ __device__ void run_pool(const DecodeArgs& a, Shared<PL>& sm, WaveState<PL::NGV>
 #pragma unroll
       for (int blk = 0; blk < 4; ++blk) lg[blk] = 16 * blk + n < nvalid ? lg[blk] : -INFINITY;
     }
-#ifdef SEMKV_TIMELINE
-    if (it == 0) SEMKV_STAMP(17);
-#endif
+    if (it == 0) SEMKV_STAMP_FINE(17);
     // ---- online softmax (base 2) for head r over this record's 64 tokens,
     // rescaled lazily: the reference maximum st.m moves only when a score
     // passes it by more than 8 (weights up to 2^8 fit the fixed-point range),
@@ -984,9 +987,7 @@ __device__ void run_pool(const DecodeArgs& a, Shared<PL>& sm, WaveState<PL::NGV>
     st.l += lsum;
 #pragma unroll
     for (int i = 0; i < NGV; ++i) st.z[i] += zadd[i];
-#ifdef SEMKV_TIMELINE
-    if (it == 0) SEMKV_STAMP(18);
-#endif
+    if (it == 0) SEMKV_STAMP_FINE(18);
 
     // ---- values: C[(h, byte)][channel] += weights (tokens) x V codes, one
     // value group's int8 weights (byte s of rint(w qw) in row 4r + s) at a time
@@ -1365,21 +1366,21 @@ __global__ __launch_bounds__((Plan<BASE, LH, LL, G>::NT)) void decode_kernel(Dec
     for (int k = 0; k < NTL; ++k)
       if (tid + k * NT < PL::LUTL / 4) d[PL::LUTH / 4 + tid + k * NT] = tl[k];
   }
-  SEMKV_STAMP(19);
+  SEMKV_STAMP_FINE(19);
   float xq = 0.0f;
   if (qt) {
     xq = hf(qbits);
     sm.qorig[h][c] = xq;
     if (BASE != 0) xq = ((qsign >> (c & 31)) & 1u) ? -xq : xq;
   }
-  SEMKV_STAMP(20);
+  SEMKV_STAMP_FINE(20);
   if (BASE != 0) xq = fwht_rows(xq, sm.ts.o);    // rotate: H (sign . q)
   if (qt) {
     sm.qf[h][c] = xq;
     if (c < kQPad - kD) sm.qf[h][kD + c] = 0.0f;
     query_runs(xq, h, c, sm);                   // the query the scores use: its runs
   }
-  SEMKV_STAMP(21);
+  SEMKV_STAMP_FINE(21);
   __syncthreads();
   build_aq<BASE, LH, G, 0, 0>(a, sm);
   build_aq<BASE, LL, G, 1, PL::GH::NG * PL::NCKH * 64>(a, sm);
