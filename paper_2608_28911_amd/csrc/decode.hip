@@ -530,12 +530,36 @@ template <int CTRL>
 __device__ inline float dpp(float x) {
   return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), CTRL, 0xF, 0xF, false));
 }
-// reductions over the 16 lanes of a row (row_ror 8, 4, 2, 1)
+// reductions over the 16 lanes of a row (row_ror 8, 4, 2, 1).  The maximum
+// is four DPP maxima written out: fmaxf of a DPP move costs three
+// instructions a step (the move, a quieting max of the moved value that the
+// IEEE-mode maxNum contract asks of an operand not known to be canonical, the
+// max), and the values here are never NaN.  Every DPP read of a register
+// written by the VALU instruction just before it needs two wait states, which
+// the compiler does not insert around inline assembly: hence the s_nop 1
+// before each (and after the last, for a DPP read that may follow).
+// Called with the whole wave active.
 __device__ inline float row_max16(float x) {
-  x = fmaxf(x, dpp<0x128>(x));
-  x = fmaxf(x, dpp<0x124>(x));
-  x = fmaxf(x, dpp<0x122>(x));
-  return fmaxf(x, dpp<0x121>(x));
+  float r;
+  __asm__("s_nop 1\n\t"
+          "v_max_f32_dpp %0, %1, %1 row_ror:8 row_mask:0xf bank_mask:0xf\n\t"
+          "s_nop 1\n\t"
+          "v_max_f32_dpp %0, %0, %0 row_ror:4 row_mask:0xf bank_mask:0xf\n\t"
+          "s_nop 1\n\t"
+          "v_max_f32_dpp %0, %0, %0 row_ror:2 row_mask:0xf bank_mask:0xf\n\t"
+          "s_nop 1\n\t"
+          "v_max_f32_dpp %0, %0, %0 row_ror:1 row_mask:0xf bank_mask:0xf\n\t"
+          "s_nop 1"
+          : "=&v"(r) : "v"(x));
+  return r;
+}
+// max of four values that are never NaN (no quieting of operands)
+__device__ inline float max4(float a, float b, float c, float d) {
+  float r;
+  __asm__("v_max3_f32 %0, %1, %2, %3\n\t"
+          "v_max_f32 %0, %0, %4"
+          : "=&v"(r) : "v"(a), "v"(b), "v"(c), "v"(d));
+  return r;
 }
 __device__ inline float row_sum16(float x) {
   x += dpp<0x128>(x);
@@ -924,8 +948,7 @@ __device__ void run_pool(const DecodeArgs& a, Shared<PL>& sm, WaveState<PL::NGV>
     // rescaled lazily: the reference maximum st.m moves only when a score
     // passes it by more than 8 (weights up to 2^8 fit the fixed-point range),
     // or on the wave's first record
-    float mt = fmaxf(fmaxf(lg[0], lg[1]), fmaxf(lg[2], lg[3]));
-    mt = row_max16(mt);
+    const float mt = row_max16(max4(lg[0], lg[1], lg[2], lg[3]));
     const bool grow = !(mt <= st.m + 8.0f);
     const float m_new = grow ? mt : st.m;
     const float alpha = grow ? __builtin_amdgcn_exp2f(st.m - m_new) : 1.0f;
