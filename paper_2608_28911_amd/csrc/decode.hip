@@ -663,8 +663,22 @@ __device__ inline float comb3(const int4v& c) {
 }
 // the same for one product of a score: |row 0| < 2^16, |row 1| < 2^17, so
 // the integer sum stays below 2^31
+// bits [OFF, OFF+7) of x as one instruction (left to itself the compiler
+// emits a shift and a mask).  Its operand must not come straight from a
+// matrix instruction: the compiler does not insert the wait states a read of
+// an MFMA result needs before inline assembly.
+template <int OFF>
+__device__ inline uint32_t bits7(uint32_t x) {
+  uint32_t r;
+  __asm__("v_bfe_u32 %0, %1, %2, 7" : "=v"(r) : "v"(x), "i"(OFF));
+  return r;
+}
 __device__ inline float comb3_score(const int4v& c) {
-  return float((c[0] << 14) + (c[1] << 7) + c[2]);
+  // two shift-adds; the empty statement keeps the compiler from re-associating
+  // them into two shifts and a three-way add
+  int t = (c[0] << 7) + c[1];
+  __asm__("" : "+v"(t));
+  return float((t << 7) + c[2]);
 }
 
 // ---------------------------------------------------------- staging ----
@@ -1028,9 +1042,9 @@ __device__ void run_pool(const DecodeArgs& a, Shared<PL>& sm, WaveState<PL::NGV>
             // of w qw + 1.5 2^23 (one rounding of the exact sum)
             const uint32_t q = __float_as_uint(fmaf(wv[blk][gv][pl], st.qw, 12582912.0f));
             uint8_t* w = pvw + pvwr[blk] + pl;
-            w[0] = uint8_t((q >> 14) & 127u);
-            w[16] = uint8_t((q >> 7) & 127u);
-            w[32] = uint8_t(q & 127u);
+            w[0] = uint8_t(bits7<14>(q));
+            w[16] = uint8_t(bits7<7>(q));
+            w[32] = uint8_t(bits7<0>(q));
           }
         // weights written above by other lanes of this wave are read below
         __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
