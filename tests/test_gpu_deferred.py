@@ -98,6 +98,14 @@ def test_generation_on_the_level_grid(levels):
     run_generation(cfgw, 130, 64 + 3, check_steps={0, 64, 66}, flush=True)
 
 
+def test_generation_with_a_partial_last_round():
+    """8 kv heads and a 1100-token prompt at 26 %: two workgroups per unit
+    and a last round of two tiles, one of them in the workgroup that also
+    takes the fp16 tail of the generated tokens."""
+    cfgw = get_config(3, n_layers=1, batch=1, n_kv_heads=8, n_q_heads=32)
+    run_generation(cfgw, 1100, 6, check_steps={0, 5}, units=[(0, 0, 0), (0, 0, 5)])
+
+
 def test_generation_g32():
     cfgw = get_config(3, n_layers=1, batch=1, n_kv_heads=1, n_q_heads=4, group=32)
     run_generation(cfgw, 64, 64 * 3, check_steps={10, 100, 191})

@@ -89,6 +89,24 @@ def test_every_fill_of_a_pools_last_record(base, lh, ll, G):
             raise AssertionError("last record with %d valid slots: %s" % (n, e)) from None
 
 
+@pytest.mark.parametrize("base,lh,ll,G", [("affine", 6, 5, 128), ("affine", 6, 5, 32), ("tq", 4, 3, 128),
+                                          ("rot_affine", 6, 5, 128), ("affine", 8, 7, 128), ("affine", 3, 2, 128)])
+@pytest.mark.parametrize("T,r", [(1100, (26, 100)), (576, (1, 1)), (2200, (1, 1)), (1100, (0, 1)),
+                                 (2200, (1, 2)), (6400, (26, 100))])
+def test_partial_last_round(base, lh, ll, G, T, r):
+    """8 kv heads, so up to 32 workgroups per unit: with the split count
+    the host picks (at most a unit's tiles / 8), these prompts leave a last
+    round of 1 to nsplit tiles after whole rounds of the 8 waves of every
+    workgroup -- its tiles in the low pool (1100 at 26 % and 0 %, 2200 at
+    1/2, 6400) or in the high pool (r = 1: 576, 2200) -- so a few waves hold
+    one record more than the rest."""
+    kw = dict(L_hi=lh, L_lo=ll) if base != "tq" else {}
+    cfgw = get_config(0 if base != "tq" else 4, base=base, group=G, r_num=r[0], r_den=r[1], batch=1,
+                      n_kv_heads=8, n_q_heads=32, n_layers=1, **kw)
+    cache, flags = _check_prefill(cfgw, T, units=[(0, 0, 0), (0, 0, 7)])
+    _check_decode(cache, cfgw, T, flags, [0])
+
+
 def _multi_chunk_scores(T, seed):
     """Three sequences: integer scores 0..3 (ties across every chunk
     boundary), all equal, and normal draws with +0, -0, +inf and -inf."""
