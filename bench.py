@@ -142,9 +142,11 @@ def indicators(cache, K, gen, dev, reps=3):
 def cpu_baseline(cfgw, seconds):
     """The oracle, as it stands, on a bounded sample of the headline workload:
     the (layer, kv head) units of sequence 0 at its context length, each
-    quantized + packed (OpenMP across rows), dequantized in fp64, then the
-    decode attention of all sampled units at once (OpenMP across units, every
-    host core).  Scaled to the units of one decode step."""
+    quantized + packed (OpenMP across rows), dequantized in fp64 (the
+    oracle's dequantization runs on one thread), then the decode attention of
+    all sampled units at once (OpenMP across units, every host core).  Scaled
+    to the units of one decode step; the single-thread figure is one unit's
+    dequantization and attention on one thread."""
     from oracle import oracle as O
     from workloads import synth
     T = cfgw.prompt_len
@@ -175,11 +177,12 @@ def cpu_baseline(cfgw, seconds):
     t_attn = time.perf_counter() - t0
     per_unit = (t_deq + t_attn) / len(units)
     units_per_step = cfgw.n_layers * cfgw.batch * cfgw.n_kv_heads
-    # one thread: the attention of one unit at this context
+    # one thread: one unit's dequantization (its share of t_deq, which ran on
+    # one thread) and its attention at this context
     O.set_threads(1)
     t0 = time.perf_counter()
     O.attention(*units[0])
-    t_one = time.perf_counter() - t0
+    t_one = time.perf_counter() - t0 + t_deq / len(units)
     O.set_threads(threads)
     # the indicators (Sec. 3.3) on 1024 tokens: delta-norm over 5 hidden states
     # of width 4096, key-norm over every layer and kv head (single thread)
@@ -204,8 +207,8 @@ def cpu_baseline(cfgw, seconds):
         "nproc": os.cpu_count(),
         "affinity_cpus": affinity,
         "kind": "oracle",
-        "sample": "%d (layer, kv head) units of sequence 0 at T=%d: fp64 dequantize (%.3f s) + softmax "
-                  "attention of 4 query heads, all units in one OpenMP region over %d threads (%.3f s); "
+        "sample": "%d (layer, kv head) units of sequence 0 at T=%d: fp64 dequantize, one thread (%.3f s), + "
+                  "softmax attention of 4 query heads, all units in one OpenMP region over %d threads (%.3f s); "
                   "scaled to %d units per decoded token" % (len(units), T, t_deq, threads, t_attn, units_per_step),
         "quantize_pack_gbps": q_bytes / t_quant / 1e9,
         "quantize_pack_cores": threads,
