@@ -112,22 +112,43 @@ int64_t decode_slots(const semkv_config& k) {
   return slots;
 }
 
+// Records on the busiest SIMD when a unit's nt tiles are dealt to ns
+// workgroups of nw waves: slot s = wave * ns + split takes tiles s, s +
+// stride, ... (stride = ns * nw), so slot s holds full + (s < left) tiles
+// (full = nt div stride, left = nt mod stride); waves w and w + nw/2 share a
+// SIMD, and the SIMD of split 0's waves 0 and nw/2 holds the most.
+int64_t busiest_simd(int64_t nt, int64_t ns, int nw) {
+  const int64_t stride = ns * nw, full = nt / stride, left = nt % stride;
+  return 2 * full + (left > 0) + (left > ns * (nw / 2));
+}
+
 // Decode split plan: the tiles of each (sequence, kv head) unit, high pool
 // then low pool, are dealt to nsplit workgroups (tile u to wave slot u mod
-// nsplit * waves), so that the whole grid is resident at once and every wave
-// has a record.  The fp16 tail rides with the last workgroup.  0: nothing
-// cached.
-// A launch of `layers` layers plans over all their units together.
+// nsplit * waves), at most as many workgroups as are resident at once: of
+// those split counts, the one that leaves the busiest SIMD the fewest
+// records, and of equals the largest (the most compute units at work; a short
+// context then leaves some waves without a record rather than giving one
+// SIMD a record more).  The fp16 tail rides with the last workgroup.  0:
+// nothing cached.  A launch of `layers` layers plans over all their units
+// together.
 int plan(const semkv_cache* c, int n_tail, int layers = 1) {
   const int64_t nt = (c->n_hi + kSlots - 1) / kSlots + (c->n_lo + kSlots - 1) / kSlots;
   if (nt == 0) return n_tail > 0 ? 1 : 0;
   const int64_t units = int64_t(c->cfg.batch) * c->cfg.n_kv_heads * layers;
-  int64_t ns = decode_slots(c->cfg) / units;
+  int64_t ns_max = decode_slots(c->cfg) / units;
   const int nw = decode_waves(c->cfg.base, c->cfg.L_hi, c->cfg.L_lo, c->cfg.group);
-  if (ns > nt / nw) ns = nt / nw;
-  if (ns > kMaxSplits / layers) ns = kMaxSplits / layers;
-  if (ns < 1) ns = 1;
-  return int(ns);
+  if (ns_max > nt) ns_max = nt;                  // every workgroup holds a tile
+  if (ns_max > kMaxSplits / layers) ns_max = kMaxSplits / layers;
+  if (ns_max < 1) ns_max = 1;
+  int64_t best = ns_max, best_load = busiest_simd(nt, ns_max, nw);
+  for (int64_t ns = ns_max - 1; ns >= 1; --ns) {
+    const int64_t load = busiest_simd(nt, ns, nw);
+    if (load < best_load) {
+      best = ns;
+      best_load = load;
+    }
+  }
+  return int(best);
 }
 
 // workspace: [layer][b][kvh] uint32 counters, one per 256-byte line, then the
